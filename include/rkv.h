@@ -1,0 +1,212 @@
+/*
+ * rkv.h - layer-routed KV-cache eviction on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of librkv.so.  It executes a static layer-wise eviction plan in the
+ * sense of "Exploring a Layer-Wise Design Space for KV Cache Eviction":
+ * Section 3.1, Eq. 1 defines the plan as, for every layer and phase
+ * (prefill, decode), an operator r and a nominal retained-token capacity b;
+ * Section 3.3, Eq. 3 defines how a fixed total capacity is split across
+ * layers; Section 3.4 defines the adapter interface (a prompt-compression
+ * handler and an incremental-update handler per operator, a plan loaded once).
+ *
+ * Operators: FULL (no eviction), STREAMING (StreamingLLM: attention sinks plus
+ * recent tokens), SNAPKV (observation-window scoring with max-pooling),
+ * H2O (accumulated-attention heavy hitters plus recent tokens).  Section 2.1
+ * names these rule families; their arithmetic is stated at each entry point.
+ *
+ * Conventions shared by every entry point
+ *  - Every function returns an rkv_status; RKV_OK is 0.  On failure a message
+ *    is available from rkv_last_error() (thread-local, valid until the next
+ *    rkv call on the same thread) and no output buffer has been written.
+ *  - Device buffers are owned by the caller (any allocator), as is the stream.
+ *    The library allocates no device memory in rkv_prefill_evict or
+ *    rkv_decode_step, never frees caller memory and never synchronises the
+ *    stream: results are valid once the caller's stream has been synchronised.
+ *  - "stream" is a hipStream_t passed as void* (NULL = the null stream).
+ *  - bf16 tensors are IEEE bfloat16, row-major, densely packed, with the
+ *    shapes stated below.  Positions are token indices within the sequence.
+ *  - A plan is immutable after creation and may be shared by concurrent
+ *    calls on different streams, each with its own workspace.
+ */
+#ifndef RKV_H
+#define RKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define RKV_VERSION 1
+
+typedef enum {
+  RKV_OK = 0,
+  RKV_ERR_INVALID_ARG = 1, /* null pointer, negative size, unknown enum value */
+  RKV_ERR_SHAPE = 2,       /* inconsistent shape (e.g. Hq not a multiple of Hkv, window > L) */
+  RKV_ERR_PLAN = 3,        /* plan violates Eq. 1 constraints (operator not valid in that phase) */
+  RKV_ERR_UNSUPPORTED = 4, /* valid request this build does not implement (e.g. head_dim != 128) */
+  RKV_ERR_WORKSPACE = 5,   /* workspace missing, too small or misaligned */
+  RKV_ERR_HIP = 6,         /* a HIP runtime call failed; rkv_last_error() has hipGetErrorString */
+  RKV_ERR_DEVICE = 7       /* a kernel reported an internal failure (see rkv_prefill_check) */
+} rkv_status;
+
+/* Operators (Section 2.1 rule families; Section 3.1 r_{l,phi} values). */
+typedef enum { RKV_FULL = 0, RKV_STREAMING = 1, RKV_SNAPKV = 2, RKV_H2O = 3 } rkv_rule;
+typedef enum { RKV_PHASE_PREFILL = 0, RKV_PHASE_DECODE = 1 } rkv_phase;
+/* Score transforms T of Section 3.3: identity (attention entropy) or a cap at the
+ * across-layer 95th percentile (PPL degradation). */
+typedef enum { RKV_T_IDENTITY = 0, RKV_T_PPL_CAP = 1 } rkv_transform;
+
+/* One row of the plan Pi of Eq. 1: operator and nominal capacity per phase.
+ * Budgets are ignored for FULL. */
+typedef struct {
+  int32_t rule_prefill, budget_prefill;
+  int32_t rule_decode, budget_decode;
+} rkv_layer;
+
+/* Operator parameters shared by all layers of a plan.
+ *  window       w: number of observation-window queries (the last w prompt positions).
+ *  pool_kernel  odd max-pool width used by SNAPKV (stride 1, clipped to the prefix).
+ *  n_sink       StreamingLLM sink count; s0 = min(n_sink, b) first positions are kept.
+ *  recent_num/recent_den  H2O keeps r = floor(b * num / den) most recent positions. */
+typedef struct {
+  int32_t window, pool_kernel, n_sink, recent_num, recent_den;
+} rkv_params;
+
+/* Tensor shape of one call: B sequences of seq_len positions, Hq query heads,
+ * Hkv KV heads (Hq % Hkv == 0; query head hq reads KV head hq / (Hq/Hkv)), head_dim d. */
+typedef struct {
+  int32_t batch, seq_len, n_q_heads, n_kv_heads, head_dim;
+} rkv_shape;
+
+typedef struct rkv_plan rkv_plan;
+
+/* Per-layer device pointers of one prefill call (host arrays of n_layers pointers).
+ *  q_win[l]     bf16 [B, Hq, w, d]   queries of positions L-w..L-1 (post-RoPE); may be NULL
+ *               for layers whose prefill operator does not score (FULL, STREAMING).
+ *  k[l], v[l]   bf16 [B, Hkv, L, d]  the prompt's keys and values.
+ *  k_out[l], v_out[l]  bf16 [B, Hkv, n_l, d]  compacted cache, n_l = retained count
+ *               (rkv_plan_retained_counts); row m holds position idx_out[l][..., m].
+ *  idx_out[l]   int32 [B, Hkv, n_l]  retained positions, strictly ascending.
+ *  score_out    NULL, or array whose entries are NULL or fp32 [B, Hkv, L]: the score each
+ *               candidate position was ranked by (defined on the operator's candidate
+ *               range [0, cand_end); other entries unspecified).  Debug/test output.
+ *  acc_out      NULL, or array whose entries are NULL or fp32 [B, Hkv, n_l]: for scoring
+ *               operators the unpooled group-mean window score of each retained position
+ *               (seeds H2O's decode-phase accumulated score); 0 for FULL / STREAMING. */
+typedef struct {
+  const void* const* q_win;
+  const void* const* k;
+  const void* const* v;
+  void* const* k_out;
+  void* const* v_out;
+  int32_t* const* idx_out;
+  float* const* score_out;
+  float* const* acc_out;
+} rkv_prefill_io;
+
+/* Decode-phase cache of every layer with a decode operator (entries of FULL layers may be NULL).
+ *  k_cache[l], v_cache[l]  bf16 [B, Hkv, C_l, d], C_l = the layer's retained decode count.
+ *  pos[l]   int32 [B, Hkv, C_l]  position held by each slot (slot order is arbitrary).
+ *  acc[l]   fp32  [B, Hkv, C_l]  H2O accumulated attention of each slot. */
+typedef struct {
+  void* const* k_cache;
+  void* const* v_cache;
+  int32_t* const* pos;
+  float* const* acc;
+} rkv_decode_state;
+
+/* One decode step's new token per layer:
+ *  q[l] bf16 [B, Hq, d]; k[l], v[l] bf16 [B, Hkv, d];
+ *  victim_out NULL or entries NULL / int32 [B, Hkv]: slot overwritten by the new token, or -1
+ *  when the new token itself was the one evicted. */
+typedef struct {
+  const void* const* q;
+  const void* const* k;
+  const void* const* v;
+  int32_t* const* victim_out;
+} rkv_decode_input;
+
+/* Section 3.3, Eq. 3: split `total` retained positions over n_layers layers.
+ * scores[n_layers] (host) -> T(scores) (transform), shift by (-min + 1e-6) if min <= 0,
+ * weights w_l = T_l / sum T, provisional b_l = total * w_l; layers below b_min are fixed
+ * at b_min and the rest is re-shared by weight until none falls below; then floor and hand
+ * the residual units to the largest fractional remainders (equal remainders: lower layer).
+ * budgets_out[n_layers] (host).  Host only, no GPU needed.
+ * Errors: RKV_ERR_INVALID_ARG for null pointers, n_layers < 1, b_min < 0,
+ * total < n_layers * b_min, non-finite scores or an unknown transform. */
+int rkv_allocate_budgets(const double* scores, int32_t n_layers, int32_t transform, int64_t total,
+                         int32_t b_min, int32_t* budgets_out);
+
+/* Section 3.1 (Eq. 1) and 3.4: validate and freeze a plan.  Host only.
+ * Operators valid in prefill: FULL, STREAMING, SNAPKV, H2O.  In decode: FULL, STREAMING, H2O
+ * (SNAPKV compresses the prompt only -> RKV_ERR_PLAN).  Budgets must be >= 0 (>= 2 for a
+ * decode H2O layer, >= 1 for decode STREAMING); window >= 1, pool_kernel odd >= 1,
+ * n_sink >= 0, 0 <= recent_num <= recent_den, recent_den >= 1.  *out receives a new plan. */
+int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params* params, rkv_plan** out);
+void rkv_plan_destroy(rkv_plan* plan);
+int rkv_plan_num_layers(const rkv_plan* plan, int32_t* n_layers);
+
+/* Retained positions per layer for a prompt of seq_len tokens in `phase`:
+ * FULL -> seq_len; otherwise min(budget, seq_len).  counts_out[n_layers] (host). */
+int rkv_plan_retained_counts(const rkv_plan* plan, int32_t phase, int32_t seq_len, int32_t* counts_out);
+
+/* Bytes of device workspace rkv_prefill_evict needs for `shape` (256-byte aligned base). */
+int rkv_prefill_workspace_size(const rkv_plan* plan, const rkv_shape* shape, size_t* bytes);
+
+/* Prefill prompt compression of every layer (the prompt-compression handler of Section 3.4),
+ * enqueued on `stream`.  Per sequence, layer and KV head h with G = Hq / Hkv:
+ *   A[hq, j] = sum_{i<w} softmax_j( Q[hq,i] . K[h,j] / sqrt(d) ), row i at position L-w+i
+ *              seeing keys j <= L-w+i (causal inside the window);
+ *   SNAPKV:   S[h,j] = mean_g maxpool_j(A[hG+g, .]) over the prefix [0, L-w);
+ *             keep top-(b-w) of S plus the window [L-w, L) (b <= w: the last b positions);
+ *   H2O:      S[h,j] = mean_g A[hG+g, j]; r = floor(b*num/den);
+ *             keep top-(b-r) of S over [0, L-r) plus [L-r, L);
+ *   STREAMING: keep [0, min(n_sink,b)) plus the last b - min(n_sink,b) positions;
+ *   FULL, or b >= L: keep everything.
+ * Top-k order is (score descending, position ascending) on fp32 scores.  K/V rows are
+ * copied bit-exactly into k_out / v_out in ascending position order.
+ * ws: caller-owned device workspace of at least rkv_prefill_workspace_size bytes, 256-byte
+ * aligned; one workspace per concurrently executing call.
+ * Errors: RKV_ERR_INVALID_ARG (null io / pointer for a layer that needs it), RKV_ERR_SHAPE,
+ * RKV_ERR_UNSUPPORTED (head_dim != 128, G * ceil(w/32) > 8, seq_len > 2^24),
+ * RKV_ERR_WORKSPACE, RKV_ERR_HIP (launch failure). */
+int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_prefill_io* io,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* Synchronously read the device status word a previous rkv_prefill_evict left in `ws`
+ * (0 = clean; nonzero = a kernel gave up on a bounded wait and its outputs are invalid).
+ * Synchronises the null stream's view of ws via a blocking copy; for tests and debugging. */
+int rkv_prefill_check(const void* ws, size_t ws_bytes, int32_t* status_out);
+
+/* One decode step (the incremental-update handler of Section 3.4) for every layer, on `stream`.
+ * shape->seq_len is ignored; `position` is the new token's position p.
+ * H2O: per (sequence, layer, KV head) the new key joins the C cached ones; each of the G query
+ *   heads takes softmax(q . k / sqrt(d)) over the C+1 entries; every entry's acc grows by the
+ *   group mean (new entry from 0, fp32); among entries with pos <= p - r
+ *   (r = floor(C*num/den)) the smallest acc is evicted, ties to the smallest position;
+ *   the new token (k, v, pos = p, acc) takes the victim's slot.
+ * STREAMING: the slot with the smallest position >= n_sink is replaced by the new token.
+ * FULL: the layer is skipped.
+ * Errors: as rkv_prefill_evict; RKV_ERR_SHAPE if position < C. */
+int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_decode_state* state,
+                    const rkv_decode_input* input, int32_t position, void* stream);
+
+/* Kernel timing for benchmarks and tests.  rkv_profile_enable(stage) makes every following
+ * launch of that stage record a pair of HIP events around it on the caller's stream
+ * (stage: 0 counter reset, 1 scoring, 2 selection, 3 gather, 4 decode; -1 disables).
+ * Up to 4096 launches are kept.  rkv_profile_read synchronises on the recorded events,
+ * returns the number of launches and their summed duration in milliseconds, and clears
+ * the record.  Host-side state shared by all threads. */
+int rkv_profile_enable(int32_t stage);
+int rkv_profile_read(int32_t* n_launches, double* total_ms);
+
+const char* rkv_last_error(void);
+int rkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RKV_H */

@@ -1,0 +1,497 @@
+// Host side of librkv: errors, the capacity allocator, plan validation, argument
+// checking, workspace layout and launch orchestration.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <mutex>
+#include <cmath>
+#include <cstring>
+#include <new>
+#include <numeric>
+
+#include "rkv_internal.h"
+
+namespace {
+thread_local std::string g_error;
+
+size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+bool rule_valid(int32_t r) { return r >= RKV_FULL && r <= RKV_H2O; }
+
+// Retained positions and selection layout of one layer (prefill phase).
+struct Layout {
+  int32_t n_keep, cand_end, k_sel, forced_lo, forced_hi, all, scored;
+};
+
+Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L) {
+  Layout o{};
+  const int32_t b = ly.budget_prefill;
+  o.scored = (ly.rule_prefill == RKV_SNAPKV || ly.rule_prefill == RKV_H2O) ? 1 : 0;
+  if (ly.rule_prefill == RKV_FULL || b >= L) {
+    o.n_keep = L; o.all = 1; o.cand_end = 0; o.k_sel = 0; o.forced_lo = 0; o.forced_hi = L;
+    return o;
+  }
+  o.n_keep = b;
+  switch (ly.rule_prefill) {
+    case RKV_STREAMING: {
+      int32_t s0 = std::min(p.n_sink, b);
+      o.cand_end = s0; o.k_sel = s0; o.forced_lo = L - (b - s0); o.forced_hi = L;
+      break;
+    }
+    case RKV_SNAPKV:
+      if (b <= p.window) { o.cand_end = 0; o.k_sel = 0; o.forced_lo = L - b; }
+      else { o.cand_end = L - p.window; o.k_sel = b - p.window; o.forced_lo = L - p.window; }
+      o.forced_hi = L;
+      break;
+    case RKV_H2O: {
+      int32_t r = (int32_t)(((int64_t)b * p.recent_num) / p.recent_den);
+      o.cand_end = L - r; o.k_sel = b - r; o.forced_lo = L - r; o.forced_hi = L;
+      break;
+    }
+    default: break;
+  }
+  return o;
+}
+
+int validate_shape(const rkv_shape* s) {
+  if (!s) return rkv::fail(RKV_ERR_INVALID_ARG, "shape is null");
+  if (s->batch < 1 || s->seq_len < 1 || s->n_q_heads < 1 || s->n_kv_heads < 1 || s->head_dim < 1)
+    return rkv::fail(RKV_ERR_SHAPE, "shape fields must be positive");
+  if (s->n_q_heads % s->n_kv_heads)
+    return rkv::fail(RKV_ERR_SHAPE, "n_q_heads must be a multiple of n_kv_heads");
+  if (s->head_dim != rkv::kHeadDim)
+    return rkv::fail(RKV_ERR_UNSUPPORTED, "head_dim must be 128");
+  if (s->seq_len > (1 << 24)) return rkv::fail(RKV_ERR_UNSUPPORTED, "seq_len above 2^24");
+  return RKV_OK;
+}
+
+int row_tiles(const rkv_params& p, const rkv_shape* s) {
+  int G = s->n_q_heads / s->n_kv_heads;
+  return G * ((p.window + 31) / 32);
+}
+
+// Scoring row tiles padded to a supported kernel instantiation (4 or 8 tiles of 32 rows).
+int kernel_row_tiles(int nt) { return nt <= 4 ? 4 : 8; }
+
+struct Group {
+  int l0, l1, n_scored;
+};
+
+std::vector<Group> layer_groups(const rkv_plan* plan, int32_t L) {
+  std::vector<Group> g;
+  int n = (int)plan->layers.size();
+  for (int l0 = 0; l0 < n; l0 += rkv::kMaxLayersPerLaunch) {
+    int l1 = std::min(n, l0 + rkv::kMaxLayersPerLaunch);
+    int sc = 0;
+    for (int l = l0; l < l1; ++l) sc += prefill_layout(plan->layers[l], plan->params, L).scored;
+    g.push_back({l0, l1, sc});
+  }
+  return g;
+}
+
+size_t group_workspace(const rkv_plan* plan, const rkv_shape* s, const Group& g) {
+  const int L = s->seq_len;
+  const int G = s->n_q_heads / s->n_kv_heads;
+  const int nt = kernel_row_tiles(row_tiles(plan->params, s));
+  const int n_heads = s->batch * g.n_scored * s->n_kv_heads;
+  const int n_chunks = (L + rkv::kChunk - 1) / rkv::kChunk;
+  return rkv::prefill_workspace_layout(n_heads, n_chunks, nt * 32, L, G, plan->params.pool_kernel / 2, true)
+      .total;
+}
+
+}  // namespace
+
+namespace rkv {
+
+namespace {
+std::mutex g_prof_mu;
+int g_prof_stage = -1;
+std::vector<hipEvent_t> g_prof_events;  // begin/end pairs
+constexpr size_t kMaxProfiled = 4096;
+}  // namespace
+
+void profile_mark(int stage, bool end, void* stream) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (stage != g_prof_stage) return;
+  if (!end && g_prof_events.size() >= 2 * kMaxProfiled) return;
+  if (end && g_prof_events.size() % 2 == 0) return;  // begin was dropped
+  hipEvent_t e;
+  if (hipEventCreate(&e) != hipSuccess) return;
+  if (hipEventRecord(e, reinterpret_cast<hipStream_t>(stream)) != hipSuccess) {
+    (void)hipEventDestroy(e);
+    return;
+  }
+  g_prof_events.push_back(e);
+}
+
+int fail(int status, const std::string& msg) {
+  g_error = msg;
+  return status;
+}
+
+void clear_error() { g_error.clear(); }
+
+PrefillWorkspace prefill_workspace_layout(int n_heads, int n_chunks, int rows, int seq_len, int group,
+                                          int pool_half, bool want_unpooled) {
+  PrefillWorkspace w{};
+  size_t off = 0;
+  w.counters = off;
+  off = round_up(off + sizeof(uint32_t) * (2 + 2 * (size_t)n_heads), 256);
+  w.stats = off;
+  off = round_up(off + sizeof(float) * 2 * (size_t)n_heads * n_chunks * rows, 256);
+  w.headstat = off;
+  off = round_up(off + sizeof(float) * 2 * (size_t)n_heads * rows, 256);
+  w.S = off;
+  off = round_up(off + sizeof(float) * (size_t)n_heads * seq_len, 256);
+  w.Su = off;
+  if (want_unpooled) off = round_up(off + sizeof(float) * (size_t)n_heads * seq_len, 256);
+  w.edge = off;
+  off = round_up(off + sizeof(float) * (size_t)n_heads * n_chunks * group * 4 * std::max(pool_half, 1), 256);
+  w.total = std::max<size_t>(off, 256);
+  return w;
+}
+
+}  // namespace rkv
+
+extern "C" {
+
+const char* rkv_last_error(void) { return g_error.c_str(); }
+
+int rkv_profile_enable(int32_t stage) {
+  rkv::clear_error();
+  if (stage < -1 || stage > rkv::kStageDecode) return rkv::fail(RKV_ERR_INVALID_ARG, "unknown stage");
+  std::lock_guard<std::mutex> lk(rkv::g_prof_mu);
+  rkv::g_prof_stage = stage;
+  return RKV_OK;
+}
+
+int rkv_profile_read(int32_t* n_launches, double* total_ms) {
+  rkv::clear_error();
+  if (!n_launches || !total_ms) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  std::lock_guard<std::mutex> lk(rkv::g_prof_mu);
+  std::vector<hipEvent_t>& ev = rkv::g_prof_events;
+  double tot = 0.0;
+  int n = 0;
+  int st = RKV_OK;
+  for (size_t i = 0; i + 1 < ev.size(); i += 2) {
+    float ms = 0.f;
+    hipError_t e = hipEventSynchronize(ev[i + 1]);
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, ev[i], ev[i + 1]);
+    if (e != hipSuccess) {
+      st = rkv::fail(RKV_ERR_HIP, std::string("event timing: ") + hipGetErrorString(e));
+      break;
+    }
+    tot += ms;
+    ++n;
+  }
+  for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  ev.clear();
+  *n_launches = n;
+  *total_ms = tot;
+  return st;
+}
+
+int rkv_version(void) { return RKV_VERSION; }
+
+int rkv_allocate_budgets(const double* scores, int32_t n_layers, int32_t transform, int64_t total,
+                         int32_t b_min, int32_t* budgets_out) {
+  rkv::clear_error();
+  if (!scores || !budgets_out) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (n_layers < 1) return rkv::fail(RKV_ERR_INVALID_ARG, "n_layers must be >= 1");
+  if (b_min < 0) return rkv::fail(RKV_ERR_INVALID_ARG, "b_min must be >= 0");
+  if (total < (int64_t)n_layers * b_min) return rkv::fail(RKV_ERR_INVALID_ARG, "total below n_layers * b_min");
+  if (total > ((int64_t)1 << 40)) return rkv::fail(RKV_ERR_INVALID_ARG, "total too large");
+  if (transform != RKV_T_IDENTITY && transform != RKV_T_PPL_CAP)
+    return rkv::fail(RKV_ERR_INVALID_ARG, "unknown transform");
+  const int n = n_layers;
+  std::vector<double> t(scores, scores + n);
+  for (double x : t)
+    if (!std::isfinite(x)) return rkv::fail(RKV_ERR_INVALID_ARG, "scores must be finite");
+  if (transform == RKV_T_PPL_CAP) {
+    // 95th percentile by linear interpolation between order statistics
+    std::vector<double> srt(t);
+    std::sort(srt.begin(), srt.end());
+    double rank = 0.95 * (n - 1);
+    int lo = (int)std::floor(rank);
+    int hi = std::min(lo + 1, n - 1);
+    double cap = srt[lo] + (rank - lo) * (srt[hi] - srt[lo]);
+    for (double& x : t) x = std::min(x, cap);
+  }
+  double mn = *std::min_element(t.begin(), t.end());
+  if (mn <= 0.0)
+    for (double& x : t) x = x - mn + 1e-6;
+  // provisional shares with the iterative b_min clamp
+  std::vector<char> fixed(n, 0);
+  std::vector<double> share(n, 0.0);
+  for (;;) {
+    double wsum = 0.0;
+    int nfixed = 0;
+    for (int i = 0; i < n; ++i) {
+      if (fixed[i]) ++nfixed; else wsum += t[i];
+    }
+    double remaining = (double)total - (double)b_min * nfixed;
+    bool added = false;
+    for (int i = 0; i < n; ++i) {
+      if (fixed[i]) { share[i] = b_min; continue; }
+      share[i] = remaining * t[i] / wsum;
+    }
+    for (int i = 0; i < n; ++i)
+      if (!fixed[i] && share[i] < b_min) { fixed[i] = 1; added = true; }
+    if (!added) break;
+  }
+  // floor, then the residual to the largest fractional remainders (ties: lower layer)
+  std::vector<int64_t> base(n);
+  std::vector<double> frac(n);
+  int64_t sum = 0;
+  for (int i = 0; i < n; ++i) {
+    base[i] = (int64_t)std::floor(share[i]);
+    frac[i] = share[i] - (double)base[i];
+    sum += base[i];
+  }
+  std::vector<int> order(n);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return frac[a] > frac[b]; });
+  int64_t residual = total - sum;
+  for (int64_t r = 0; r < residual && r < n; ++r) base[order[r]] += 1;
+  for (int i = 0; i < n; ++i) {
+    if (base[i] > INT32_MAX) return rkv::fail(RKV_ERR_INVALID_ARG, "budget overflows int32");
+  }
+  for (int i = 0; i < n; ++i) budgets_out[i] = (int32_t)base[i];
+  return RKV_OK;
+}
+
+int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params* params, rkv_plan** out) {
+  rkv::clear_error();
+  if (!layers || !params || !out) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (n_layers < 1) return rkv::fail(RKV_ERR_INVALID_ARG, "n_layers must be >= 1");
+  const rkv_params& p = *params;
+  if (p.window < 1) return rkv::fail(RKV_ERR_PLAN, "window must be >= 1");
+  if (p.pool_kernel < 1 || p.pool_kernel % 2 == 0) return rkv::fail(RKV_ERR_PLAN, "pool_kernel must be odd and >= 1");
+  if (p.pool_kernel / 2 > rkv::kMaxPoolHalf) return rkv::fail(RKV_ERR_UNSUPPORTED, "pool_kernel above 129");
+  if (p.n_sink < 0) return rkv::fail(RKV_ERR_PLAN, "n_sink must be >= 0");
+  if (p.recent_den < 1 || p.recent_num < 0 || p.recent_num > p.recent_den)
+    return rkv::fail(RKV_ERR_PLAN, "need 0 <= recent_num <= recent_den, recent_den >= 1");
+  for (int l = 0; l < n_layers; ++l) {
+    const rkv_layer& ly = layers[l];
+    if (!rule_valid(ly.rule_prefill) || !rule_valid(ly.rule_decode))
+      return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": unknown rule");
+    if (ly.budget_prefill < 0 || ly.budget_decode < 0)
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": negative budget");
+    if (ly.rule_decode == RKV_SNAPKV)
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": SnapKV compresses the prompt only, not valid in decode");
+    if (ly.rule_decode == RKV_H2O && ly.budget_decode < 2)
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": decode H2O needs budget >= 2");
+    if (ly.rule_decode == RKV_STREAMING && ly.budget_decode < 1)
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": decode StreamingLLM needs budget >= 1");
+  }
+  rkv_plan* plan = new (std::nothrow) rkv_plan;
+  if (!plan) return rkv::fail(RKV_ERR_INVALID_ARG, "out of host memory");
+  plan->layers.assign(layers, layers + n_layers);
+  plan->params = p;
+  *out = plan;
+  return RKV_OK;
+}
+
+void rkv_plan_destroy(rkv_plan* plan) { delete plan; }
+
+int rkv_plan_num_layers(const rkv_plan* plan, int32_t* n_layers) {
+  rkv::clear_error();
+  if (!plan || !n_layers) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  *n_layers = (int32_t)plan->layers.size();
+  return RKV_OK;
+}
+
+int rkv_plan_retained_counts(const rkv_plan* plan, int32_t phase, int32_t seq_len, int32_t* counts_out) {
+  rkv::clear_error();
+  if (!plan || !counts_out) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (phase != RKV_PHASE_PREFILL && phase != RKV_PHASE_DECODE) return rkv::fail(RKV_ERR_INVALID_ARG, "unknown phase");
+  if (seq_len < 0) return rkv::fail(RKV_ERR_INVALID_ARG, "seq_len must be >= 0");
+  for (size_t l = 0; l < plan->layers.size(); ++l) {
+    const rkv_layer& ly = plan->layers[l];
+    int32_t rule = phase == RKV_PHASE_PREFILL ? ly.rule_prefill : ly.rule_decode;
+    int32_t b = phase == RKV_PHASE_PREFILL ? ly.budget_prefill : ly.budget_decode;
+    counts_out[l] = rule == RKV_FULL ? seq_len : std::min(b, seq_len);
+  }
+  return RKV_OK;
+}
+
+int rkv_prefill_workspace_size(const rkv_plan* plan, const rkv_shape* shape, size_t* bytes) {
+  rkv::clear_error();
+  if (!plan || !bytes) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  int st = validate_shape(shape);
+  if (st) return st;
+  size_t need = 256;
+  for (const Group& g : layer_groups(plan, shape->seq_len)) need = std::max(need, group_workspace(plan, shape, g));
+  *bytes = need;
+  return RKV_OK;
+}
+
+int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_prefill_io* io, void* ws,
+                      size_t ws_bytes, void* stream) {
+  rkv::clear_error();
+  if (!plan || !io) return rkv::fail(RKV_ERR_INVALID_ARG, "null plan or io");
+  int st = validate_shape(shape);
+  if (st) return st;
+  const rkv_params& p = plan->params;
+  const int L = shape->seq_len;
+  if (p.window > L) return rkv::fail(RKV_ERR_SHAPE, "window larger than seq_len");
+  if (!io->k || !io->v || !io->k_out || !io->v_out || !io->idx_out)
+    return rkv::fail(RKV_ERR_INVALID_ARG, "io arrays k, v, k_out, v_out, idx_out are required");
+  const int n = (int)plan->layers.size();
+  const int G = shape->n_q_heads / shape->n_kv_heads;
+  const int nt = row_tiles(p, shape);
+  bool any_scored = false;
+  for (int l = 0; l < n; ++l) {
+    Layout lo = prefill_layout(plan->layers[l], p, L);
+    any_scored |= lo.scored != 0;
+    if (!io->k[l] || !io->v[l]) return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null k or v");
+    if (!io->k_out[l] || !io->v_out[l] || !io->idx_out[l])
+      if (lo.n_keep > 0) return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null output");
+    if (lo.scored && (!io->q_win || !io->q_win[l]))
+      return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": scoring rule needs q_win");
+  }
+  if (any_scored && nt > rkv::kMaxRowTiles)
+    return rkv::fail(RKV_ERR_UNSUPPORTED, "G * ceil(window / 32) must be <= 8");
+  if (any_scored && L > rkv::kMaxScoredSeqLen)
+    return rkv::fail(RKV_ERR_UNSUPPORTED, "scoring rules support seq_len <= 36864");
+  size_t need = 256;
+  std::vector<Group> groups = layer_groups(plan, L);
+  for (const Group& g : groups) need = std::max(need, group_workspace(plan, shape, g));
+  if (!ws) return rkv::fail(RKV_ERR_WORKSPACE, "workspace is null");
+  if (((uintptr_t)ws) % 256) return rkv::fail(RKV_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < need)
+    return rkv::fail(RKV_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
+
+  const int ktiles = kernel_row_tiles(nt);
+  for (const Group& g : groups) {
+    rkv::PrefillLaunch P;
+    std::memset(&P, 0, sizeof(P));
+    P.n_layers = g.l1 - g.l0;
+    P.batch = shape->batch;
+    P.seq_len = L;
+    P.n_q_heads = shape->n_q_heads;
+    P.n_kv_heads = shape->n_kv_heads;
+    P.window = p.window;
+    P.group = G;
+    P.row_tiles_per_group = (p.window + 31) / 32;
+    P.n_chunks = (L + rkv::kChunk - 1) / rkv::kChunk;
+    P.pool_half = p.pool_kernel / 2;
+    P.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
+    int slot = 0;
+    int64_t rows = 0;
+    bool want_unpooled = false;
+    for (int i = 0; i < P.n_layers; ++i) {
+      const int l = g.l0 + i;
+      Layout lo = prefill_layout(plan->layers[l], p, L);
+      rkv::PrefillLayer& d = P.layer[i];
+      d.q = io->q_win ? (const uint16_t*)io->q_win[l] : nullptr;
+      d.k = (const uint16_t*)io->k[l];
+      d.v = (const uint16_t*)io->v[l];
+      d.k_out = (uint16_t*)io->k_out[l];
+      d.v_out = (uint16_t*)io->v_out[l];
+      d.idx = io->idx_out[l];
+      d.score = io->score_out ? io->score_out[l] : nullptr;
+      d.acc = io->acc_out ? io->acc_out[l] : nullptr;
+      d.rule = plan->layers[l].rule_prefill;
+      d.n_keep = lo.n_keep;
+      d.cand_end = lo.cand_end;
+      d.k_sel = lo.k_sel;
+      d.forced_lo = lo.forced_lo;
+      d.forced_hi = lo.forced_hi;
+      d.all = lo.all;
+      d.slot = lo.scored ? slot : -1;
+      if (lo.scored) {
+        P.slot_layer[slot] = i;
+        if (d.rule == RKV_SNAPKV && d.acc) want_unpooled = true;
+        ++slot;
+      }
+      P.rows_prefix[i] = rows;
+      rows += (int64_t)shape->batch * shape->n_kv_heads * lo.n_keep;
+    }
+    P.rows_prefix[P.n_layers] = rows;
+    P.n_scored = slot;
+    P.want_unpooled = want_unpooled ? 1 : 0;
+    const int n_heads = shape->batch * slot * shape->n_kv_heads;
+    rkv::PrefillWorkspace W =
+        rkv::prefill_workspace_layout(n_heads, P.n_chunks, ktiles * 32, L, G, P.pool_half, true);
+    char* base = (char*)ws;
+    P.counters = (uint32_t*)(base + W.counters);
+    P.stats = (float*)(base + W.stats);
+    P.headstat = (float*)(base + W.headstat);
+    P.S = (float*)(base + W.S);
+    P.Su = (float*)(base + W.Su);
+    P.edge = (float*)(base + W.edge);
+    int err = rkv::launch_prefill(P, ktiles, stream);
+    if (err) return rkv::fail(RKV_ERR_HIP, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)err));
+  }
+  return RKV_OK;
+}
+
+int rkv_prefill_check(const void* ws, size_t ws_bytes, int32_t* status_out) {
+  rkv::clear_error();
+  if (!ws || !status_out) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (ws_bytes < sizeof(uint32_t)) return rkv::fail(RKV_ERR_WORKSPACE, "workspace too small");
+  uint32_t v = 0;
+  hipError_t e = hipMemcpy(&v, ws, sizeof(v), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return rkv::fail(RKV_ERR_HIP, std::string("hipMemcpy: ") + hipGetErrorString(e));
+  *status_out = (int32_t)v;
+  return RKV_OK;
+}
+
+int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_decode_state* state,
+                    const rkv_decode_input* input, int32_t position, void* stream) {
+  rkv::clear_error();
+  if (!plan || !state || !input) return rkv::fail(RKV_ERR_INVALID_ARG, "null plan, state or input");
+  int st = validate_shape(shape);
+  if (st) return st;
+  if (!state->k_cache || !state->v_cache || !state->pos || !state->acc || !input->q || !input->k || !input->v)
+    return rkv::fail(RKV_ERR_INVALID_ARG, "state and input arrays are required");
+  const rkv_params& p = plan->params;
+  const int n = (int)plan->layers.size();
+  for (int l0 = 0; l0 < n; l0 += rkv::kMaxLayersPerLaunch) {
+    rkv::DecodeLaunch D;
+    std::memset(&D, 0, sizeof(D));
+    D.batch = shape->batch;
+    D.n_q_heads = shape->n_q_heads;
+    D.n_kv_heads = shape->n_kv_heads;
+    D.group = shape->n_q_heads / shape->n_kv_heads;
+    D.position = position;
+    D.n_sink = p.n_sink;
+    D.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
+    int cnt = 0, max_cap = 0;
+    for (int l = l0; l < std::min(n, l0 + rkv::kMaxLayersPerLaunch); ++l) {
+      const rkv_layer& ly = plan->layers[l];
+      if (ly.rule_decode == RKV_FULL) continue;
+      const int C = ly.budget_decode;
+      if (position < C) return rkv::fail(RKV_ERR_SHAPE, "position must be >= the layer's capacity");
+      if (!state->k_cache[l] || !state->v_cache[l] || !state->pos[l] || !state->acc[l] || !input->q[l] ||
+          !input->k[l] || !input->v[l])
+        return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null decode buffer");
+      rkv::DecodeLayer& d = D.layer[cnt++];
+      d.k_cache = (uint16_t*)state->k_cache[l];
+      d.v_cache = (uint16_t*)state->v_cache[l];
+      d.pos = state->pos[l];
+      d.acc = state->acc[l];
+      d.q = (const uint16_t*)input->q[l];
+      d.k = (const uint16_t*)input->k[l];
+      d.v = (const uint16_t*)input->v[l];
+      d.victim = input->victim_out ? input->victim_out[l] : nullptr;
+      d.rule = ly.rule_decode;
+      d.capacity = C;
+      d.recent = (int32_t)(((int64_t)C * p.recent_num) / p.recent_den);
+      max_cap = std::max(max_cap, C);
+    }
+    if (!cnt) continue;
+    const int G = shape->n_q_heads / shape->n_kv_heads;
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+      return rkv::fail(RKV_ERR_UNSUPPORTED, "decode needs n_q_heads / n_kv_heads in {1, 2, 4, 8}");
+    if ((size_t)(G + 1) * (max_cap + 1) * sizeof(float) > 150 * 1024)
+      return rkv::fail(RKV_ERR_UNSUPPORTED, "decode capacity too large for one workgroup's LDS");
+    D.n_layers = cnt;
+    int err = rkv::launch_decode(D, max_cap, stream);
+    if (err) return rkv::fail(RKV_ERR_HIP, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)err));
+  }
+  return RKV_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,170 @@
+"""Host-side checks of librkv.so that need no GPU: exported symbols, the allocator against the
+oracle, plan validation and argument checking (every case fails before any HIP call)."""
+import ctypes as C
+import json
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import paper_2606_15157_amd as rkv
+from paper_2606_15157_amd import _abi
+from oracle import alloc as oalloc
+from synth.workloads import B_MIN, mixed_route, pyramid_weights
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "rkv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(rkv_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = _abi.lib()
+    names = declared_functions()
+    assert len(names) >= 10
+    for name in names:
+        assert hasattr(L, name), name
+    assert sorted(names) == sorted(_abi.EXPORTED)
+    assert rkv.version() == 1
+
+
+# ------------------------------------------------------------------ allocator vs the oracle
+
+def test_allocator_matches_stored_workload_budgets():
+    g = json.load(open(os.path.join(GOLDEN, "budgets.json")))
+    b512 = rkv.allocate_budgets(pyramid_weights(32), 32 * 512, B_MIN)
+    assert b512 == g["pyramid_512"]
+    for avg, vec in g["sweep"].items():
+        assert rkv.allocate_budgets(b512, 32 * int(avg), B_MIN) == vec
+
+
+def test_allocator_hand_cases():
+    assert rkv.allocate_budgets([1, 1, 1], 10, 0) == [4, 3, 3]
+    assert rkv.allocate_budgets([10, 3, 1], 24, 5) == [14, 5, 5]
+    assert rkv.allocate_budgets([-1.0, 0.0, 1.0], 30, 0) == oalloc.allocate_from_scores([-1, 0, 1], 0, 30, 0).tolist()
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.lists(st.floats(-50.0, 100.0), min_size=1, max_size=40), st.integers(0, 64), st.integers(0, 4000),
+       st.sampled_from([rkv.T_IDENTITY, rkv.T_PPL_CAP]))
+def test_allocator_agrees_with_oracle(scores, b_min, extra, transform):
+    total = len(scores) * b_min + extra
+    got = np.array(rkv.allocate_budgets(scores, total, b_min, transform))
+    t = oalloc.shift_nonpositive(oalloc.transform(scores, transform))
+    want = oalloc.allocate(t, total, b_min)
+    if not np.array_equal(got, want):
+        # the two sides may sum in different orders; a disagreement is only acceptable at a
+        # near-tie of fractional remainders at the rounding cut
+        share = oalloc.clamped_shares(t, float(total), float(b_min))
+        frac = np.sort(share - np.floor(share))
+        assert np.min(np.diff(frac)) < 1e-9 if len(frac) > 1 else False
+    assert got.sum() == total and (got >= b_min).all()
+
+
+def test_allocator_rejects_bad_arguments():
+    L = _abi.lib()
+    out = (C.c_int32 * 3)()
+    w = (C.c_double * 3)(1, 2, 3)
+    assert L.rkv_allocate_budgets(None, 3, 0, 10, 0, out) == 1
+    assert L.rkv_allocate_budgets(w, 3, 0, 5, 2, out) == 1          # total < n * b_min
+    assert L.rkv_allocate_budgets(w, 3, 9, 10, 0, out) == 1          # unknown transform
+    assert L.rkv_last_error()
+    nan = (C.c_double * 3)(1, float("nan"), 3)
+    assert L.rkv_allocate_budgets(nan, 3, 0, 10, 0, out) == 1
+
+
+# ------------------------------------------------------------------ plans
+
+def test_plan_validation():
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan([rkv.SNAPKV], [64], [rkv.SNAPKV], [64])
+    assert e.value.status == 3                                       # SnapKV is prefill-only
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan([rkv.SNAPKV], [-1])
+    assert e.value.status == 3
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan([rkv.SNAPKV], [64], pool_kernel=6)
+    assert e.value.status == 3
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan([7], [64])
+    assert e.value.status == 1
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan([rkv.H2O], [64], [rkv.H2O], [1])
+    assert e.value.status == 3
+
+
+def test_retained_counts_and_workspace():
+    route = mixed_route()
+    budgets = rkv.allocate_budgets(pyramid_weights(32), 32 * 512, B_MIN)
+    plan = rkv.Plan(route, budgets)
+    assert plan.n_layers == 32
+    assert plan.retained_counts(8192) == budgets
+    assert plan.retained_counts(500) == [min(b, 500) for b in budgets]
+    full = rkv.Plan([rkv.FULL, rkv.SNAPKV], [3, 10])
+    assert full.retained_counts(100) == [100, 10]
+    ws = plan.workspace_size(1, 8192, 32, 8)
+    assert ws > 30 * 8 * 8192 * 4          # at least one fp32 score per scored head position
+    assert ws % 256 == 0
+
+
+# ------------------------------------------------------------------ prefill argument checks
+
+FAKE = 0x10000  # never dereferenced: every case below must fail validation first
+
+
+def call_prefill(plan, shape, io=True, ws=FAKE, ws_bytes=1 << 40, n=None, null_q=False):
+    L = _abi.lib()
+    n = n or plan.n_layers
+    fake = [FAKE] * n
+    if io:
+        iob = _abi.PrefillIO(rkv._parr([None] * n if null_q else fake), rkv._parr(fake), rkv._parr(fake),
+                             rkv._parr(fake), rkv._parr(fake), rkv._parr(fake), None, None)
+        iop = C.byref(iob)
+    else:
+        iop = None
+    sh = _abi.Shape(*shape)
+    return L.rkv_prefill_evict(plan.handle, C.byref(sh), iop, C.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+@pytest.mark.parametrize("shape,status", [
+    ((1, 1024, 30, 8, 128), 2),     # Hq not a multiple of Hkv
+    ((1, 1024, 32, 8, 64), 4),      # head_dim != 128
+    ((1, 16, 32, 8, 128), 2),       # window (32) > seq_len
+    ((0, 1024, 32, 8, 128), 2),     # empty batch
+    ((1, 1024, 64, 2, 128), 4),     # G * ceil(w/32) = 32 row tiles > 8
+    ((1, 40000, 32, 8, 128), 4),    # scored seq_len above the supported maximum
+])
+def test_prefill_shape_errors(shape, status):
+    plan = rkv.Plan([rkv.SNAPKV], [128])
+    assert call_prefill(plan, shape) == status
+    assert _abi.lib().rkv_last_error()
+
+
+def test_prefill_io_and_workspace_errors():
+    plan = rkv.Plan([rkv.SNAPKV, rkv.STREAMING], [128, 64])
+    shape = (1, 1024, 32, 8, 128)
+    assert call_prefill(plan, shape, io=False) == 1
+    assert call_prefill(plan, shape, null_q=True) == 1              # scoring layer without queries
+    assert call_prefill(plan, shape, ws=0) == 5
+    assert call_prefill(plan, shape, ws=FAKE + 8) == 5               # misaligned
+    assert call_prefill(plan, shape, ws_bytes=1024) == 5             # too small
+    assert "workspace" in _abi.lib().rkv_last_error().decode()
+
+
+def test_decode_argument_errors():
+    L = _abi.lib()
+    plan = rkv.Plan([rkv.H2O], [64], [rkv.H2O], [64])
+    fake = rkv._parr([FAKE])
+    st_ = _abi.DecodeState(fake, fake, fake, fake)
+    inp = _abi.DecodeInput(fake, fake, fake, None)
+    sh = _abi.Shape(1, 1, 32, 8, 128)
+    assert L.rkv_decode_step(plan.handle, C.byref(sh), C.byref(st_), C.byref(inp), 10, None) == 2   # position < C
+    assert L.rkv_decode_step(plan.handle, C.byref(sh), None, C.byref(inp), 100, None) == 1
+    sh2 = _abi.Shape(1, 1, 24, 8, 128)                                                               # G = 3
+    assert L.rkv_decode_step(plan.handle, C.byref(sh2), C.byref(st_), C.byref(inp), 100, None) == 4

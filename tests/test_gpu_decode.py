@@ -1,0 +1,116 @@
+"""GPU parity of the decode-phase H2O / StreamingLLM update, teacher-forced per step."""
+import numpy as np
+import pytest
+
+from oracle import decode as OD
+from oracle import prefill as OP
+from parity import bits_to_torch, check_scores, oracle_unpooled, torch_to_bits
+from synth import decode_steps, prefill_layer
+
+pytestmark = pytest.mark.gpu
+
+
+def prefill_state(rules_dec, C, L, B, n_layers, Hq=32, Hkv=8, w=32):
+    import paper_2606_15157_amd as rkv
+    import torch
+    plan = rkv.Plan([OP.H2O] * n_layers, [C] * n_layers, rules_dec, [C] * n_layers, window=w)
+    xs = [[prefill_layer(5, s, l, seq_len=L, n_q_heads=Hq, n_kv_heads=Hkv, window=w) for s in range(B)]
+          for l in range(n_layers)]
+    q = [bits_to_torch(np.stack([x["q"] for x in seqs])) for seqs in xs]
+    k = [bits_to_torch(np.stack([x["k"] for x in seqs])) for seqs in xs]
+    v = [bits_to_torch(np.stack([x["v"] for x in seqs])) for seqs in xs]
+    out = rkv.evict_prefill(plan, q, k, v, acc_out=True)
+    torch.cuda.synchronize()
+    # the decode state seeds: prefill H2O retained set and its unpooled window scores
+    for l in range(n_layers):
+        idx = out["idx"][l].cpu().numpy()
+        acc = out["acc"][l].cpu().numpy()
+        for s in range(B):
+            su = oracle_unpooled(xs[l][s]["q"], xs[l][s]["k"])
+            for h in range(Hkv):
+                check_scores(acc[s, h], su[h, idx[s, h]], f"seed l{l} s{s} h{h}")
+    state = {"k_cache": out["k_out"], "v_cache": out["v_out"], "pos": out["idx"], "acc": out["acc"]}
+    return plan, state
+
+
+def snapshot(state, l):
+    return {"k": torch_to_bits(state["k_cache"][l]), "v": torch_to_bits(state["v_cache"][l]),
+            "pos": state["pos"][l].cpu().numpy().copy(), "acc": state["acc"][l].cpu().numpy().copy()}
+
+
+@pytest.mark.parametrize("C", [64, 200])
+def test_h2o_decode_teacher_forced(C):
+    import paper_2606_15157_amd as rkv
+    import torch
+    B, Hq, Hkv, L, steps, n_layers = 2, 32, 8, 640, 24, 2
+    G = Hq // Hkv
+    recent = C // 2
+    plan, state = prefill_state([OP.H2O] * n_layers, C, L, B, n_layers)
+    ins = [[decode_steps(5, s, l, steps=steps) for s in range(B)] for l in range(n_layers)]
+    n_close = 0
+    for t in range(steps):
+        p = L + t
+        before = [snapshot(state, l) for l in range(n_layers)]
+        q = [bits_to_torch(np.stack([ins[l][s]["q"][t] for s in range(B)])) for l in range(n_layers)]
+        k = [bits_to_torch(np.stack([ins[l][s]["k"][t] for s in range(B)])) for l in range(n_layers)]
+        v = [bits_to_torch(np.stack([ins[l][s]["v"][t] for s in range(B)])) for l in range(n_layers)]
+        vic = [torch.empty((B, Hkv), dtype=torch.int32, device="cuda") for _ in range(n_layers)]
+        rkv.decode_step(plan, state, q, k, v, p, victim_out=vic)
+        torch.cuda.synchronize()
+        for l in range(n_layers):
+            after = snapshot(state, l)
+            vv = vic[l].cpu().numpy()
+            for s in range(B):
+                for h in range(Hkv):
+                    kc = OP.bf16_to_f64(before[l]["k"][s, h])
+                    qg = OP.bf16_to_f64(ins[l][s]["q"][t][h * G:(h + 1) * G])
+                    kt = OP.bf16_to_f64(ins[l][s]["k"][t][h])
+                    acc_all, v_ora, cand = OD.h2o_step(kc, before[l]["pos"][s, h], before[l]["acc"][s, h].astype(np.float64),
+                                                       qg, kt, p, recent)
+                    what = f"step {t} layer {l} seq {s} head {h}"
+                    e = vv[s, h] if vv[s, h] >= 0 else C
+                    mn = acc_all[cand].min()
+                    assert cand[e], what + ": victim is protected"
+                    assert acc_all[e] <= mn * (1 + 1e-3) + 1e-30, what + ": victim is not a minimum"
+                    n_close += int(e != v_ora)
+                    exp_acc = acc_all[:C].copy()
+                    if e < C:
+                        exp_acc[e] = acc_all[C]
+                    check_scores(after["acc"][s, h], exp_acc, what + " acc")
+                    pos_exp = before[l]["pos"][s, h].copy()
+                    k_exp = before[l]["k"][s, h].copy()
+                    v_exp = before[l]["v"][s, h].copy()
+                    if e < C:
+                        pos_exp[e] = p
+                        k_exp[e] = ins[l][s]["k"][t][h]
+                        v_exp[e] = ins[l][s]["v"][t][h]
+                    assert np.array_equal(after["pos"][s, h], pos_exp), what
+                    assert np.array_equal(after["k"][s, h], k_exp), what
+                    assert np.array_equal(after["v"][s, h], v_exp), what
+    print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
+
+
+def test_streaming_decode_replaces_oldest_non_sink():
+    import paper_2606_15157_amd as rkv
+    import torch
+    B, Hq, Hkv, C, L = 1, 32, 8, 48, 256
+    plan = rkv.Plan([OP.STREAMING], [C], [OP.STREAMING], [C], window=32, n_sink=4)
+    x = prefill_layer(6, 0, 0, seq_len=L)
+    out = rkv.evict_prefill(plan, [bits_to_torch(x["q"][None])], [bits_to_torch(x["k"][None])],
+                            [bits_to_torch(x["v"][None])], acc_out=True)
+    state = {"k_cache": out["k_out"], "v_cache": out["v_out"], "pos": out["idx"], "acc": out["acc"]}
+    d = decode_steps(6, 0, 0, steps=5)
+    for t in range(5):
+        p = L + t
+        pos_before = state["pos"][0].cpu().numpy().copy()
+        vic = [torch.empty((B, Hkv), dtype=torch.int32, device="cuda")]
+        rkv.decode_step(plan, state, [bits_to_torch(d["q"][t][None])], [bits_to_torch(d["k"][t][None])],
+                        [bits_to_torch(d["v"][t][None])], p, victim_out=vic)
+        torch.cuda.synchronize()
+        vv = vic[0].cpu().numpy()
+        for h in range(Hkv):
+            pb = pos_before[0, h]
+            cand = np.flatnonzero(pb >= 4)
+            assert vv[0, h] == cand[np.argmin(pb[cand])]
+            assert state["pos"][0].cpu().numpy()[0, h, vv[0, h]] == p
+            assert np.array_equal(torch_to_bits(state["k_cache"][0])[0, h, vv[0, h]], d["k"][t][h])

@@ -1,0 +1,167 @@
+"""GPU parity of the prefill eviction path (through the C ABI) against the CPU oracle."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import prefill as OP
+from parity import (bits_to_torch, check_gather, check_retained, check_scores, oracle_unpooled,
+                    torch_to_bits)
+from synth import f32_to_bf16_bits, prefill_layer
+from synth.workloads import B_MIN, mixed_route, pyramid_weights
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def run_case(rules, budgets, layers, *, window, pool_kernel=7, n_sink=4, num=1, den=2, check_acc=True,
+             label=""):
+    """layers: list (per layer) of list (per sequence) of dicts with q/k/v bits."""
+    import torch
+    import paper_2606_15157_amd as rkv
+    plan = rkv.Plan(rules, budgets, window=window, pool_kernel=pool_kernel, n_sink=n_sink, recent_num=num,
+                    recent_den=den)
+    q_t, k_t, v_t = [], [], []
+    for l, seqs in enumerate(layers):
+        q_t.append(bits_to_torch(np.stack([x["q"] for x in seqs])))
+        k_t.append(bits_to_torch(np.stack([x["k"] for x in seqs])))
+        v_t.append(bits_to_torch(np.stack([x["v"] for x in seqs])))
+    out = rkv.evict_prefill(plan, q_t, k_t, v_t, score_out=True, acc_out=True)
+    torch.cuda.synchronize()
+    assert rkv.prefill_check(out["workspace"]) == 0, "a scoring work item timed out"
+    n_amb = 0
+    for l, seqs in enumerate(layers):
+        idx = out["idx"][l].cpu().numpy()
+        sc = out["scores"][l].cpu().numpy()
+        acc = out["acc"][l].cpu().numpy()
+        ko = torch_to_bits(out["k_out"][l])
+        vo = torch_to_bits(out["v_out"][l])
+        for s, x in enumerate(seqs):
+            ora = OP.evict_layer(rules[l], budgets[l], x["q"], x["k"], x["v"], window=window,
+                                 pool_kernel=pool_kernel, n_sink=n_sink, recent_num=num, recent_den=den)
+            L = x["k"].shape[1]
+            su = oracle_unpooled(x["q"], x["k"]) if rules[l] in (OP.SNAPKV, OP.H2O) else None
+            for h in range(x["k"].shape[0]):
+                what = f"{label} layer {l} seq {s} head {h}"
+                if ora["scores"] is not None:
+                    n = ora["scores"].shape[1]
+                    check_scores(sc[s, h, :n], ora["scores"][h], what)
+                n_amb += check_retained(idx[s, h], ora, h, L, what)
+                check_gather(ko[s, h], vo[s, h], x["k"][h], x["v"][h], idx[s, h], what)
+                if check_acc and su is not None:
+                    check_scores(acc[s, h], su[h, idx[s, h]], what + " acc")
+                if check_acc and su is None:
+                    assert (acc[s, h] == 0).all()
+    return out, n_amb
+
+
+def gen(workload, seq, layer, L, w=32, Hq=32, Hkv=8, n_hh=16):
+    return prefill_layer(workload, seq, layer, seq_len=L, n_q_heads=Hq, n_kv_heads=Hkv, window=w, n_hh=n_hh)
+
+
+@pytest.mark.parametrize("rule", [OP.SNAPKV, OP.H2O, OP.STREAMING, OP.FULL])
+def test_single_layer_1k(rule):
+    """Single layer, L=1024, 32/8 heads, w=32, pool 7, budget 128."""
+    run_case([rule], [128], [[gen(1, 0, 0, 1024)]], window=32, label="c1")
+
+
+@pytest.mark.parametrize("L", [33, 300, 777, 1000, 2049])
+def test_ragged_lengths(L):
+    """Context lengths that are not multiples of the 256-key chunk (several chunks + a tail)."""
+    b = min(100, L - 1)
+    rules = [OP.SNAPKV, OP.H2O, OP.STREAMING]
+    run_case(rules, [b, b, b], [[gen(7, 0, l, L)] for l in range(3)], window=32, label=f"L{L}")
+
+
+@pytest.mark.parametrize("budget", [0, 1, 2, 5, 31, 32, 33, 511, 512, 513, 4096])
+def test_degenerate_budgets(budget):
+    """Budgets around the window size, the context length and zero."""
+    L = 512
+    rules = [OP.SNAPKV, OP.H2O, OP.STREAMING, OP.FULL]
+    run_case(rules, [budget] * 4, [[gen(8, 0, l, L)] for l in range(4)], window=32, label=f"b{budget}")
+
+
+def test_window_totals_sum_to_w():
+    """H2O keeping every position reports the unpooled group-mean score on all of [0, L):
+    every window row's softmax sums to 1, so each KV head's scores sum to w."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    x = gen(9, 0, 0, 1536)
+    plan = rkv.Plan([OP.H2O], [4096], window=32)
+    out = rkv.evict_prefill(plan, [bits_to_torch(x["q"][None])], [bits_to_torch(x["k"][None])],
+                            [bits_to_torch(x["v"][None])], score_out=True)
+    torch.cuda.synchronize()
+    tot = out["scores"][0].double().sum(-1).cpu().numpy()
+    np.testing.assert_allclose(tot, 32.0, rtol=1e-4)
+
+
+def test_uniform_keys_break_ties_by_position():
+    """Equal keys give exactly equal prefix scores; the lowest positions must win."""
+    L, w, b = 1024, 32, 200
+    rng = np.random.default_rng(5)
+    q = f32_to_bf16_bits(rng.standard_normal((32, w, 128)).astype(np.float32))
+    k = f32_to_bf16_bits(np.tile(rng.standard_normal(128).astype(np.float32), (8, L, 1)))
+    v = f32_to_bf16_bits(rng.standard_normal((8, L, 128)).astype(np.float32))
+    x = {"q": q, "k": k, "v": v}
+    out, _ = run_case([OP.SNAPKV, OP.H2O], [b, b], [[x], [x]], window=w, label="uniform")
+    idx = out["idx"][0].cpu().numpy()
+    for h in range(8):
+        assert idx[0, h].tolist() == list(range(b - w)) + list(range(L - w, L))
+    idx = out["idx"][1].cpu().numpy()
+    for h in range(8):
+        assert idx[0, h].tolist() == list(range(b - b // 2)) + list(range(L - b // 2, L))
+
+
+def test_batch_of_distinct_sequences():
+    L = 2048
+    rules = [OP.SNAPKV, OP.H2O]
+    layers = [[gen(3, s, l, L) for s in range(3)] for l in range(2)]
+    run_case(rules, [300, 300], layers, window=32, label="batch3")
+
+
+def test_window_64_two_tile_groups():
+    """w = 64: each query head spans two 32-row tiles (the 8-tile scoring kernel)."""
+    L = 4096
+    rules = [OP.SNAPKV, OP.H2O]
+    layers = [[gen(4, 0, l, L, w=64, n_hh=64)] for l in range(2)]
+    run_case(rules, [1024, 1024], layers, window=64, label="w64")
+
+
+def test_odd_window_and_group_shapes():
+    """w = 20 (padded rows), G = 2 (16 query heads on 8 KV heads), pool kernel 5."""
+    L = 1500
+    rules = [OP.SNAPKV, OP.H2O]
+    layers = [[gen(6, 0, l, L, w=20, Hq=16)] for l in range(2)]
+    run_case(rules, [150, 150], layers, window=20, pool_kernel=5, label="w20g2")
+
+
+def test_full_route_8k_matches_oracle():
+    """The 32-layer mixed route at L=8192 (StreamingLLM 0-1, SnapKV 2-15, H2O 16-27,
+    SnapKV 28-31), PyramidKV-ramp budgets summing to 32 x 512, full size, every layer."""
+    g = json.load(open(os.path.join(GOLDEN, "budgets.json")))
+    budgets = g["pyramid_512"]
+    rules = mixed_route()
+    layers = [[gen(2, 0, l, 8192)] for l in range(32)]
+    out, n_amb = run_case(rules, budgets, layers, window=32, label="route8k")
+    print(f"positions in tie bands: {n_amb}")
+
+
+def test_repeat_runs_are_bitwise_identical():
+    """Race detector: two runs on the same inputs give identical scores, indices and rows."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    L = 4096
+    rules = [OP.SNAPKV, OP.H2O, OP.STREAMING]
+    xs = [gen(11, 0, l, L) for l in range(3)]
+    plan = rkv.Plan(rules, [400, 400, 400], window=32)
+    q = [bits_to_torch(x["q"][None]) for x in xs]
+    k = [bits_to_torch(x["k"][None]) for x in xs]
+    v = [bits_to_torch(x["v"][None]) for x in xs]
+    a = rkv.evict_prefill(plan, q, k, v, score_out=True, acc_out=True)
+    b = rkv.evict_prefill(plan, q, k, v, score_out=True, acc_out=True)
+    torch.cuda.synchronize()
+    for key in ("idx", "scores", "acc", "k_out", "v_out"):
+        for l in range(3):
+            assert torch.equal(a[key][l], b[key][l]), (key, l)
