@@ -23,12 +23,15 @@ struct Layout {
   int32_t n_keep, cand_end, k_sel, forced_lo, forced_hi, all, scored;
 };
 
-Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L) {
+// `want_scores`: the caller asked for score_out / acc_out of this layer.  A scoring rule is
+// scored when it has to rank candidates or when its scores are an output.
+Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L, bool want_scores = true) {
   Layout o{};
   const int32_t b = ly.budget_prefill;
   o.scored = (ly.rule_prefill == RKV_SNAPKV || ly.rule_prefill == RKV_H2O) ? 1 : 0;
   if (ly.rule_prefill == RKV_FULL || b >= L) {
     o.n_keep = L; o.all = 1; o.cand_end = 0; o.k_sel = 0; o.forced_lo = 0; o.forced_hi = L;
+    if (o.scored && !want_scores) o.scored = 0;
     return o;
   }
   o.n_keep = b;
@@ -50,6 +53,7 @@ Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L) {
     }
     default: break;
   }
+  if (o.scored && o.k_sel == 0 && !want_scores) o.scored = 0;
   return o;
 }
 
@@ -136,17 +140,16 @@ PrefillWorkspace prefill_workspace_layout(int n_heads, int n_chunks, int rows, i
   PrefillWorkspace w{};
   size_t off = 0;
   w.counters = off;
-  off = round_up(off + sizeof(uint32_t) * (2 + 2 * (size_t)n_heads), 256);
+  off = round_up(off + sizeof(uint32_t) * (2 + (size_t)n_heads), 256);
   w.stats = off;
   off = round_up(off + sizeof(float) * 2 * (size_t)n_heads * n_chunks * rows, 256);
-  w.headstat = off;
-  off = round_up(off + sizeof(float) * 2 * (size_t)n_heads * rows, 256);
   w.S = off;
   off = round_up(off + sizeof(float) * (size_t)n_heads * seq_len, 256);
   w.Su = off;
   if (want_unpooled) off = round_up(off + sizeof(float) * (size_t)n_heads * seq_len, 256);
   w.edge = off;
   off = round_up(off + sizeof(float) * (size_t)n_heads * n_chunks * group * 4 * std::max(pool_half, 1), 256);
+  w.end = off;
   w.total = std::max<size_t>(off, 256);
   return w;
 }
@@ -352,8 +355,6 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
   }
   if (any_scored && nt > rkv::kMaxRowTiles)
     return rkv::fail(RKV_ERR_UNSUPPORTED, "G * ceil(window / 32) must be <= 8");
-  if (any_scored && L > rkv::kMaxScoredSeqLen)
-    return rkv::fail(RKV_ERR_UNSUPPORTED, "scoring rules support seq_len <= 36864");
   size_t need = 256;
   std::vector<Group> groups = layer_groups(plan, L);
   for (const Group& g : groups) need = std::max(need, group_workspace(plan, shape, g));
@@ -377,12 +378,12 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     P.n_chunks = (L + rkv::kChunk - 1) / rkv::kChunk;
     P.pool_half = p.pool_kernel / 2;
     P.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
-    int slot = 0;
-    int64_t rows = 0;
+    int slot = 0, n_unscored = 0;
     bool want_unpooled = false;
     for (int i = 0; i < P.n_layers; ++i) {
       const int l = g.l0 + i;
-      Layout lo = prefill_layout(plan->layers[l], p, L);
+      const bool want = (io->score_out && io->score_out[l]) || (io->acc_out && io->acc_out[l]);
+      Layout lo = prefill_layout(plan->layers[l], p, L, want);
       rkv::PrefillLayer& d = P.layer[i];
       d.q = io->q_win ? (const uint16_t*)io->q_win[l] : nullptr;
       d.k = (const uint16_t*)io->k[l];
@@ -404,12 +405,12 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
         P.slot_layer[slot] = i;
         if (d.rule == RKV_SNAPKV && d.acc) want_unpooled = true;
         ++slot;
+      } else if (lo.n_keep > 0) {
+        P.unscored_layer[n_unscored++] = i;
       }
-      P.rows_prefix[i] = rows;
-      rows += (int64_t)shape->batch * shape->n_kv_heads * lo.n_keep;
     }
-    P.rows_prefix[P.n_layers] = rows;
     P.n_scored = slot;
+    P.n_unscored = n_unscored;
     P.want_unpooled = want_unpooled ? 1 : 0;
     const int n_heads = shape->batch * slot * shape->n_kv_heads;
     rkv::PrefillWorkspace W =
@@ -417,7 +418,7 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     char* base = (char*)ws;
     P.counters = (uint32_t*)(base + W.counters);
     P.stats = (float*)(base + W.stats);
-    P.headstat = (float*)(base + W.headstat);
+    P.fill_vec4 = (int64_t)((W.end - W.stats) / 16);
     P.S = (float*)(base + W.S);
     P.Su = (float*)(base + W.Su);
     P.edge = (float*)(base + W.edge);

@@ -1,29 +1,35 @@
-// Prefill prompt compression kernels for gfx950 (CDNA4).
+// Prefill prompt compression for gfx950 (CDNA4): one fused kernel per launch group.
 //
-// One call runs, on the caller's stream:
-//   zero_counters  clear the work-queue and barrier counters of the workspace
-//   score_kernel   window Q K^T on bf16 MFMA (fp32 accumulate), causal mask, softmax
-//                  normalised over all visible keys, window column sum, max-pool and
-//                  query-group mean -> one fp32 score per (sequence, layer, KV head, key)
-//   select_kernel  per (sequence, layer, KV head): top-k by (score desc, position asc)
-//                  with a bitwise radix search for the k-th value and an ordered compaction
-//   gather_kernel  copy the retained K and V rows (16 lanes x 16 B per 256-byte row)
+// Per (sequence, scored layer, KV head) -- a "head" -- the window scores are
+//   A[g][j] = sum_i softmax_j(Q[g,i] . K[j] / sqrt(d))      (w window rows per query head g)
+//   S[j]    = mean_g maxpool(A[g])[j]  (SnapKV)  or  mean_g A[g][j]  (H2O)
+// The softmax of a window row is normalised over every key while the window sum runs over
+// rows, so a head is done in two passes over its keys, each split into 512-key chunks:
+//   stats item  (head, chunk): logits on MFMA (K chunk as the 32-row A operand, window queries
+//               from LDS as B), per-row running max and sum of exponentials; the last chunk of
+//               the head to finish folds all chunks into one log-normaliser per row;
+//   score item  (head, chunk): the same logits again (the chunk's K is re-read from the
+//               on-die caches: score items run a fixed number of steps after their head's stats
+//               items), probabilities exp2(z - normaliser), column sums per query head inside
+//               each lane (queries as the A operand put a key in every lane), max-pool inside
+//               the chunk, group mean -> S;
+//   select item (head): fixes the pooled score next to chunk borders, finds the k-th largest
+//               score with three radix-histogram passes, writes the retained positions in
+//               ascending order (ties at the k-th value taken by position);
+//   gather item (head, part): copies the retained K and V rows, 16 lanes x 16 B per row.
+// Layers that need no scores (StreamingLLM, Full, or budgets covering the prompt) get copy
+// items only.  Items take tickets from an atomic counter, so they start in ticket order; an item
+// waits only for items with earlier tickets (which never wait for later ones), and every wait is
+// bounded (on time-out the workspace status word is set and the item carries on).
 //
-// Softmax normalisation of a window row needs its maximum and sum over every key, while the
-// window sum runs over rows.  A scoring work item owns 256 keys of one KV head for all of
-// its G*w window rows and keeps its exponentials in registers; items publish per-row chunk
-// maxima and sums, the last item of a head to arrive combines them, and every item then
-// finishes its column sums with the head's normalisers.  Work items take tickets from an
-// atomic counter, so the items of a head are always dispatched before any later ticket; a
-// waiting item only ever waits for items that already hold tickets, which guarantees
-// progress.  Each wait is bounded; on time-out the item flags the workspace status word.
-//
-// Cross-workgroup data is written and read with agent-scope relaxed atomics, which bypass the
-// XCD-local caches; ordering uses workgroup fences plus vmcnt(0) waits, avoiding agent-scope
-// fences (L2 flush and invalidate).
+// Data handed between workgroups goes through agent-scope relaxed atomics (they bypass the
+// XCD-local caches); ordering uses workgroup fences plus vmcnt(0) waits rather than agent-scope
+// fences, which would flush and invalidate L2.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
+
+#include <algorithm>
 
 #include "rkv_internal.h"
 
@@ -34,21 +40,39 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 512;
+constexpr int kThreads = 256;            // 4 waves, one per SIMD
 constexpr int kWaves = kThreads / 64;
+constexpr int kKeysPerWave = kChunk / kWaves;   // 128 keys = 4 tiles of 32
+constexpr int kTilesPerWave = kKeysPerWave / 32;
+constexpr int kKDepth = 2;               // key tiles in registers per wave (1 loading ahead)
+static_assert(kTilesPerWave % kKDepth == 0, "tile loop is unrolled by the ring depth");
+constexpr int kRowTilesPerPass = 1;      // row tiles whose accumulators are live at once
 constexpr int kQStride = 136;            // bf16 per LDS row of Q: 128 + 8 padding (272 B)
-constexpr int kTStride = 36;             // floats per row of a wave's 32x32 transpose tile
-constexpr uint32_t kSpinLimit = 1u << 20;
-constexpr int kSelectThreads = 512;
-constexpr int kGatherThreads = 256;
+constexpr uint32_t kSpinLimit = 1u << 21;
+constexpr int kHistBins = 2048;
+
+enum ItemType { kItemStats = 0, kItemScore = 1, kItemSelect = 2, kItemGather = 3, kItemCopy = 4 };
 
 __device__ __forceinline__ void store_coherent(float* p, float v) {
-  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_coherent(int32_t* p, int32_t v) {
+  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), (uint32_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ float load_coherent(const float* p) {
   return __uint_as_float(__hip_atomic_load(reinterpret_cast<const uint32_t*>(p), __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT));
+}
+__device__ __forceinline__ int32_t load_coherent(const int32_t* p) {
+  return (int32_t)__hip_atomic_load(reinterpret_cast<const uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_coherent2(float* p, float a, float b) {
+  const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float2 load_coherent2(const float* p) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
 }
 // Wait until this wave's memory operations have completed (ordering only, no cache flush).
 __device__ __forceinline__ void vmem_release() {
@@ -59,503 +83,781 @@ __device__ __forceinline__ void vmem_acquire() {
   __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
+// Bounded wait (one thread) until *flag >= target.
+__device__ __forceinline__ void wait_at_least(uint32_t* flag, uint32_t target, uint32_t* status) {
+  uint32_t it = 0;
+  while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    __builtin_amdgcn_s_sleep(2);
+    if (++it > kSpinLimit) {
+      atomicOr(status, 1u);
+      break;
+    }
+  }
+  vmem_acquire();
+}
+
+// Online combination of (max, sum) pairs in log2 units.
+__device__ __forceinline__ void combine_ms(float& M, float& S, float m, float l) {
+  if (!(l > 0.f)) return;
+  if (m > M) {
+    S = S * __builtin_amdgcn_exp2f(M - m) + l;
+    M = m;
+  } else {
+    S += l * __builtin_amdgcn_exp2f(m - M);
+  }
+}
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-__global__ void zero_counters(uint32_t* c, int n) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) c[i] = 0u;
+// Clears the counters and fills the statistics, score and chunk-edge regions with the NaN
+// pattern that marks "not written yet" (every written value is a number).
+__global__ void reset_workspace(uint32_t* counters, int n_counters, u32x4* fill, int64_t n_fill) {
+  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = i0; i < n_counters; i += stride) counters[i] = 0u;
+  const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+  for (int64_t i = i0; i < n_fill; i += stride) fill[i] = nan4;
 }
 
-// ------------------------------------------------------------------------------------------
-// Scoring.  NT = number of 32-row tiles of window rows per KV head (G * ceil(w/32), padded).
-// Wave v of the work item computes the 32 x (NT*32) logit block of keys [c*256 + 32v, +32):
-// MFMA A operand = 32 keys (straight from HBM into VGPRs), B operand = 32 query rows (LDS).
-// Output element (key m, row n) of tile t lives in lane n + 32*((m/4)%2), register
-// (m%4) + 4*(m/8): each lane owns one window row and 16 of the wave's keys.
-// ------------------------------------------------------------------------------------------
-template <int NT>
-__global__ __launch_bounds__(kThreads) void score_kernel(const PrefillLaunch P) {
+__device__ __forceinline__ bool unwritten(float x) { return x != x; }
+
+// ---------------------------------------------------------------------------------------------
+// Work-item decoding.
+// ---------------------------------------------------------------------------------------------
+__device__ __forceinline__ int64_t clampi(int64_t x, int64_t lo, int64_t hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+// Tickets issued before step s.  Step s holds the stats items of head s, the score items of
+// head s - lb, the select item of head s - lb - ls and the gather items of head s - lb - ls - lg.
+struct Lags {
+  int64_t b, s, g;
+};
+__device__ __forceinline__ int64_t step_prefix(int64_t s, int64_t nH, int64_t NC, const Lags& lag) {
+  return NC * clampi(s, 0, nH) + NC * clampi(s - lag.b, 0, nH) + clampi(s - lag.b - lag.s, 0, nH) +
+         (int64_t)kGatherParts * clampi(s - lag.b - lag.s - lag.g, 0, nH);
+}
+
+struct Item {
+  int type, head, chunk, part;
+};
+
+__device__ Item decode_item(int64_t t, const PrefillLaunch& P, int nH) {
+  Item it{};
+  const int64_t NC = P.n_chunks;
+  const Lags lag{P.lag_score, P.lag_select, P.lag_gather};
+  const int64_t n_steps = nH + lag.b + lag.s + lag.g;
+  const int64_t scored_total = nH > 0 ? step_prefix(n_steps, nH, NC, lag) : 0;
+  if (t >= scored_total) {
+    const int64_t u = t - scored_total;
+    it.type = kItemCopy;
+    it.part = (int)(u % kGatherParts);
+    it.head = (int)(u / kGatherParts);   // (unscored layer, sequence, KV head)
+    return it;
+  }
+  int64_t lo = 0, hi = n_steps - 1;      // largest s with prefix(s) <= t
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) / 2;
+    if (step_prefix(mid, nH, NC, lag) <= t) lo = mid; else hi = mid - 1;
+  }
+  const int64_t s = lo;
+  int64_t w = t - step_prefix(s, nH, NC, lag);
+  if (s < nH) {
+    if (w < NC) { it.type = kItemStats; it.head = (int)s; it.chunk = (int)w; return it; }
+    w -= NC;
+  }
+  const int64_t hb = s - lag.b, hs = hb - lag.s, hg = hs - lag.g;
+  if (hb >= 0 && hb < nH) {
+    if (w < NC) { it.type = kItemScore; it.head = (int)hb; it.chunk = (int)w; return it; }
+    w -= NC;
+  }
+  if (hs >= 0 && hs < nH) {
+    if (w < 1) { it.type = kItemSelect; it.head = (int)hs; return it; }
+    w -= 1;
+  }
+  it.type = kItemGather;
+  it.head = (int)hg;
+  it.part = (int)w;
+  return it;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Shared pieces of the stats and score items.
+// ---------------------------------------------------------------------------------------------
+template <int NT, int NTG>
+__device__ __forceinline__ void load_q_to_lds(uint16_t* sQ, const PrefillLaunch& P, const PrefillLayer& ly, int s, int h) {
   constexpr int R = NT * 32;
-  constexpr int kQBytes = R * kQStride * 2;
-  constexpr int kTBytes = kWaves * 32 * kTStride * 4;
-  constexpr int kUnion = kQBytes > kTBytes ? kQBytes : kTBytes;
-  __shared__ __attribute__((aligned(16))) unsigned char sQT[kUnion];
-  __shared__ float sRed[kWaves][R];
-  __shared__ float sMax[R], sSum[R], sFac[R];
-  __shared__ float sA[NT][kChunk];
-  __shared__ int sTicket, sFlag;
-
-  uint16_t* sQ = reinterpret_cast<uint16_t*>(sQT);
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hf = lane >> 5, ln = lane & 31;
-  uint32_t* counters = P.counters;
-
-  if (tid == 0) sTicket = (int)atomicAdd(&counters[1], 1u);
-  __syncthreads();
-  const int ticket = sTicket;
-  const int NC = P.n_chunks, L = P.seq_len, w = P.window, G = P.group, NTg = P.row_tiles_per_group;
-  const int Hkv = P.n_kv_heads, B = P.batch;
-  const int n_heads = B * P.n_scored * Hkv;
-  const int hd = ticket / NC, c = ticket - hd * NC;
-  const int h = hd % Hkv, s = (hd / Hkv) % B, slot = hd / (Hkv * B);
-  const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
-  const int nt_used = G * NTg;
-
-  // ---- window queries of this KV head's group -> LDS (zero rows for padding)
-  {
-    const uint16_t* qb = ly.q + (size_t)(s * P.n_q_heads + h * G) * w * kHeadDim;
-    for (int e = tid; e < R * 16; e += kThreads) {
-      const int row = e >> 4, piece = e & 15;
-      const int g = row / (NTg * 32), i = row - g * (NTg * 32);
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (g < G && i < w) val = *reinterpret_cast<const u32x4*>(qb + (size_t)(g * w + i) * kHeadDim + piece * 8);
-      *reinterpret_cast<u32x4*>(sQ + row * kQStride + piece * 8) = val;
-    }
+  constexpr int kPer = R * 16 / kThreads;   // 16-byte pieces per thread
+  const int G = P.group, w = P.window;
+  const uint16_t* qb = ly.q + (size_t)(s * P.n_q_heads + h * G) * w * kHeadDim;
+  u32x4 val[kPer];
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {       // all loads in flight together
+    const int e = threadIdx.x + i * kThreads;
+    const int row = e >> 4, piece = e & 15;
+    const int t = row >> 5;
+    const int g = t / NTG, ii = (t - g * NTG) * 32 + (row & 31);
+    val[i] = u32x4{0u, 0u, 0u, 0u};
+    if (g < G && ii < w) val[i] = *reinterpret_cast<const u32x4*>(qb + (size_t)(g * w + ii) * kHeadDim + piece * 8);
   }
-  // ---- this wave's 32 keys, dims [64*hf, 64*hf + 64) per lane, straight to registers
-  const int key0 = c * kChunk + wv * 32;
-  const size_t head_base = (size_t)(s * Hkv + h) * L;
-  u32x4 kf[8];
-  {
-    int key = key0 + ln;
-    key = key < L ? key : L - 1;
-    const uint16_t* kp = ly.k + (head_base + key) * kHeadDim + hf * 64;
 #pragma unroll
-    for (int st = 0; st < 8; ++st) kf[st] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kp + st * 8));
+  for (int i = 0; i < kPer; ++i) {
+    const int e = threadIdx.x + i * kThreads;
+    *reinterpret_cast<u32x4*>(sQ + (e >> 4) * kQStride + (e & 15) * 8) = val[i];
   }
-  __syncthreads();
+}
 
-  f32x16 acc[NT];
+// Lane of a 32-key tile: key `key` (clamped into the head), dims 64*hf + [0, 64).
+__device__ __forceinline__ void load_k_frag(u32x4 (&kf)[8], const uint16_t* khead, int key, int L, int hf) {
+  key = key < L ? key : L - 1;
+  const uint16_t* kp = khead + (size_t)key * kHeadDim + hf * 64;
 #pragma unroll
-  for (int t = 0; t < NT; ++t)
+  for (int st = 0; st < 8; ++st) kf[st] = *reinterpret_cast<const u32x4*>(kp + st * 8);
+}
+
+// One 32-key tile against NH row tiles starting at t0: 8 k-steps of 16 dims.  KEYS_AS_COLUMNS = false puts
+// the keys on the MFMA A operand (output lane = window row), true puts the window queries on A
+// (output lane = key).  The scheduling barriers keep the compiler from hoisting all 32 query
+// fragment reads from LDS ahead of the MFMAs (that costs 128 VGPRs).
+template <int NH, bool KEYS_AS_COLUMNS>
+__device__ __forceinline__ void mfma_tile(f32x16 (&acc)[NH], const u32x4 (&kf)[8], const uint16_t* sQ, int ln, int hf,
+                                          int t0, int nt_used) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[t][r] = 0.f;
+  for (int i = 0; i < NH; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
 #pragma unroll
   for (int st = 0; st < 8; ++st) {
-    const bf16x8 a = as_bf16x8(kf[st]);
+    const bf16x8 kb = as_bf16x8(kf[st]);
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      if (t < nt_used) {
-        const bf16x8 b = *reinterpret_cast<const bf16x8*>(sQ + (t * 32 + ln) * kQStride + hf * 64 + st * 8);
-        acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[t], 0, 0, 0);
+    for (int i = 0; i < NH; ++i) {
+      if (t0 + i < nt_used) {
+        const bf16x8 qf = *reinterpret_cast<const bf16x8*>(sQ + ((t0 + i) * 32 + ln) * kQStride + hf * 64 + st * 8);
+        if (KEYS_AS_COLUMNS) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf, kb, acc[i], 0, 0, 0);
+        else acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf, acc[i], 0, 0, 0);
       }
     }
-  }
-
-  // ---- mask (causal inside the window, ragged tail, padding rows) and chunk row maxima
-  const float NEG_INF = -__builtin_inff();
-  const bool need_mask = (key0 + 32 > L - w) || (nt_used < NT) || (w % 32 != 0);
-  float part[NT];
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    const int row = t * 32 + ln;
-    const int g = row / (NTg * 32), i = row - g * (NTg * 32);
-    const bool rvalid = (t < nt_used) && (i < w);
-    const int rpos = L - w + i;
-    float m = NEG_INF;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      float z = acc[t][r];
-      if (need_mask) {
-        const int kk = key0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-        if (!rvalid || kk >= L || kk > rpos) z = NEG_INF;
-        acc[t][r] = z;
-      }
-      m = fmaxf(m, z);
-    }
-    m = fmaxf(m, __shfl_xor(m, 32));
-    part[t] = m;
-  }
-  if (hf == 0) {
-#pragma unroll
-    for (int t = 0; t < NT; ++t) sRed[wv][t * 32 + ln] = part[t];
-  }
-  __syncthreads();
-  if (tid < R) {
-    float m = sRed[0][tid];
-#pragma unroll
-    for (int v = 1; v < kWaves; ++v) m = fmaxf(m, sRed[v][tid]);
-    sMax[tid] = m;
-  }
-  __syncthreads();
-
-  // ---- exponentials relative to the chunk maximum (kept in registers) and chunk row sums
-  const float sl2 = P.scale_log2;
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    float mref = sMax[t * 32 + ln];
-    mref = (mref == NEG_INF) ? 0.f : mref * sl2;
-    float sm = 0.f;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const float e = __builtin_amdgcn_exp2f(fmaf(acc[t][r], sl2, -mref));
-      acc[t][r] = e;
-      sm += e;
-    }
-    sm += __shfl_xor(sm, 32);
-    part[t] = sm;
-  }
-  if (hf == 0) {
-#pragma unroll
-    for (int t = 0; t < NT; ++t) sRed[wv][t * 32 + ln] = part[t];
-  }
-  __syncthreads();
-  float* stat = P.stats + ((size_t)hd * NC + c) * R * 2;
-  if (tid < R) {
-    float sm = 0.f;
-#pragma unroll
-    for (int v = 0; v < kWaves; ++v) sm += sRed[v][tid];
-    sSum[tid] = sm;
-    const float m = sMax[tid];
-    store_coherent(stat + 2 * tid, m == NEG_INF ? NEG_INF : m * sl2);
-    store_coherent(stat + 2 * tid + 1, sm);
-  }
-  vmem_release();
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t old = __hip_atomic_fetch_add(&counters[2 + hd], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    sFlag = (old == (uint32_t)(NC - 1)) ? 1 : 0;
-  }
-  __syncthreads();
-
-  // ---- head normalisers: the last item combines every chunk's (max, sum), the others wait
-  float* hstat = P.headstat + (size_t)hd * R * 2;
-  if (sFlag) {
-    vmem_acquire();
-    if (tid < R) {
-      float M = NEG_INF, S = 0.f;
-      const float* st0 = P.stats + (size_t)hd * NC * R * 2 + 2 * tid;
-      for (int cc = 0; cc < NC; ++cc) {
-        const float m = load_coherent(st0 + (size_t)cc * R * 2);
-        const float l = load_coherent(st0 + (size_t)cc * R * 2 + 1);
-        if (l > 0.f) {
-          if (m > M) { S = S * __builtin_amdgcn_exp2f(M - m) + l; M = m; }
-          else S += l * __builtin_amdgcn_exp2f(m - M);
-        }
-      }
-      const float inv = S > 0.f ? 1.0f / S : 0.f;
-      store_coherent(hstat + 2 * tid, M);
-      store_coherent(hstat + 2 * tid + 1, inv);
-      sRed[0][tid] = M;
-      sRed[1][tid] = inv;
-    }
-    vmem_release();
-    __syncthreads();
-    if (tid == 0) __hip_atomic_store(&counters[2 + n_heads + hd], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  } else {
-    if (tid == 0) {
-      uint32_t it = 0;
-      while (__hip_atomic_load(&counters[2 + n_heads + hd], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u) {
-        __builtin_amdgcn_s_sleep(2);
-        if (++it > kSpinLimit) {
-          atomicOr(&counters[0], 1u);
-          break;
-        }
-      }
-      vmem_acquire();
-    }
-    __syncthreads();
-    if (tid < R) {
-      sRed[0][tid] = load_coherent(hstat + 2 * tid);
-      sRed[1][tid] = load_coherent(hstat + 2 * tid + 1);
-    }
-  }
-  __syncthreads();
-  if (tid < R) {
-    const float mc = sMax[tid];
-    const float M = sRed[0][tid], inv = sRed[1][tid];
-    sFac[tid] = (inv == 0.f || mc == NEG_INF) ? 0.f : __builtin_amdgcn_exp2f(mc * sl2 - M) * inv;
-  }
-  __syncthreads();
-
-  // ---- per query head column sums: scale by the row factor, transpose through LDS, reduce
-  {
-    float* T = reinterpret_cast<float*>(sQT) + wv * 32 * kTStride;
-    for (int g = 0; g < G; ++g) {
-      float v[16];
-#pragma unroll
-      for (int r = 0; r < 16; ++r) v[r] = 0.f;
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        if (t >= g * NTg && t < (g + 1) * NTg) {
-          const float f = sFac[t * 32 + ln];
-#pragma unroll
-          for (int r = 0; r < 16; ++r) v[r] = fmaf(f, acc[t][r], v[r]);
-        }
-      }
-      // row ln, keys 8q + 4hf + {0..3}
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        float4 x = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
-        *reinterpret_cast<float4*>(T + ln * kTStride + 8 * q + 4 * hf) = x;
-      }
-      __builtin_amdgcn_wave_barrier();
-      float sum = 0.f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) sum += T[(16 * hf + j) * kTStride + ln];
-      sum += __shfl_xor(sum, 32);
-      __builtin_amdgcn_wave_barrier();
-      if (hf == 0) sA[g][wv * 32 + ln] = sum;
-    }
-  }
-  __syncthreads();
-
-  // ---- group mean (unpooled), in-chunk max-pool (SnapKV), scores and chunk-edge values
-  const int cbase = c * kChunk;
-  if (tid < kChunk) {
-    const int key = cbase + tid;
-    if (key < L) {
-      float su = 0.f;
-      for (int g = 0; g < G; ++g) su += sA[g][tid];
-      su = su / (float)G;
-      float* Srow = P.S + (size_t)hd * L;
-      if (ly.rule == RKV_SNAPKV) {
-        const int npre = L - w;
-        float sc = su;
-        if (key < npre) {
-          const int ph = P.pool_half;
-          const int lo = max(key - ph, cbase), hi = min(min(key + ph, cbase + kChunk - 1), npre - 1);
-          sc = 0.f;
-          for (int g = 0; g < G; ++g) {
-            float m = NEG_INF;
-            for (int t = lo; t <= hi; ++t) m = fmaxf(m, sA[g][t - cbase]);
-            sc += m;
-          }
-          sc = sc / (float)G;
-        }
-        Srow[key] = sc;
-        if (P.want_unpooled) P.Su[(size_t)hd * L + key] = su;
-      } else {
-        Srow[key] = su;
-      }
-    }
-  }
-  if (ly.rule == RKV_SNAPKV && P.pool_half > 0) {
-    const int E = 4 * P.pool_half, twoP = 2 * P.pool_half;
-    float* ed = P.edge + ((size_t)hd * NC + c) * G * E;
-    for (int e = tid; e < G * E; e += kThreads) {
-      const int g = e / E, o = e - g * E;
-      const int kl = o < twoP ? o : kChunk - twoP + (o - twoP);
-      ed[e] = (cbase + kl < L) ? sA[g][kl] : 0.f;
-    }
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// ------------------------------------------------------------------------------------------
-// Selection.  One workgroup per (layer slot, sequence, KV head).
-// ------------------------------------------------------------------------------------------
-__device__ __forceinline__ int block_sum(int v, int* sh) {
-  // sh: kSelectThreads / 64 + 1 ints
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+// Masking of one accumulator tile (causal inside the window, ragged tail, padding rows).
+template <int NTG>
+__device__ __forceinline__ void mask_rows_lane(f32x16& acc, int t, int ln, int hf, int tile_key0, int G, int w, int L) {
+  // lane = window row ln of tile t, registers = keys tile_key0 + 8(r/4) + 4hf + r%4
+  const int g = t / NTG, i = (t - g * NTG) * 32 + ln;
+  const bool valid = g < G && i < w;
+  const int last = min(L - 1, L - w + i);
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  if (lane == 0) sh[wv] = v;
-  __syncthreads();
-  int t = 0;
+  for (int r = 0; r < 16; ++r) {
+    const int kk = tile_key0 + 8 * (r >> 2) + 4 * hf + (r & 3);
+    if (!valid || kk > last) acc[r] = -__builtin_inff();
+  }
+}
+template <int NTG>
+__device__ __forceinline__ void mask_rows_regs(f32x16& p, int t, int hf, int key, int G, int w, int L) {
+  // lane = key, registers = window rows t*32 + 8(r/4) + 4hf + r%4
 #pragma unroll
-  for (int i = 0; i < kSelectThreads / 64; ++i) t += sh[i];
-  __syncthreads();
-  return t;
+  for (int r = 0; r < 16; ++r) {
+    const int rr = 8 * (r >> 2) + 4 * hf + (r & 3);
+    const int g = t / NTG, i = (t - g * NTG) * 32 + rr;
+    if (!(g < G && i < w && key < L && key <= L - w + i)) p[r] = 0.f;
+  }
 }
 
-// exclusive prefix over threads of a per-thread count; returns the prefix, *total gets the sum
-__device__ __forceinline__ int block_exclusive_scan(int v, int* sh, int* total) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  int inc = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(inc, o);
-    if (lane >= o) inc += y;
-  }
-  if (lane == 63) sh[wv] = inc;
-  __syncthreads();
-  int before = 0, tot = 0;
-#pragma unroll
-  for (int i = 0; i < kSelectThreads / 64; ++i) {
-    const int x = sh[i];
-    before += (i < wv) ? x : 0;
-    tot += x;
-  }
-  __syncthreads();
-  *total = tot;
-  return before + inc - v;
+// Window-row bookkeeping for row tile t, row-in-tile rr: whether the row exists and its position.
+template <int NTG>
+__device__ __forceinline__ bool row_visible(int t, int rr, int key, int G, int w, int L) {
+  const int g = t / NTG, i = (t - g * NTG) * 32 + rr;
+  return g < G && i < w && key < L && key <= L - w + i;
 }
 
-__global__ __launch_bounds__(kSelectThreads) void select_kernel(const PrefillLaunch P) {
-  extern __shared__ float sS[];
-  __shared__ int sh[kSelectThreads / 64 + 1];
-  const int tid = threadIdx.x;
-  const int hd = blockIdx.x;
+// ---------------------------------------------------------------------------------------------
+// The fused kernel.  NT = row tiles (G * NTG, padded), NTG = row tiles per query head.
+// ---------------------------------------------------------------------------------------------
+template <int NT, int NTG>
+__global__ __launch_bounds__(kThreads, 2) void evict_kernel(const PrefillLaunch P) {
+  constexpr int R = NT * 32;
+  constexpr int NG = NT / NTG;           // query heads per KV head supported by this instance
+  constexpr int kQBytes = R * kQStride * 2;
+  constexpr int kAuxA = kWaves * R * 2 * 4;
+  constexpr int kGroupsB = kThreads / R > 0 ? kThreads / R : 1;
+  constexpr int kAuxB = (NG * kChunk + R + kGroupsB * R * 2) * 4;
+  constexpr int kAuxBytes = kAuxA > kAuxB ? kAuxA : kAuxB;
+  constexpr int kItemBytes = kQBytes + kAuxBytes;
+  constexpr int kSelFixed = kHistBins * 4 + 64;
+  constexpr int kLdsBytes = kItemBytes > kSelFixed + 4096 ? kItemBytes : kSelFixed + 4096;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[kLdsBytes];
+  __shared__ int sInfo[4];
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hf = lane >> 5, ln = lane & 31;
+  uint32_t* counters = P.counters;
+  uint32_t* status = counters;
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_chunks;
-  const int h = hd % Hkv, s = (hd / Hkv) % B, slot = hd / (Hkv * B);
-  const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
-  const int bh = s * Hkv + h;
-  const float* Srow = P.S + (size_t)hd * L;
-  const bool snap = ly.rule == RKV_SNAPKV;
-  // candidate range over which scores are defined
-  const int n_score = ly.all ? (snap ? L - w : L) : ly.cand_end;
+  const int nH = B * P.n_scored * Hkv;
+  uint32_t* selDone = counters + 2;
 
-  for (int j = tid; j < n_score; j += kSelectThreads) sS[j] = Srow[j];
+  if (tid == 0) {
+    // Workgroups are dispatched in index order (round-robin over the XCDs), so the block index
+    // is the ticket: every item an item waits for has a smaller index and has been dispatched.
+    const Item it = decode_item((int64_t)blockIdx.x, P, nH);
+    sInfo[0] = it.type; sInfo[1] = it.head; sInfo[2] = it.chunk; sInfo[3] = it.part;
+  }
   __syncthreads();
-  // SnapKV: redo the pooled score of positions within pool_half of an interior chunk boundary
-  if (snap && P.pool_half > 0 && n_score > 0) {
-    const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
-    const float NEG_INF = -__builtin_inff();
-    const int npre = L - w;
-    for (int e = tid; e < (NC - 1) * twoP; e += kSelectThreads) {
-      const int cb = 1 + e / twoP, o = e - (e / twoP) * twoP;
-      const int bnd = cb * kChunk;
-      const int j = bnd - ph + o;
-      if (j < 0 || j >= npre || j >= n_score) continue;
-      const float* left = P.edge + ((size_t)hd * NC + (cb - 1)) * G * E;   // keys [bnd-2P, bnd) at [2P, 4P)
-      const float* right = P.edge + ((size_t)hd * NC + cb) * G * E;        // keys [bnd, bnd+2P) at [0, 2P)
-      const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
-      float sc = 0.f;
-      for (int g = 0; g < G; ++g) {
-        float m = NEG_INF;
-        for (int t = lo; t <= hi; ++t) {
-          const float a = (t < bnd) ? left[g * E + twoP + (t - (bnd - twoP))] : right[g * E + (t - bnd)];
-          m = fmaxf(m, a);
-        }
-        sc += m;
-      }
-      sS[j] = sc / (float)G;
-    }
-    __syncthreads();
-  }
-  if (ly.score) {
-    float* so = ly.score + (size_t)bh * L;
-    for (int j = tid; j < n_score; j += kSelectThreads) so[j] = sS[j];
-  }
+  const int type = sInfo[0], head = sInfo[1], chunk = sInfo[2], part = sInfo[3];
+  const float sl2 = P.scale_log2;
+  const float NEG_INF = -__builtin_inff();
 
-  int32_t* idx = ly.idx + (size_t)bh * ly.n_keep;
-  float* acc = ly.acc ? ly.acc + (size_t)bh * ly.n_keep : nullptr;
-  const float* accsrc = snap ? P.Su + (size_t)hd * L : Srow;
-  if (ly.all) {
-    for (int m = tid; m < ly.n_keep; m += kSelectThreads) {
-      idx[m] = m;
-      if (acc) acc[m] = accsrc[m];
+  // ============================================================== gather / copy items
+  if (type == kItemGather || type == kItemCopy) {
+    const int h = head % Hkv, s = (head / Hkv) % B, li = head / (Hkv * B);
+    const PrefillLayer& ly = P.layer[type == kItemGather ? P.slot_layer[li] : P.unscored_layer[li]];
+    const int bh = s * Hkv + h;
+    const int n_keep = ly.n_keep;
+    const int r0 = (int)((int64_t)part * n_keep / kGatherParts), r1 = (int)((int64_t)(part + 1) * n_keep / kGatherParts);
+    if (r1 <= r0) return;
+    if (type == kItemGather) {
+      if (tid == 0) wait_at_least(&selDone[head], 1u, status);
+      __syncthreads();
+    }
+    int32_t* idx = ly.idx + (size_t)bh * n_keep;
+    const size_t hbase = (size_t)bh * L;
+    const int piece = tid & 15, rsub = tid >> 4;
+    constexpr int kRowsPerPass = (kThreads / 16) * 8;   // 16 row groups x 8 rows in flight
+    for (int m0 = r0; m0 < r1; m0 += kRowsPerPass) {
+      int pos[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int m = m0 + rsub + 16 * u;
+        pos[u] = -1;
+        if (m < r1) {
+          if (type == kItemGather) pos[u] = load_coherent(idx + m);
+          else pos[u] = ly.all ? m : (m < ly.cand_end ? m : ly.forced_lo + (m - ly.cand_end));
+        }
+      }
+      u32x4 kv[8], vv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (pos[u] >= 0) {
+          const size_t src = (hbase + pos[u]) * kHeadDim + piece * 8;
+          kv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.k + src));
+          vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.v + src));
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int m = m0 + rsub + 16 * u;
+        if (pos[u] >= 0) {
+          const size_t dst = ((size_t)bh * n_keep + m) * kHeadDim + piece * 8;
+          __builtin_nontemporal_store(kv[u], reinterpret_cast<u32x4*>(ly.k_out + dst));
+          __builtin_nontemporal_store(vv[u], reinterpret_cast<u32x4*>(ly.v_out + dst));
+          if (type == kItemCopy && piece == 0) {
+            idx[m] = pos[u];
+            if (ly.acc) ly.acc[(size_t)bh * n_keep + m] = 0.f;
+          }
+        }
+      }
     }
     return;
   }
-  const int n = ly.cand_end, k = ly.k_sel;
-  if (k > 0) {
-    // k-th largest candidate score: largest pattern T with #(x >= T) >= k (scores are >= 0,
-    // so unsigned order of the bit patterns is the numeric order)
-    uint32_t prefix = 0u;
-    for (int bit = 30; bit >= 0; --bit) {
-      const uint32_t cand = prefix | (1u << bit);
-      int cnt = 0;
-      for (int j = tid; j < n; j += kSelectThreads) cnt += (__float_as_uint(sS[j]) >= cand) ? 1 : 0;
-      cnt = block_sum(cnt, sh);
-      if (cnt >= k) prefix = cand;
-    }
-    const uint32_t tau = prefix;
-    // ordered compaction over contiguous per-thread segments
-    const int seg = (n + kSelectThreads - 1) / kSelectThreads;
-    const int j0 = min(n, tid * seg), j1 = min(n, j0 + seg);
-    int gt = 0, eq = 0;
-    for (int j = j0; j < j1; ++j) {
-      const uint32_t x = __float_as_uint(sS[j]);
-      gt += x > tau;
-      eq += x == tau;
-    }
-    int tot_gt, tot_eq;
-    const int pre_gt = block_exclusive_scan(gt, sh, &tot_gt);
-    const int pre_eq = block_exclusive_scan(eq, sh, &tot_eq);
-    const int need = k - tot_gt;   // ties at tau taken in position order
-    int out = pre_gt + min(pre_eq, need);
-    int er = pre_eq;
-    for (int j = j0; j < j1; ++j) {
-      const uint32_t x = __float_as_uint(sS[j]);
-      bool take = x > tau;
-      if (x == tau) {
-        take = er < need;
-        ++er;
+
+  const int h = head % Hkv, s = (head / Hkv) % B, slot = head / (Hkv * B);
+  const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
+  const int bh = s * Hkv + h;
+  const bool snap = ly.rule == RKV_SNAPKV;
+
+  // ============================================================== select item
+  if (type == kItemSelect) {
+    int* sHist = reinterpret_cast<int*>(smem);
+    int* sScan = sHist + kHistBins;          // kWaves ints
+    int* sSel = sScan + 8;                   // 2 ints
+    float* sCache = reinterpret_cast<float*>(smem + kSelFixed);
+    const int cache_cap = (kLdsBytes - kSelFixed) / 4;
+    float* Srow = P.S + (size_t)head * L;
+    const int n_score = ly.all ? (snap ? L - w : L) : ly.cand_end;
+    const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
+    const bool fix = snap && ph > 0 && n_score > 0 && NC > 1;
+    const int n_edge = fix ? NC * G * E : 0;
+    const bool cached = n_score + n_edge <= cache_cap;
+    float* sEdge = sCache + n_score;          // chunk-edge column sums (cached path)
+    const float* Erow = P.edge + (size_t)head * NC * G * E;
+    // wait (bounded) until every score of the head is written (and the unpooled scores when they
+    // seed acc_out); keep the candidate scores and the chunk-edge values in LDS when they fit
+    const float* Surow = P.Su + (size_t)head * L;
+    const bool need_su = snap && ly.acc != nullptr;
+    for (int j0 = tid; j0 < L; j0 += kThreads * 8) {
+      float x[8], y[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kThreads;
+        x[u] = j < L ? load_coherent(Srow + j) : 0.f;
+        y[u] = (need_su && j < L) ? load_coherent(Surow + j) : 0.f;
       }
-      if (take) {
-        idx[out] = j;
-        if (acc) acc[out] = accsrc[j];
-        ++out;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kThreads;
+        uint32_t it = 0;
+        while (unwritten(x[u]) || unwritten(y[u])) {
+          __builtin_amdgcn_s_sleep(2);
+          x[u] = load_coherent(Srow + j);
+          if (need_su) y[u] = load_coherent(Surow + j);
+          if (++it > kSpinLimit) {
+            atomicOr(status, 1u);
+            x[u] = 0.f;
+            y[u] = 0.f;
+          }
+        }
+        if (cached && j < n_score) sCache[j] = x[u];
       }
+    }
+    auto edge_at = [&](int e) -> float {
+      float a = load_coherent(Erow + e);
+      uint32_t it = 0;
+      while (unwritten(a)) {
+        __builtin_amdgcn_s_sleep(2);
+        a = load_coherent(Erow + e);
+        if (++it > kSpinLimit) {
+          atomicOr(status, 1u);
+          a = 0.f;
+        }
+      }
+      return a;
+    };
+    if (fix && cached) {
+      for (int e0 = tid; e0 < n_edge; e0 += kThreads * 4) {
+        float a[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) a[u] = e0 + u * kThreads < n_edge ? load_coherent(Erow + e0 + u * kThreads) : 0.f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = e0 + u * kThreads;
+          if (e < n_edge) sEdge[e] = unwritten(a[u]) ? edge_at(e) : a[u];
+        }
+      }
+    }
+    __syncthreads();
+    // SnapKV: redo the pooled score of positions within pool_half of an interior chunk border
+    if (fix) {
+      const int npre = L - w;
+      for (int e = tid; e < (NC - 1) * twoP; e += kThreads) {
+        const int cb = 1 + e / twoP, o = e - (e / twoP) * twoP;
+        const int bnd = cb * kChunk;
+        const int j = bnd - ph + o;
+        if (j < 0 || j >= npre || j >= n_score) continue;
+        // chunk cb-1 holds keys [bnd-2P, bnd) at offsets [2P, 4P); chunk cb keys [bnd, bnd+2P) at [0, 2P)
+        const int left = (cb - 1) * G * E, right = cb * G * E;
+        const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
+        float sc = 0.f;
+        for (int g = 0; g < G; ++g) {
+          float m = NEG_INF;
+          for (int t = lo; t <= hi; ++t) {
+            const int ei = (t < bnd) ? left + g * E + twoP + (t - (bnd - twoP)) : right + g * E + (t - bnd);
+            m = fmaxf(m, cached ? sEdge[ei] : edge_at(ei));
+          }
+          sc += m;
+        }
+        if (cached) sCache[j] = sc / (float)G;
+        else store_coherent(Srow + j, sc / (float)G);
+      }
+      if (!cached) vmem_release();
+    }
+    __syncthreads();
+    auto get = [&](int j) -> float { return cached ? sCache[j] : load_coherent(Srow + j); };
+    if (ly.score) {
+      float* so = ly.score + (size_t)bh * L;
+      for (int j = tid; j < n_score; j += kThreads) so[j] = get(j);
+    }
+    int32_t* idx = ly.idx + (size_t)bh * ly.n_keep;
+    float* acc = ly.acc ? ly.acc + (size_t)bh * ly.n_keep : nullptr;
+    const float* accsrc = snap ? Surow : Srow;
+    if (ly.all) {
+      for (int m = tid; m < ly.n_keep; m += kThreads) store_coherent(idx + m, m);
+    } else {
+      const int n = ly.cand_end, k = ly.k_sel;
+      if (k > 0) {
+        // k-th largest candidate score: three radix passes over the 31 value bits (scores are
+        // >= 0, so the unsigned order of their bit patterns is the numeric order)
+        uint32_t prefix = 0u, pmask = 0u;
+        int kk = k;
+#pragma unroll 1
+        for (int pass = 0; pass < 3; ++pass) {
+          const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+          const int nb = pass == 0 ? 2048 : 1024;
+          for (int b = tid; b < nb; b += kThreads) sHist[b] = 0;
+          __syncthreads();
+          for (int j = tid; j < n; j += kThreads) {
+            const uint32_t x = __float_as_uint(get(j));
+            if ((x & pmask) == prefix) atomicAdd(&sHist[(x >> shift) & (nb - 1)], 1);
+          }
+          __syncthreads();
+          const int per = nb / kThreads;
+          int cnt = 0;
+          for (int i = 0; i < per; ++i) cnt += sHist[nb - 1 - (tid * per + i)];
+          int inc = cnt;  // inclusive scan of cnt over the workgroup
+#pragma unroll
+          for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(inc, o);
+            if (lane >= o) inc += y;
+          }
+          if (lane == 63) sScan[wv] = inc;
+          __syncthreads();
+          int above = inc - cnt;
+          for (int i = 0; i < wv; ++i) above += sScan[i];
+          if (kk > above && kk <= above + cnt) {
+            for (int i = 0; i < per; ++i) {
+              const int b = nb - 1 - (tid * per + i);
+              const int hb = sHist[b];
+              if (kk <= above + hb) {
+                sSel[0] = b;
+                sSel[1] = kk - above;
+                break;
+              }
+              above += hb;
+            }
+          }
+          __syncthreads();
+          prefix |= (uint32_t)sSel[0] << shift;
+          pmask |= (uint32_t)(nb - 1) << shift;
+          kk = sSel[1];
+          __syncthreads();
+        }
+        const uint32_t tau = prefix;
+        const int need = kk;  // ties at tau taken in position order
+        const int seg = (n + kThreads - 1) / kThreads;
+        const int j0 = min(n, tid * seg), j1 = min(n, j0 + seg);
+        int gt = 0, eq = 0;
+        for (int j = j0; j < j1; ++j) {
+          const uint32_t x = __float_as_uint(get(j));
+          gt += x > tau;
+          eq += x == tau;
+        }
+        const int v = gt | (eq << 16);   // exclusive scan of the packed counts
+        int inc = v;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(inc, o);
+          if (lane >= o) inc += y;
+        }
+        if (lane == 63) sScan[wv] = inc;
+        __syncthreads();
+        int pre = inc - v;
+        for (int i = 0; i < wv; ++i) pre += sScan[i];
+        const int pre_gt = pre & 0xffff, pre_eq = pre >> 16;
+        int out = pre_gt + min(pre_eq, need);
+        int er = pre_eq;
+        for (int j = j0; j < j1; ++j) {
+          const uint32_t x = __float_as_uint(get(j));
+          bool take = x > tau;
+          if (x == tau) {
+            take = er < need;
+            ++er;
+          }
+          if (take) {
+            store_coherent(idx + out, j);
+            ++out;
+          }
+        }
+      }
+      const int nf = ly.forced_hi - ly.forced_lo;
+      for (int t = tid; t < nf; t += kThreads) store_coherent(idx + k + t, ly.forced_lo + t);
+    }
+    vmem_release();
+    __syncthreads();
+    if (tid == 0) __hip_atomic_store(&selDone[head], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (acc) {
+      // scores of the retained positions (they seed decode-phase accumulation)
+      for (int m0 = tid; m0 < ly.n_keep; m0 += kThreads * 8) {
+        int pos[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) pos[u] = m0 + u * kThreads < ly.n_keep ? load_coherent(idx + m0 + u * kThreads) : -1;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (pos[u] >= 0) acc[m0 + u * kThreads] = load_coherent(accsrc + pos[u]);
+      }
+    }
+    return;
+  }
+
+  // ============================================================== stats and score items
+  uint16_t* sQ = reinterpret_cast<uint16_t*>(smem);
+  float* aux = reinterpret_cast<float*>(smem + kQBytes);
+  const int nt_used = G * NTG;
+  const int c = chunk;
+  const size_t head_base = (size_t)bh * L;
+  const uint16_t* khead = ly.k + head_base * kHeadDim;
+  const int wave_key0 = c * kChunk + wv * kKeysPerWave;
+  const bool padded_rows = (nt_used < NT) || (w != NTG * 32);
+
+  u32x4 kf[kKDepth][8];              // ring of key tiles: the current one and kKDepth-1 ahead
+#pragma unroll
+  for (int d = 0; d < kKDepth - 1; ++d) load_k_frag(kf[d], khead, wave_key0 + d * 32 + ln, L, hf);
+  load_q_to_lds<NT, NTG>(sQ, P, ly, s, h);
+  float* sMp = aux + NG * kChunk;     // score items: per-row log-normalisers
+  if (type == kItemScore) {
+    // fold every chunk's (max, sum) of this head into exp2 offsets M + log2(sum) per row,
+    // waiting (bounded) for chunks whose statistics are not written yet
+    constexpr int kGroups = kThreads / R > 0 ? kThreads / R : 1;
+    constexpr int kRowsPerPass = kThreads / kGroups;
+    float* sPart = sMp + R;           // [kGroups][R][2]
+    for (int r0 = 0; r0 < R; r0 += kRowsPerPass) {
+      const int r = r0 + tid % kRowsPerPass;
+      const int j = tid / kRowsPerPass;
+      float M = NEG_INF, Ls = 0.f;
+      const float* st0 = P.stats + (size_t)head * NC * R * 2 + 2 * r;
+      for (int c0 = j; c0 < NC; c0 += kGroups * 8) {
+        float2 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int cc = c0 + u * kGroups;
+          v[u] = cc < NC ? load_coherent2(st0 + (size_t)cc * R * 2) : make_float2(NEG_INF, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          uint32_t it = 0;
+          while (unwritten(v[u].x)) {
+            __builtin_amdgcn_s_sleep(2);
+            v[u] = load_coherent2(st0 + (size_t)(c0 + u * kGroups) * R * 2);
+            if (++it > kSpinLimit) {
+              atomicOr(status, 1u);
+              v[u] = make_float2(NEG_INF, 0.f);
+            }
+          }
+          combine_ms(M, Ls, v[u].x, v[u].y);
+        }
+      }
+      sPart[(j * R + r) * 2] = M;
+      sPart[(j * R + r) * 2 + 1] = Ls;
+    }
+    __syncthreads();
+    for (int r = tid; r < R; r += kThreads) {
+      float M = sPart[r * 2], Ls = sPart[r * 2 + 1];
+      for (int j = 1; j < kGroups; ++j) combine_ms(M, Ls, sPart[(j * R + r) * 2], sPart[(j * R + r) * 2 + 1]);
+      // probabilities are exp2(z - M - log2 L); rows without keys (padding) get +inf -> 0
+      sMp[r] = Ls > 0.f ? M + __log2f(Ls) : __builtin_inff();
     }
   }
-  const int nf = ly.forced_hi - ly.forced_lo;
-  for (int t = tid; t < nf; t += kSelectThreads) {
-    idx[k + t] = ly.forced_lo + t;
-    if (acc) acc[k + t] = accsrc[ly.forced_lo + t];
+  __syncthreads();
+
+  if (type == kItemStats) {
+    float run_m[NT], run_l[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) { run_m[t] = NEG_INF; run_l[t] = 0.f; }
+    // one key tile: logits for half of the row tiles at a time, then the running row
+    // max / sum; lane = window row ln of tile t, registers = keys tile_key0 + 8(r/4) + 4hf + r%4
+    auto tile = [&](const u32x4 (&kft)[8], int tile_key0) {
+      const bool need_mask = padded_rows || (tile_key0 + 32 > L - w);
+#pragma unroll
+      for (int half = 0; half < NT / kRowTilesPerPass; ++half) {
+        constexpr int NH = kRowTilesPerPass;
+        f32x16 acc[NH];
+        mfma_tile<NH, false>(acc, kft, sQ, ln, hf, half * NH, nt_used);
+#pragma unroll
+        for (int i = 0; i < NH; ++i) {
+          const int t = half * NH + i;
+          if (t >= nt_used) continue;
+          if (need_mask) mask_rows_lane<NTG>(acc[i], t, ln, hf, tile_key0, G, w, L);
+          float tm = acc[i][0];
+#pragma unroll
+          for (int r = 1; r < 16; ++r) tm = fmaxf(tm, acc[i][r]);
+          if (tm == NEG_INF) continue;
+          const float nm = fmaxf(run_m[t], tm * sl2);
+          float sm = run_l[t] * __builtin_amdgcn_exp2f(run_m[t] - nm);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sm += __builtin_amdgcn_exp2f(fmaf(acc[i][r], sl2, -nm));
+          run_m[t] = nm;
+          run_l[t] = sm;
+        }
+      }
+    };
+#pragma unroll 1
+    for (int base = 0; base < kTilesPerWave; base += kKDepth) {
+#pragma unroll
+      for (int i = 0; i < kKDepth; ++i) {
+        const int kt = base + i;
+        // keys kKDepth-1 tiles ahead load while this tile is multiplied and exponentiated
+        if (kt + kKDepth - 1 < kTilesPerWave)
+          load_k_frag(kf[(i + kKDepth - 1) % kKDepth], khead, wave_key0 + (kt + kKDepth - 1) * 32 + ln, L, hf);
+        if (wave_key0 + kt * 32 < L) tile(kf[i], wave_key0 + kt * 32);
+      }
+    }
+    // fold the two lanes that share a row, then the four waves
+    float* sRed = aux;  // [kWaves][R][2]
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const float m2 = __shfl_xor(run_m[t], 32), l2 = __shfl_xor(run_l[t], 32);
+      float M = run_m[t], Ls = run_l[t];
+      combine_ms(M, Ls, m2, l2);
+      if (hf == 0) {
+        sRed[(wv * R + t * 32 + ln) * 2] = M;
+        sRed[(wv * R + t * 32 + ln) * 2 + 1] = Ls;
+      }
+    }
+    __syncthreads();
+    float* stat = P.stats + ((size_t)head * NC + c) * R * 2;
+    for (int r = tid; r < R; r += kThreads) {
+      float M = NEG_INF, Ls = 0.f;
+#pragma unroll
+      for (int v = 0; v < kWaves; ++v) combine_ms(M, Ls, sRed[(v * R + r) * 2], sRed[(v * R + r) * 2 + 1]);
+      store_coherent2(stat + 2 * r, M, Ls);
+    }
+    return;
+  }
+
+  // ---------------------------------------------------------------- score item
+  float* sA = aux;  // [NG][kChunk] window column sums of this chunk per query head
+  // one key tile: probabilities for half of the row tiles at a time and their column sums per
+  // query head; lane = key tile_key0 + ln, registers = rows t*32 + 8(r/4) + 4hf + r%4
+  auto tile = [&](const u32x4 (&kft)[8], int tile_key0, int local0) {
+    const int key = tile_key0 + ln;
+    const bool need_mask = padded_rows || (tile_key0 + 32 > L - w);
+    float col[NG];
+#pragma unroll
+    for (int g = 0; g < NG; ++g) col[g] = 0.f;
+#pragma unroll
+    for (int half = 0; half < NT / kRowTilesPerPass; ++half) {
+      constexpr int NH = kRowTilesPerPass;
+      f32x16 acc[NH];
+      mfma_tile<NH, true>(acc, kft, sQ, ln, hf, half * NH, nt_used);
+#pragma unroll
+      for (int i = 0; i < NH; ++i) {
+        const int t = half * NH + i;
+        if (t >= nt_used) continue;
+        float mp[16];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float4 v = *reinterpret_cast<const float4*>(sMp + t * 32 + 8 * q + 4 * hf);
+          mp[4 * q] = v.x; mp[4 * q + 1] = v.y; mp[4 * q + 2] = v.z; mp[4 * q + 3] = v.w;
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][r] = __builtin_amdgcn_exp2f(fmaf(acc[i][r], sl2, -mp[r]));
+        if (need_mask) mask_rows_regs<NTG>(acc[i], t, hf, key, G, w, L);
+        float cs = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) cs += acc[i][r];
+        col[t / NTG] += cs;
+      }
+    }
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const float v = col[g] + __shfl_xor(col[g], 32);
+      if (hf == 0 && g < G) sA[g * kChunk + local0 + ln] = v;
+    }
+  };
+#pragma unroll 1
+  for (int base = 0; base < kTilesPerWave; base += kKDepth) {
+#pragma unroll
+    for (int i = 0; i < kKDepth; ++i) {
+      const int kt = base + i;
+      if (kt + kKDepth - 1 < kTilesPerWave)
+        load_k_frag(kf[(i + kKDepth - 1) % kKDepth], khead, wave_key0 + (kt + kKDepth - 1) * 32 + ln, L, hf);
+      if (wave_key0 + kt * 32 < L) tile(kf[i], wave_key0 + kt * 32, wv * kKeysPerWave + kt * 32);
+    }
+  }
+  __syncthreads();
+
+  // group mean (unpooled), in-chunk max-pool (SnapKV), scores and chunk-edge values
+  const int cbase = c * kChunk;
+  float* Srow = P.S + (size_t)head * L;
+  for (int kl = tid; kl < kChunk; kl += kThreads) {
+    const int key = cbase + kl;
+    if (key >= L) break;
+    float su = 0.f;
+    for (int g = 0; g < G; ++g) su += sA[g * kChunk + kl];
+    su = su / (float)G;
+    if (snap) {
+      const int npre = L - w;
+      float sc = su;
+      if (key < npre) {
+        const int ph = P.pool_half;
+        const int lo = max(key - ph, cbase), hi = min(min(key + ph, cbase + kChunk - 1), npre - 1);
+        sc = 0.f;
+        for (int g = 0; g < G; ++g) {
+          float m = NEG_INF;
+          for (int t = lo; t <= hi; ++t) m = fmaxf(m, sA[g * kChunk + t - cbase]);
+          sc += m;
+        }
+        sc = sc / (float)G;
+      }
+      store_coherent(Srow + key, sc);
+      if (P.want_unpooled) store_coherent(P.Su + (size_t)head * L + key, su);
+    } else {
+      store_coherent(Srow + key, su);
+    }
+  }
+  if (snap && P.pool_half > 0) {
+    const int E = 4 * P.pool_half, twoP = 2 * P.pool_half;
+    float* ed = P.edge + ((size_t)head * NC + c) * G * E;
+    for (int e = tid; e < G * E; e += kThreads) {
+      const int g = e / E, o = e - g * E;
+      const int kl = o < twoP ? o : kChunk - twoP + (o - twoP);
+      store_coherent(ed + e, (cbase + kl < L) ? sA[g * kChunk + kl] : 0.f);
+    }
   }
 }
 
-// ------------------------------------------------------------------------------------------
-// Gather: 16 consecutive threads copy one 256-byte row of K and of V.
-// ------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kGatherThreads) void gather_kernel(const PrefillLaunch P) {
-  const int64_t gid = (int64_t)blockIdx.x * kGatherThreads + threadIdx.x;
-  const int64_t row = gid >> 4;
-  const int piece = (int)(gid & 15);
-  if (row >= P.rows_prefix[P.n_layers]) return;
-  int li = 0;
-  while (li + 1 < P.n_layers && P.rows_prefix[li + 1] <= row) ++li;
-  const PrefillLayer& ly = P.layer[li];
-  const int64_t local = row - P.rows_prefix[li];
-  const int n_keep = ly.n_keep;
-  const int64_t bh = local / n_keep;
-  const int m = (int)(local - bh * n_keep);
-  int pos;
-  if (ly.slot >= 0) {
-    pos = ly.idx[bh * n_keep + m];
-  } else {
-    pos = ly.all ? m : (m < ly.cand_end ? m : ly.forced_lo + (m - ly.cand_end));
-    if (piece == 0) {
-      ly.idx[bh * n_keep + m] = pos;
-      if (ly.acc) ly.acc[bh * n_keep + m] = 0.f;
-    }
+template <int NT, int NTG>
+int resident_groups() {
+  static int cached = -1;
+  if (cached < 0) {
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, evict_kernel<NT, NTG>, kThreads, 0) != hipSuccess ||
+        per_cu < 1)
+      per_cu = 1;
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+      cus = 256;
+    cached = per_cu * cus;
   }
-  const int L = P.seq_len;
-  const size_t src = ((size_t)bh * L + pos) * kHeadDim + piece * 8;
-  const size_t dst = ((size_t)bh * n_keep + m) * kHeadDim + piece * 8;
-  const u32x4 kv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.k + src));
-  const u32x4 vv = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.v + src));
-  *reinterpret_cast<u32x4*>(ly.k_out + dst) = kv;
-  *reinterpret_cast<u32x4*>(ly.v_out + dst) = vv;
+  return cached;
+}
+
+template <int NT, int NTG>
+int launch_evict(PrefillLaunch P, hipStream_t st, void* stream) {
+  const int nH = P.batch * P.n_scored * P.n_kv_heads;
+  // Lags between a head's phases, in steps: about one resident round of workgroups between its
+  // stats and score items and between its score and select items (so those items rarely wait,
+  // and the score items still find the head's K in the on-die caches); the gather items only
+  // wait for the one select item.
+  const int per_step = 2 * P.n_chunks + 1 + kGatherParts;
+  const int round = (resident_groups<NT, NTG>() + per_step - 1) / per_step;
+  P.lag_score = round + 1;
+  P.lag_select = round + 1;
+  P.lag_gather = round / 3 + 1;
+  const int64_t scored = nH > 0 ? (int64_t)nH * (2 * P.n_chunks + 1 + kGatherParts) : 0;
+  const int64_t copies = (int64_t)P.n_unscored * P.batch * P.n_kv_heads * kGatherParts;
+  const int64_t total = scored + copies;
+  if (total <= 0) return 0;
+  if (total > 0x7fffffff) return (int)hipErrorInvalidValue;
+  P.n_tickets = (int)total;
+  profile_mark(kStageScore, false, stream);
+  evict_kernel<NT, NTG><<<(unsigned)total, kThreads, 0, st>>>(P);
+  profile_mark(kStageScore, true, stream);
+  return 0;
 }
 
 }  // namespace
 
 int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int n_heads = P.batch * P.n_scored * P.n_kv_heads;
-  if (P.n_scored > 0) {
-    const int nc = 2 + 2 * n_heads;
+  const int nH = P.batch * P.n_scored * P.n_kv_heads;
+  {
+    const int nc = 2 + nH;
+    const int64_t n_fill = nH > 0 ? P.fill_vec4 : 0;
+    int64_t blocks = (std::max<int64_t>(nc, n_fill) + 255) / 256;
+    if (blocks > 4096) blocks = 4096;
     profile_mark(kStageZero, false, stream);
-    zero_counters<<<(nc + 255) / 256, 256, 0, st>>>(P.counters, nc);
+    reset_workspace<<<(unsigned)blocks, 256, 0, st>>>(P.counters, nc, reinterpret_cast<u32x4*>(P.stats), n_fill);
     profile_mark(kStageZero, true, stream);
-    const unsigned grid = (unsigned)n_heads * (unsigned)P.n_chunks;
-    profile_mark(kStageScore, false, stream);
-    if (row_tiles == 4) score_kernel<4><<<grid, kThreads, 0, st>>>(P);
-    else score_kernel<8><<<grid, kThreads, 0, st>>>(P);
-    profile_mark(kStageScore, true, stream);
-    const size_t lds = sizeof(float) * (size_t)P.seq_len;
-    static bool attr_set = false;
-    if (!attr_set) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, 150 * 1024);
-      if (e != hipSuccess) return (int)e;
-      attr_set = true;
-    }
-    profile_mark(kStageSelect, false, stream);
-    select_kernel<<<n_heads, kSelectThreads, lds, st>>>(P);
-    profile_mark(kStageSelect, true, stream);
   }
-  const int64_t rows = P.rows_prefix[P.n_layers];
-  if (rows > 0) {
-    const int64_t threads = rows * 16;
-    const unsigned grid = (unsigned)((threads + kGatherThreads - 1) / kGatherThreads);
-    profile_mark(kStageGather, false, stream);
-    gather_kernel<<<grid, kGatherThreads, 0, st>>>(P);
-    profile_mark(kStageGather, true, stream);
-  }
+  int err = 0;
+  const int ntg = P.row_tiles_per_group;
+  if (row_tiles == 4 && ntg == 1) err = launch_evict<4, 1>(P, st, stream);
+  else if (row_tiles == 4 && ntg == 2) err = launch_evict<4, 2>(P, st, stream);
+  else if (row_tiles == 4) err = launch_evict<4, 4>(P, st, stream);
+  else if (ntg == 1) err = launch_evict<8, 1>(P, st, stream);
+  else if (ntg == 2) err = launch_evict<8, 2>(P, st, stream);
+  else if (ntg == 4) err = launch_evict<8, 4>(P, st, stream);
+  else err = launch_evict<8, 8>(P, st, stream);
+  if (err) return err;
   return (int)hipGetLastError();
 }
 

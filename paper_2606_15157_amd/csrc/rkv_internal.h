@@ -13,10 +13,10 @@ namespace rkv {
 
 constexpr int kHeadDim = 128;      // head_dim the kernels are built for
 constexpr int kMaxLayersPerLaunch = 32;
-constexpr int kChunk = 256;        // keys per scoring work item
+constexpr int kChunk = 768;        // keys per scoring work item (4 waves x 6 tiles of 32)
 constexpr int kMaxRowTiles = 8;    // G * ceil(w / 32) supported by the scoring kernel
 constexpr int kMaxPoolHalf = 64;   // pool_kernel / 2 supported
-constexpr int kMaxScoredSeqLen = 36864;  // select keeps one head's scores in LDS
+constexpr int kGatherParts = 4;    // gather work items per (sequence, layer, KV head)
 
 // Per-layer work description of one prefill launch group.
 struct PrefillLayer {
@@ -38,6 +38,11 @@ struct PrefillLayer {
   int32_t all;            // 1: every position kept (FULL or b >= L)
 };
 
+// One launch of the fused eviction kernel over a group of up to 32 layers.
+// Work items, in ticket order (ticket = atomic counter, so items start in this order):
+//   step s: stats items of head s, score items of head s - lag_score, the select item of head
+//   s - lag_score - lag_select and the gather items of head s - lag_score - lag_select -
+//   lag_gather; then the copy items of the layers that are not scored.  Heads are (scored slot, sequence, KV head) triples.
 struct PrefillLaunch {
   PrefillLayer layer[kMaxLayersPerLaunch];
   int32_t n_layers;
@@ -48,23 +53,29 @@ struct PrefillLaunch {
   int32_t n_chunks;       // ceil(L / kChunk)
   int32_t pool_half;      // pool_kernel / 2
   int32_t want_unpooled;  // write the unpooled score array (acc seeding) for SnapKV layers
+  int32_t lag_score;      // steps from a head's stats items to its score items
+  int32_t lag_select;     // steps from its score items to its select item
+  int32_t lag_gather;     // steps from its select item to its gather items
+  int32_t n_unscored;     // layers copied without scoring
+  int32_t n_tickets;      // total work items (= grid size)
   float scale_log2;       // log2(e) / sqrt(d)
   // workspace regions
-  uint32_t* counters;     // [0] status, [1] ticket, then arrive[n_heads], ready[n_heads]
-  float* stats;           // [n_heads][n_chunks][R][2]  chunk row max / sum
-  float* headstat;        // [n_heads][R][2]            head row max / reciprocal sum
+  uint32_t* counters;     // [0] status, [1] unused, then per head: selection done
+  // stats .. edge are contiguous; the reset kernel fills them with NaN ("not written yet")
+  float* stats;           // [n_heads][n_chunks][R][2]  chunk row max (log2 units) / sum
+  int64_t fill_vec4;      // 16-byte units from `stats` to the end of `edge`
   float* S;               // [n_heads][L]  ranking score
   float* Su;              // [n_heads][L]  unpooled group-mean score (SnapKV layers, if wanted)
   float* edge;            // [n_heads][n_chunks][G][4 * pool_half] per-query-head A at chunk edges
-  int64_t rows_prefix[kMaxLayersPerLaunch + 1];  // gather rows before each layer
   int32_t slot_layer[kMaxLayersPerLaunch];       // scored slot -> layer index in this group
+  int32_t unscored_layer[kMaxLayersPerLaunch];   // unscored layer list
 };
 
 static_assert(sizeof(PrefillLaunch) <= 4000, "kernel argument block too large");
 
 // Workspace layout for one launch group.
 struct PrefillWorkspace {
-  size_t counters, stats, headstat, S, Su, edge, total;
+  size_t counters, stats, S, Su, edge, end, total;
 };
 
 PrefillWorkspace prefill_workspace_layout(int n_heads, int n_chunks, int rows, int seq_len, int group,

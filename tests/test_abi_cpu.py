@@ -138,7 +138,7 @@ def call_prefill(plan, shape, io=True, ws=FAKE, ws_bytes=1 << 40, n=None, null_q
     ((1, 16, 32, 8, 128), 2),       # window (32) > seq_len
     ((0, 1024, 32, 8, 128), 2),     # empty batch
     ((1, 1024, 64, 2, 128), 4),     # G * ceil(w/32) = 32 row tiles > 8
-    ((1, 40000, 32, 8, 128), 4),    # scored seq_len above the supported maximum
+    ((1, (1 << 24) + 1, 32, 8, 128), 4),   # seq_len above 2^24
 ])
 def test_prefill_shape_errors(shape, status):
     plan = rkv.Plan([rkv.SNAPKV], [128])
