@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <mutex>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <numeric>
@@ -81,6 +82,24 @@ struct Group {
   int l0, l1, n_scored;
 };
 
+// Test hook: RKV_FORCE_TWO_PASS=1 selects the two-pass scoring kernel (normally used for prompts
+// too long for the single-pass one) so that it can be checked on short prompts too.
+int force_two_pass() {
+  const char* e = std::getenv("RKV_FORCE_TWO_PASS");
+  return (e && std::atoi(e) != 0) ? 1 : 0;
+}
+
+// Two-pass scoring: pass B trails pass A by this many items in each workgroup (RKV_SCORE_LAG
+// overrides it for tuning runs).
+int score_lag() {
+  static int lag = -1;
+  if (lag < 0) {
+    const char* e = std::getenv("RKV_SCORE_LAG");
+    lag = e ? std::max(0, std::atoi(e)) : 6;
+  }
+  return lag;
+}
+
 std::vector<Group> layer_groups(const rkv_plan* plan, int32_t L) {
   std::vector<Group> g;
   int n = (int)plan->layers.size();
@@ -97,10 +116,9 @@ size_t group_workspace(const rkv_plan* plan, const rkv_shape* s, const Group& g)
   const int L = s->seq_len;
   const int G = s->n_q_heads / s->n_kv_heads;
   const int nt = kernel_row_tiles(row_tiles(plan->params, s));
-  const int n_heads = s->batch * g.n_scored * s->n_kv_heads;
-  const int n_chunks = (L + rkv::kChunk - 1) / rkv::kChunk;
-  return rkv::prefill_workspace_layout(n_heads, n_chunks, nt * 32, L, G, plan->params.pool_kernel / 2, true)
-      .total;
+  const int n_jobs = s->batch * g.n_scored * s->n_kv_heads;
+  const int n_slices = (L + rkv::kSlice - 1) / rkv::kSlice;
+  return rkv::prefill_workspace_layout(n_jobs, n_slices, nt * 32, L, G, plan->params.pool_kernel / 2).total;
 }
 
 }  // namespace
@@ -135,20 +153,21 @@ int fail(int status, const std::string& msg) {
 
 void clear_error() { g_error.clear(); }
 
-PrefillWorkspace prefill_workspace_layout(int n_heads, int n_chunks, int rows, int seq_len, int group,
-                                          int pool_half, bool want_unpooled) {
+PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half) {
   PrefillWorkspace w{};
   size_t off = 0;
   w.counters = off;
-  off = round_up(off + sizeof(uint32_t) * (2 + (size_t)n_heads), 256);
+  off = round_up(off + sizeof(uint32_t) * (2 + 2 * (size_t)n_jobs), 256);
   w.stats = off;
-  off = round_up(off + sizeof(float) * 2 * (size_t)n_heads * n_chunks * rows, 256);
+  off = round_up(off + sizeof(float) * 2 * (size_t)n_jobs * n_slices * rows, 256);
+  w.lam = off;
+  off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
   w.S = off;
-  off = round_up(off + sizeof(float) * (size_t)n_heads * seq_len, 256);
+  off = round_up(off + sizeof(float) * (size_t)n_jobs * seq_len, 256);
   w.Su = off;
-  if (want_unpooled) off = round_up(off + sizeof(float) * (size_t)n_heads * seq_len, 256);
+  off = round_up(off + sizeof(float) * (size_t)n_jobs * seq_len, 256);
   w.edge = off;
-  off = round_up(off + sizeof(float) * (size_t)n_heads * n_chunks * group * 4 * std::max(pool_half, 1), 256);
+  off = round_up(off + sizeof(float) * (size_t)n_jobs * n_slices * group * 4 * std::max(pool_half, 1), 256);
   w.end = off;
   w.total = std::max<size_t>(off, 256);
   return w;
@@ -375,10 +394,12 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     P.window = p.window;
     P.group = G;
     P.row_tiles_per_group = (p.window + 31) / 32;
-    P.n_chunks = (L + rkv::kChunk - 1) / rkv::kChunk;
+    P.n_slices = (L + rkv::kSlice - 1) / rkv::kSlice;
     P.pool_half = p.pool_kernel / 2;
     P.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
-    int slot = 0, n_unscored = 0;
+    P.score_lag = score_lag();
+    P.force_two_pass = force_two_pass();
+    int slot = 0, n_gather = 0;
     bool want_unpooled = false;
     for (int i = 0; i < P.n_layers; ++i) {
       const int l = g.l0 + i;
@@ -405,20 +426,18 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
         P.slot_layer[slot] = i;
         if (d.rule == RKV_SNAPKV && d.acc) want_unpooled = true;
         ++slot;
-      } else if (lo.n_keep > 0) {
-        P.unscored_layer[n_unscored++] = i;
       }
+      if (lo.n_keep > 0) P.gather_layer[n_gather++] = i;
     }
     P.n_scored = slot;
-    P.n_unscored = n_unscored;
+    P.n_gather = n_gather;
     P.want_unpooled = want_unpooled ? 1 : 0;
-    const int n_heads = shape->batch * slot * shape->n_kv_heads;
-    rkv::PrefillWorkspace W =
-        rkv::prefill_workspace_layout(n_heads, P.n_chunks, ktiles * 32, L, G, P.pool_half, true);
+    const int n_jobs = shape->batch * slot * shape->n_kv_heads;
+    rkv::PrefillWorkspace W = rkv::prefill_workspace_layout(n_jobs, P.n_slices, ktiles * 32, L, G, P.pool_half);
     char* base = (char*)ws;
     P.counters = (uint32_t*)(base + W.counters);
     P.stats = (float*)(base + W.stats);
-    P.fill_vec4 = (int64_t)((W.end - W.stats) / 16);
+    P.lam = (float*)(base + W.lam);
     P.S = (float*)(base + W.S);
     P.Su = (float*)(base + W.Su);
     P.edge = (float*)(base + W.edge);

@@ -1,30 +1,34 @@
-// Prefill prompt compression for gfx950 (CDNA4): one fused kernel per launch group.
+// Prefill prompt compression for gfx950 (CDNA4).
 //
-// Per (sequence, scored layer, KV head) -- a "head" -- the window scores are
+// Per (sequence, scored layer, KV head) -- a "job" -- the window scores are (Section 2.1, the
+// SnapKV and H2O retention rules the route composes)
 //   A[g][j] = sum_i softmax_j(Q[g,i] . K[j] / sqrt(d))      (w window rows per query head g)
 //   S[j]    = mean_g maxpool(A[g])[j]  (SnapKV)  or  mean_g A[g][j]  (H2O)
-// The softmax of a window row is normalised over every key while the window sum runs over
-// rows, so a head is done in two passes over its keys, each split into 512-key chunks:
-//   stats item  (head, chunk): logits on MFMA (K chunk as the 32-row A operand, window queries
-//               from LDS as B), per-row running max and sum of exponentials; the last chunk of
-//               the head to finish folds all chunks into one log-normaliser per row;
-//   score item  (head, chunk): the same logits again (the chunk's K is re-read from the
-//               on-die caches: score items run a fixed number of steps after their head's stats
-//               items), probabilities exp2(z - normaliser), column sums per query head inside
-//               each lane (queries as the A operand put a key in every lane), max-pool inside
-//               the chunk, group mean -> S;
-//   select item (head): fixes the pooled score next to chunk borders, finds the k-th largest
-//               score with three radix-histogram passes, writes the retained positions in
-//               ascending order (ties at the k-th value taken by position);
-//   gather item (head, part): copies the retained K and V rows, 16 lanes x 16 B per row.
-// Layers that need no scores (StreamingLLM, Full, or budgets covering the prompt) get copy
-// items only.  Items take tickets from an atomic counter, so they start in ticket order; an item
-// waits only for items with earlier tickets (which never wait for later ones), and every wait is
-// bounded (on time-out the workspace status word is set and the item carries on).
+// A row's softmax is normalised over every key while the window sum runs over rows, so a row's
+// normaliser is known only once every key of the job has been seen.  Work items are (job,
+// slice of 128 keys); each of the four waves of a workgroup takes one 32-key tile of the slice.
+//   scoring kernel (persistent, two passes per item with a fixed lag between them):
+//     pass A streams the K tile from HBM into registers and multiplies it by the job's G*w
+//       query rows (in LDS) on MFMA with the keys as the A operand, so a lane holds one window
+//       row and the row max / sum of exp2 need no cross-lane work; the slice publishes them;
+//     the slice of a job that counts itself in last folds all slices into one log2-normaliser
+//       per row;
+//     pass B, `lag` items later, re-reads the tile (L2 / MALL) and multiplies with the queries
+//       as the A operand, so a lane holds one key; the accumulator starts at -normaliser, exp2
+//       gives probabilities and the window sum over rows stays inside the lane; max-pool inside
+//       the slice (SnapKV) and the group mean give S;
+//   select kernel (one workgroup per job): repairs the pooled score next to slice borders,
+//     finds the k-th largest score with three radix-histogram passes and writes the retained
+//     positions in ascending order;
+//   gather kernel: copies the retained K and V rows.
+// K is read from HBM once; the logits are formed twice (MFMA is not the bound, and no
+// exponentials have to be held across the wait for the normaliser).
 //
-// Data handed between workgroups goes through agent-scope relaxed atomics (they bypass the
-// XCD-local caches); ordering uses workgroup fences plus vmcnt(0) waits rather than agent-scope
-// fences, which would flush and invalidate L2.
+// Data handed between workgroups of one launch goes through agent-scope relaxed atomics
+// (they bypass the XCD-local caches); a slice counts itself in only after a vmcnt(0) wait has
+// retired its statistics stores, and normalisers are written once over a NaN "not written"
+// mark, so no agent-scope fence (which would flush and invalidate L2) is needed.  Every wait is
+// bounded: on time-out the workspace status word is set and the kernel carries on.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -42,29 +46,17 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;            // 4 waves, one per SIMD
 constexpr int kWaves = kThreads / 64;
-constexpr int kKeysPerWave = kChunk / kWaves;   // 128 keys = 4 tiles of 32
-constexpr int kTilesPerWave = kKeysPerWave / 32;
-constexpr int kKDepth = 2;               // key tiles in registers per wave (1 loading ahead)
-static_assert(kTilesPerWave % kKDepth == 0, "tile loop is unrolled by the ring depth");
-constexpr int kRowTilesPerPass = 1;      // row tiles whose accumulators are live at once
-constexpr int kQStride = 136;            // bf16 per LDS row of Q: 128 + 8 padding (272 B)
+static_assert(kSlice == kWaves * 32, "one 32-key tile per wave");
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kHistBins = 2048;
-
-enum ItemType { kItemStats = 0, kItemScore = 1, kItemSelect = 2, kItemGather = 3, kItemCopy = 4 };
+constexpr int kSelectLds = 128 * 1024;   // dynamic LDS of the select kernel (scores cached up to ~30K keys)
 
 __device__ __forceinline__ void store_coherent(float* p, float v) {
   __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void store_coherent(int32_t* p, int32_t v) {
-  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), (uint32_t)v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 __device__ __forceinline__ float load_coherent(const float* p) {
   return __uint_as_float(__hip_atomic_load(reinterpret_cast<const uint32_t*>(p), __ATOMIC_RELAXED,
                                            __HIP_MEMORY_SCOPE_AGENT));
-}
-__device__ __forceinline__ int32_t load_coherent(const int32_t* p) {
-  return (int32_t)__hip_atomic_load(reinterpret_cast<const uint32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void store_coherent2(float* p, float a, float b) {
   const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
@@ -87,7 +79,7 @@ __device__ __forceinline__ void vmem_acquire() {
 __device__ __forceinline__ void wait_at_least(uint32_t* flag, uint32_t target, uint32_t* status) {
   uint32_t it = 0;
   while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-    __builtin_amdgcn_s_sleep(2);
+    __builtin_amdgcn_s_sleep(1);
     if (++it > kSpinLimit) {
       atomicOr(status, 1u);
       break;
@@ -96,7 +88,7 @@ __device__ __forceinline__ void wait_at_least(uint32_t* flag, uint32_t target, u
   vmem_acquire();
 }
 
-// Online combination of (max, sum) pairs in log2 units.
+// Online combination of (max, sum) pairs in log2 units; empty pairs (sum 0) are skipped.
 __device__ __forceinline__ void combine_ms(float& M, float& S, float m, float l) {
   if (!(l > 0.f)) return;
   if (m > M) {
@@ -109,230 +101,1081 @@ __device__ __forceinline__ void combine_ms(float& M, float& S, float m, float l)
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// Clears the counters and fills the statistics, score and chunk-edge regions with the NaN
-// pattern that marks "not written yet" (every written value is a number).
-__global__ void reset_workspace(uint32_t* counters, int n_counters, u32x4* fill, int64_t n_fill) {
-  const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = i0; i < n_counters; i += stride) counters[i] = 0u;
-  const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
-  for (int64_t i = i0; i < n_fill; i += stride) fill[i] = nan4;
-}
+// Waits for every outstanding load of this wave.  Used right after a batch of loads whose values
+// feed predicated stores: with loads still pending at the branch joins, the compiler would wait
+// for all memory operations (earlier stores included) before every one of those stores.
+__device__ __forceinline__ void loads_done() { __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8)); }
 
-__device__ __forceinline__ bool unwritten(float x) { return x != x; }
-
-// ---------------------------------------------------------------------------------------------
-// Work-item decoding.
-// ---------------------------------------------------------------------------------------------
-__device__ __forceinline__ int64_t clampi(int64_t x, int64_t lo, int64_t hi) { return x < lo ? lo : (x > hi ? hi : x); }
-
-// Tickets issued before step s.  Step s holds the stats items of head s, the score items of
-// head s - lb, the select item of head s - lb - ls and the gather items of head s - lb - ls - lg.
-struct Lags {
-  int64_t b, s, g;
-};
-__device__ __forceinline__ int64_t step_prefix(int64_t s, int64_t nH, int64_t NC, const Lags& lag) {
-  return NC * clampi(s, 0, nH) + NC * clampi(s - lag.b, 0, nH) + clampi(s - lag.b - lag.s, 0, nH) +
-         (int64_t)kGatherParts * clampi(s - lag.b - lag.s - lag.g, 0, nH);
-}
-
-struct Item {
-  int type, head, chunk, part;
-};
-
-__device__ Item decode_item(int64_t t, const PrefillLaunch& P, int nH) {
-  Item it{};
-  const int64_t NC = P.n_chunks;
-  const Lags lag{P.lag_score, P.lag_select, P.lag_gather};
-  const int64_t n_steps = nH + lag.b + lag.s + lag.g;
-  const int64_t scored_total = nH > 0 ? step_prefix(n_steps, nH, NC, lag) : 0;
-  if (t >= scored_total) {
-    const int64_t u = t - scored_total;
-    it.type = kItemCopy;
-    it.part = (int)(u % kGatherParts);
-    it.head = (int)(u / kGatherParts);   // (unscored layer, sequence, KV head)
-    return it;
-  }
-  int64_t lo = 0, hi = n_steps - 1;      // largest s with prefix(s) <= t
-  while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) / 2;
-    if (step_prefix(mid, nH, NC, lag) <= t) lo = mid; else hi = mid - 1;
-  }
-  const int64_t s = lo;
-  int64_t w = t - step_prefix(s, nH, NC, lag);
-  if (s < nH) {
-    if (w < NC) { it.type = kItemStats; it.head = (int)s; it.chunk = (int)w; return it; }
-    w -= NC;
-  }
-  const int64_t hb = s - lag.b, hs = hb - lag.s, hg = hs - lag.g;
-  if (hb >= 0 && hb < nH) {
-    if (w < NC) { it.type = kItemScore; it.head = (int)hb; it.chunk = (int)w; return it; }
-    w -= NC;
-  }
-  if (hs >= 0 && hs < nH) {
-    if (w < 1) { it.type = kItemSelect; it.head = (int)hs; return it; }
-    w -= 1;
-  }
-  it.type = kItemGather;
-  it.head = (int)hg;
-  it.part = (int)w;
-  return it;
+// Zeroes the counters and marks every per-row normaliser "not written" (NaN).
+__global__ void reset_counters(uint32_t* counters, int n, uint32_t* lam, int n_lam) {
+  const int i0 = blockIdx.x * blockDim.x + threadIdx.x, stride = gridDim.x * blockDim.x;
+  for (int i = i0; i < n; i += stride) counters[i] = 0u;
+  for (int i = i0; i < n_lam; i += stride) lam[i] = 0xffffffffu;
 }
 
 // ---------------------------------------------------------------------------------------------
-// Shared pieces of the stats and score items.
+// Cross-lane sums over the 32 window rows held by the lanes of each half-wave.
 // ---------------------------------------------------------------------------------------------
-template <int NT, int NTG>
-__device__ __forceinline__ void load_q_to_lds(uint16_t* sQ, const PrefillLaunch& P, const PrefillLayer& ly, int s, int h) {
-  constexpr int R = NT * 32;
-  constexpr int kPer = R * 16 / kThreads;   // 16-byte pieces per thread
-  const int G = P.group, w = P.window;
-  const uint16_t* qb = ly.q + (size_t)(s * P.n_q_heads + h * G) * w * kHeadDim;
-  u32x4 val[kPer];
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+// One halving step between lane pairs (permutation CTRL pairs each lane with one whose `bit` is
+// the opposite): value pair (a, b) becomes a-sum in lanes with bit 0 and b-sum in lanes with bit 1.
+template <int CTRL, int N, int V>
+__device__ __forceinline__ void dpp_halve(float (&v)[V], int bit) {
+  if constexpr (N == 1) {
+    v[0] += dppf<CTRL>(v[0]);
+  } else {
 #pragma unroll
-  for (int i = 0; i < kPer; ++i) {       // all loads in flight together
-    const int e = threadIdx.x + i * kThreads;
-    const int row = e >> 4, piece = e & 15;
-    const int t = row >> 5;
-    const int g = t / NTG, ii = (t - g * NTG) * 32 + (row & 31);
-    val[i] = u32x4{0u, 0u, 0u, 0u};
-    if (g < G && ii < w) val[i] = *reinterpret_cast<const u32x4*>(qb + (size_t)(g * w + ii) * kHeadDim + piece * 8);
-  }
-#pragma unroll
-  for (int i = 0; i < kPer; ++i) {
-    const int e = threadIdx.x + i * kThreads;
-    *reinterpret_cast<u32x4*>(sQ + (e >> 4) * kQStride + (e & 15) * 8) = val[i];
+    for (int i = 0; i < N / 2; ++i) {
+      const float a = v[2 * i], b = v[2 * i + 1];
+      const float keep = bit ? b : a, send = bit ? a : b;
+      v[i] = keep + dppf<CTRL>(send);
+    }
   }
 }
+// Reduce-scatter of V values per lane over the 32 lanes of each half-wave.  Afterwards lane l
+// holds max(V / 32, 1) sums: value i is the sum of original value 32 i + sel(l) (V >= 32), or
+// of value sel(l) & 15 (V = 16, duplicated in lanes l and l ^ 1), where
+// sel(l) = bit4(l) | bit3(l) << 1 | bit2(l) << 2 | bit1(l) << 3 | bit0(l) << 4.
+template <int V>
+__device__ __forceinline__ void reduce_scatter32(float (&v)[V], int lane) {
+  static_assert(V == 16 || V == 32 || V == 64 || V == 128, "unsupported value count");
+  constexpr int N1 = V / 2;
+#pragma unroll
+  for (int i = 0; i < N1; ++i) {   // lanes l and l ^ 16: rows 0/1 and 2/3 of 16 lanes swap halves
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[2 * i]), __float_as_uint(v[2 * i + 1]), false,
+                                                    false);
+    v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  dpp_halve<0x128, N1, V>(v, (lane >> 3) & 1);        // row_ror:8   -> lane l ^ 8
+  dpp_halve<0x141, N1 / 2, V>(v, (lane >> 2) & 1);    // row_half_mirror -> 7 - l within 8
+  dpp_halve<0x4E, N1 / 4, V>(v, (lane >> 1) & 1);     // quad_perm [2,3,0,1] -> l ^ 2
+  dpp_halve<0xB1, N1 / 8, V>(v, lane & 1);            // quad_perm [1,0,3,2] -> l ^ 1
+}
+// The same reduce-scatter on NV accumulator vectors in place (value i = e[i / 16][i % 16]).
+template <int CTRL, int N, int NV>
+__device__ __forceinline__ void dpp_halve_v(f32x16 (&e)[NV], int bit) {
+  if constexpr (N == 1) {
+    e[0][0] += dppf<CTRL>(e[0][0]);
+  } else {
+#pragma unroll
+    for (int i = 0; i < N / 2; ++i) {
+      const float a = e[(2 * i) >> 4][(2 * i) & 15], b = e[(2 * i + 1) >> 4][(2 * i + 1) & 15];
+      const float keep = bit ? b : a, send = bit ? a : b;
+      e[i >> 4][i & 15] = keep + dppf<CTRL>(send);
+    }
+  }
+}
+template <int NV>
+__device__ __forceinline__ void reduce_scatter32_v(f32x16 (&e)[NV], int lane) {
+  constexpr int V = NV * 16;
+  static_assert(V == 16 || V == 32 || V == 64 || V == 128, "unsupported value count");
+  constexpr int N1 = V / 2;
+#pragma unroll
+  for (int i = 0; i < N1; ++i) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(e[(2 * i) >> 4][(2 * i) & 15]),
+                                                    __float_as_uint(e[(2 * i + 1) >> 4][(2 * i + 1) & 15]), false, false);
+    e[i >> 4][i & 15] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
+  }
+  dpp_halve_v<0x128, N1, NV>(e, (lane >> 3) & 1);
+  dpp_halve_v<0x141, N1 / 2, NV>(e, (lane >> 2) & 1);
+  dpp_halve_v<0x4E, N1 / 4, NV>(e, (lane >> 1) & 1);
+  dpp_halve_v<0xB1, N1 / 8, NV>(e, lane & 1);
+}
+__device__ __forceinline__ int rs_sel(int lane) {
+  return ((lane >> 4) & 1) | (((lane >> 3) & 1) << 1) | (((lane >> 2) & 1) << 2) | (((lane >> 1) & 1) << 3) |
+         ((lane & 1) << 4);
+}
 
-// Lane of a 32-key tile: key `key` (clamped into the head), dims 64*hf + [0, 64).
-__device__ __forceinline__ void load_k_frag(u32x4 (&kf)[8], const uint16_t* khead, int key, int L, int hf) {
+// ---------------------------------------------------------------------------------------------
+// Operand staging.
+// ---------------------------------------------------------------------------------------------
+// The job's query rows in LDS: R rows of 256 B in 16-byte chunks, chunk c of row r at
+// position 16 r + (c ^ (r & 15)), so the 32 rows one MFMA fragment read touches sit in distinct
+// banks.  Loaded by LDS DMA (each wave instruction fills 1 KB); padding rows (query head >= G
+// or window row >= w) are filled from row 0 and masked later.
+template <int NRT, int NTH>
+__device__ __forceinline__ void issue_q_to_lds(uint16_t* sQ, const uint16_t* qjob, int G, int w) {
+  constexpr int R = NRT * 32;
+  constexpr int kPerWave = R * 16 / kThreads;   // instructions per wave
+  int lane = threadIdx.x & 63;
+  asm volatile("" : "+v"(lane));               // recompute the lane addresses here, do not keep them live
+  const int wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < kPerWave; ++i) {
+    const int base = (i * kWaves + wv) * 64;    // first chunk this instruction writes
+    const int x = base + lane;
+    const int row = x >> 4, c = (x & 15) ^ (row & 15);
+    const int g = row / (NTH * 32), ii = row - g * (NTH * 32);
+    const size_t off = (g < G && ii < w) ? (size_t)(g * w + ii) * kHeadDim : 0;
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(qjob + off + c * 8),
+        (__attribute__((address_space(3))) void*)(sQ + base * 8), 16, 0, 0);
+  }
+}
+__device__ __forceinline__ bf16x8 q_frag(const uint16_t* sQ, int row, int chunk) {
+  return *reinterpret_cast<const bf16x8*>(sQ + (row * 16 + (chunk ^ (row & 15))) * 8);
+}
+// A-operand lanes of one 32-key tile: key `key` (clamped into the job), dims 64*hf + [0, 64).
+__device__ __forceinline__ void load_k_tile(u32x4 (&kf)[8], const uint16_t* khead, int key, int L, int hf) {
   key = key < L ? key : L - 1;
-  const uint16_t* kp = khead + (size_t)key * kHeadDim + hf * 64;
+  const u32x4* kp = reinterpret_cast<const u32x4*>(khead + (size_t)key * kHeadDim + hf * 64);
 #pragma unroll
-  for (int st = 0; st < 8; ++st) kf[st] = *reinterpret_cast<const u32x4*>(kp + st * 8);
+  for (int st = 0; st < 8; ++st) kf[st] = kp[st];
 }
 
-// One 32-key tile against NH row tiles starting at t0: 8 k-steps of 16 dims.  KEYS_AS_COLUMNS = false puts
-// the keys on the MFMA A operand (output lane = window row), true puts the window queries on A
-// (output lane = key).  The scheduling barriers keep the compiler from hoisting all 32 query
-// fragment reads from LDS ahead of the MFMAs (that costs 128 VGPRs).
-template <int NH, bool KEYS_AS_COLUMNS>
-__device__ __forceinline__ void mfma_tile(f32x16 (&acc)[NH], const u32x4 (&kf)[8], const uint16_t* sQ, int ln, int hf,
-                                          int t0, int nt_used) {
+struct JobRef {
+  int job, slice, slot, s, h;
+};
+__device__ __forceinline__ JobRef decode_item(int64_t it, int nsl, int B, int Hkv) {
+  JobRef r;
+  r.job = (int)(it / nsl);
+  r.slice = (int)(it - (int64_t)r.job * nsl);
+  r.h = r.job % Hkv;
+  r.s = (r.job / Hkv) % B;
+  r.slot = r.job / (Hkv * B);
+  return r;
+}
+// Moves an item reference forward by n_wg items (= dj jobs and ds slices) with carries, so a
+// persistent workgroup walks its items without divisions.
+__device__ __forceinline__ void advance(JobRef& r, int dj, int ds, int nsl, int B, int Hkv) {
+  r.slice += ds;
+  int j = dj;
+  if (r.slice >= nsl) {
+    r.slice -= nsl;
+    ++j;
+  }
+  r.job += j;
+  r.h += j;
+  while (r.h >= Hkv) {
+    r.h -= Hkv;
+    if (++r.s == B) {
+      r.s = 0;
+      ++r.slot;
+    }
+  }
+}
+
+// Group mean, max-pool inside the slice (SnapKV, clipped to the prefix [0, L - w)), scores and
+// the slice-edge column sums the select kernel uses to redo the pool next to slice borders.
+// sCol[g][kl] holds the window column sum of key cbase + kl for query head g (SnapKV with G > 1)
+// or the sum over the group (otherwise).  Thread = (key, query-head half) for SnapKV.
+template <int NG>
+__device__ __forceinline__ void store_scores(const PrefillLaunch& P, bool snap, int job, int slice, int cbase,
+                                             const float (*sCol)[kSlice], float inv_g) {
+  const int tid = threadIdx.x, L = P.seq_len, w = P.window, G = P.group, nsl = P.n_slices;
+  const float NEG_INF = -__builtin_inff();
+  float* Srow = P.S + (size_t)job * L;
+  if (snap) {
+    const int kl = tid >> 1, kk = cbase + kl, npre = L - w, ph = P.pool_half;
+    const int g0 = (tid & 1) * ((G + 1) >> 1), g1 = min(G, g0 + ((G + 1) >> 1));
+    float su = 0.f, sc = 0.f;
+    if (kk < L) {
+      const int lo = max(kk - ph, cbase) - cbase, hi = min(min(kk + ph, cbase + kSlice - 1), npre - 1) - cbase;
+      for (int g = g0; g < g1; ++g) {
+        const float* cg = sCol[NG > 1 ? g : 0];
+        su += cg[kl];
+        float m = NEG_INF;
+        if (ph == 3) {   // the common 7-wide pool: independent reads
+          float x[7];
 #pragma unroll
-  for (int i = 0; i < NH; ++i)
+          for (int u = 0; u < 7; ++u) {
+            const int q = kl - 3 + u;
+            x[u] = (q >= lo && q <= hi) ? cg[q] : NEG_INF;
+          }
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
-#pragma unroll
-  for (int st = 0; st < 8; ++st) {
-    const bf16x8 kb = as_bf16x8(kf[st]);
-#pragma unroll
-    for (int i = 0; i < NH; ++i) {
-      if (t0 + i < nt_used) {
-        const bf16x8 qf = *reinterpret_cast<const bf16x8*>(sQ + ((t0 + i) * 32 + ln) * kQStride + hf * 64 + st * 8);
-        if (KEYS_AS_COLUMNS) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qf, kb, acc[i], 0, 0, 0);
-        else acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kb, qf, acc[i], 0, 0, 0);
+          for (int u = 0; u < 7; ++u) m = fmaxf(m, x[u]);
+        } else {
+          for (int u = lo; u <= hi; ++u) m = fmaxf(m, cg[u]);
+        }
+        sc += m;
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
+    su += __shfl_xor(su, 1);
+    sc += __shfl_xor(sc, 1);
+    if ((tid & 1) == 0 && kk < L) {
+      su *= inv_g;
+      Srow[kk] = kk < npre ? sc * inv_g : su;
+      if (P.want_unpooled) P.Su[(size_t)job * L + kk] = su;
+    }
+    if (ph > 0) {
+      const int E = 4 * ph, twoP = 2 * ph;
+      float* ed = P.edge + ((size_t)job * nsl + slice) * G * E;
+      for (int e = tid; e < G * E; e += kThreads) {
+        const int g = e / E, o = e - g * E;
+        const int kl2 = o < twoP ? o : kSlice - twoP + (o - twoP);
+        ed[e] = (cbase + kl2 < L) ? sCol[NG > 1 ? g : 0][kl2] : 0.f;
+      }
+    }
+  } else if (tid < kSlice && cbase + tid < L) {
+    Srow[cbase + tid] = sCol[0][tid] * inv_g;
   }
 }
 
-// Masking of one accumulator tile (causal inside the window, ragged tail, padding rows).
-template <int NTG>
-__device__ __forceinline__ void mask_rows_lane(f32x16& acc, int t, int ln, int hf, int tile_key0, int G, int w, int L) {
-  // lane = window row ln of tile t, registers = keys tile_key0 + 8(r/4) + 4hf + r%4
-  const int g = t / NTG, i = (t - g * NTG) * 32 + ln;
-  const bool valid = g < G && i < w;
-  const int last = min(L - 1, L - w + i);
+// The last slice of a job to count itself in folds every slice's (max, sum) into one
+// log2-normaliser per row (max + log2(sum), +inf for rows without visible keys).  The
+// normalisers start as NaN ("not written") and are read back through coherent loads.
+template <int R>
+__device__ void fold_job(const PrefillLaunch& P, int job, float2 (*sPart)[R]) {
+  constexpr int kGroups = kThreads / R;
+  static_assert(kGroups >= 1 && kGroups <= kWaves, "rows per workgroup");
+  const int tid = threadIdx.x, nsl = P.n_slices;
+  const int r = tid % R, j = tid / R;
+  float M = -__builtin_inff(), Z = 0.f;
+  const float* st = P.stats + (size_t)job * nsl * R * 2 + 2 * r;
+  for (int c0 = j; c0 < nsl; c0 += kGroups * 16) {
+    float2 v[16];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int kk = tile_key0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-    if (!valid || kk > last) acc[r] = -__builtin_inff();
+    for (int u = 0; u < 16; ++u) {
+      const int cc = c0 + u * kGroups;
+      v[u] = cc < nsl ? load_coherent2(st + (size_t)cc * R * 2) : make_float2(-__builtin_inff(), 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) combine_ms(M, Z, v[u].x, v[u].y);
   }
-}
-template <int NTG>
-__device__ __forceinline__ void mask_rows_regs(f32x16& p, int t, int hf, int key, int G, int w, int L) {
-  // lane = key, registers = window rows t*32 + 8(r/4) + 4hf + r%4
+  sPart[j][r] = make_float2(M, Z);
+  __syncthreads();
+  if (tid < R) {
+    float m = sPart[0][tid].x, z = sPart[0][tid].y;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int rr = 8 * (r >> 2) + 4 * hf + (r & 3);
-    const int g = t / NTG, i = (t - g * NTG) * 32 + rr;
-    if (!(g < G && i < w && key < L && key <= L - w + i)) p[r] = 0.f;
+    for (int q = 1; q < kGroups; ++q) combine_ms(m, z, sPart[q][tid].x, sPart[q][tid].y);
+    store_coherent(P.lam + (size_t)job * R + tid, z > 0.f ? m + __log2f(z) : __builtin_inff());
   }
 }
 
-// Window-row bookkeeping for row tile t, row-in-tile rr: whether the row exists and its position.
-template <int NTG>
-__device__ __forceinline__ bool row_visible(int t, int rr, int key, int G, int w, int L) {
-  const int g = t / NTG, i = (t - g * NTG) * 32 + rr;
-  return g < G && i < w && key < L && key <= L - w + i;
+// Fold used by the single-pass kernel: thread = (row pair, slice group); the statistics of up to
+// 8 slices per thread are loaded together (16 B each) before they are combined.
+template <int R>
+__device__ void fold_job_pairs(const PrefillLaunch& P, int job, float2 (*sPart)[R]) {
+  constexpr int kPairs = R / 2;
+  constexpr int kGroups = kThreads / kPairs;     // slice groups
+  static_assert(kGroups >= 1 && kGroups * 2 <= 2 * kWaves, "partials fit the statistics buffer");
+  const int tid = threadIdx.x, nsl = P.n_slices;
+  const int pr = tid % kPairs, j = tid / kPairs;
+  float M0 = -__builtin_inff(), Z0 = 0.f, M1 = -__builtin_inff(), Z1 = 0.f;
+  const float* st = P.stats + (size_t)job * nsl * R * 2 + 4 * pr;
+  for (int c0 = j; c0 < nsl; c0 += kGroups * 8) {
+    float4 v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int cc = c0 + u * kGroups;
+      if (cc < nsl) {
+        const float2 a = load_coherent2(st + (size_t)cc * R * 2), b = load_coherent2(st + (size_t)cc * R * 2 + 2);
+        v[u] = make_float4(a.x, a.y, b.x, b.y);
+      } else {
+        v[u] = make_float4(-__builtin_inff(), 0.f, -__builtin_inff(), 0.f);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      combine_ms(M0, Z0, v[u].x, v[u].y);
+      combine_ms(M1, Z1, v[u].z, v[u].w);
+    }
+  }
+  sPart[j][2 * pr] = make_float2(M0, Z0);
+  sPart[j][2 * pr + 1] = make_float2(M1, Z1);
+  __syncthreads();
+  if (tid < R) {
+    float m = sPart[0][tid].x, z = sPart[0][tid].y;
+#pragma unroll
+    for (int q = 1; q < kGroups; ++q) combine_ms(m, z, sPart[q][tid].x, sPart[q][tid].y);
+    store_coherent(P.lam + (size_t)job * R + tid, z > 0.f ? m + __log2f(z) : __builtin_inff());
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
-// The fused kernel.  NT = row tiles (G * NTG, padded), NTG = row tiles per query head.
+// Single-pass scoring (prompts whose slices of one job fit in the resident workgroups at once).
+// Workgroup w takes items w, w + n_wg, ...; per item the four waves each multiply one 32-key
+// tile of K (A operand, straight from HBM) by the job's query rows (B operand, LDS):
+//   lane = window row, registers = 16 keys -> tile row max, e = exp2(z - max) and row sums stay
+//   in the lane; the slice publishes (max, sum) per row and counts itself in; the last slice of
+//   the job folds all slices into one log2-normaliser per row (NaN until written);
+//   every slice keeps e in registers, waits for the normalisers, rescales e into probabilities
+//   and sums them over the window rows with a 32-lane reduce-scatter (permlane16 swap + DPP),
+//   per query head for SnapKV, over the group for H2O; pooling and the group mean give S.
+// Three workgroups share a CU, so while one waits for its job's normalisers the others compute.
 // ---------------------------------------------------------------------------------------------
-template <int NT, int NTG>
-__global__ __launch_bounds__(kThreads, 2) void evict_kernel(const PrefillLaunch P) {
-  constexpr int R = NT * 32;
-  constexpr int NG = NT / NTG;           // query heads per KV head supported by this instance
-  constexpr int kQBytes = R * kQStride * 2;
-  constexpr int kAuxA = kWaves * R * 2 * 4;
-  constexpr int kGroupsB = kThreads / R > 0 ? kThreads / R : 1;
-  constexpr int kAuxB = (NG * kChunk + R + kGroupsB * R * 2) * 4;
-  constexpr int kAuxBytes = kAuxA > kAuxB ? kAuxA : kAuxB;
-  constexpr int kItemBytes = kQBytes + kAuxBytes;
-  constexpr int kSelFixed = kHistBins * 4 + 64;
-  constexpr int kLdsBytes = kItemBytes > kSelFixed + 4096 ? kItemBytes : kSelFixed + 4096;
-  __shared__ __attribute__((aligned(16))) unsigned char smem[kLdsBytes];
-  __shared__ int sInfo[4];
+template <int NRT, int NTH>
+__global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel(const PrefillLaunch P, int n_wg) {
+  constexpr int R = NRT * 32;
+  constexpr int NG = NRT / NTH;
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[R * kHeadDim];
+  __shared__ float2 sStat[kWaves][R];
+  __shared__ float sLam[R];
+  __shared__ float sCol[NG][kSlice];
+  __shared__ int sFlag;
 
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hf = lane >> 5, ln = lane & 31;
-  uint32_t* counters = P.counters;
-  uint32_t* status = counters;
-  const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_chunks;
-  const int nH = B * P.n_scored * Hkv;
-  uint32_t* selDone = counters + 2;
-
-  if (tid == 0) {
-    // Workgroups are dispatched in index order (round-robin over the XCDs), so the block index
-    // is the ticket: every item an item waits for has a smaller index and has been dispatched.
-    const Item it = decode_item((int64_t)blockIdx.x, P, nH);
-    sInfo[0] = it.type; sInfo[1] = it.head; sInfo[2] = it.chunk; sInfo[3] = it.part;
-  }
-  __syncthreads();
-  const int type = sInfo[0], head = sInfo[1], chunk = sInfo[2], part = sInfo[3];
+  const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
+  const int nsl = P.n_slices;
+  const int n_jobs = B * P.n_scored * Hkv;
+  const int64_t n_items = (int64_t)n_jobs * nsl;
   const float sl2 = P.scale_log2;
+  const float inv_g = 1.f / (float)G;
+  const float NEG_INF = -__builtin_inff();
+  uint32_t* status = P.counters;
+  uint32_t* arrive = P.counters + 2;
+  const bool padded_rows = (G * NTH < NRT) || (w != NTH * 32);
+
+  const int64_t first = blockIdx.x;
+  if (first >= n_items) return;
+  const int T = (int)((n_items - 1 - first) / n_wg + 1);
+  const int dj = n_wg / nsl, ds = n_wg - dj * nsl;   // item stride n_wg in (jobs, slices)
+  auto q_of = [&](const JobRef& j) -> const uint16_t* {
+    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
+    return ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim;
+  };
+  auto k_tile = [&](u32x4 (&dst)[8], const JobRef& j) {
+    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
+    load_k_tile(dst, ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim, j.slice * kSlice + wv * 32 + ln, L, hf);
+  };
+
+  u32x4 kf[8];
+  JobRef jc = decode_item(first, nsl, B, Hkv);
+  issue_q_to_lds<NRT, NTH>(sQ, q_of(jc), G, w);
+  k_tile(kf, jc);
+
+#pragma unroll 1
+  for (int t = 0; t < T; ++t) {
+    const PrefillLayer& ly = P.layer[P.slot_layer[jc.slot]];
+    const bool snap = ly.rule == RKV_SNAPKV;
+    const int job = jc.job, cbase = jc.slice * kSlice, tile_key0 = cbase + wv * 32;
+    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // this item's query block and K tile
+    __syncthreads();
+
+    // ---- logits and exponentials: lane = window row ln of row tile rt, registers = keys
+    // tile_key0 + 8(r/4) + 4hf + r%4
+    f32x16 e[NRT];
+    float mw[NRT];   // tile row max in log2 units (0 for rows with no visible key in the tile)
+    const bool mask_a = padded_rows || tile_key0 + 32 > L - w;
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) e[rt][r] = 0.f;
+#pragma unroll
+      for (int st = 0; st < 8; ++st)
+        e[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[st]), q_frag(sQ, rt * 32 + ln, 8 * hf + st), e[rt],
+                                                        0, 0, 0);
+      if (mask_a) {
+        const int g = rt / NTH, ii = (rt - g * NTH) * 32 + ln;
+        const int last = (g < G && ii < w) ? min(L - 1, L - w + ii) : -1;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kk = tile_key0 + 8 * (r >> 2) + 4 * hf + (r & 3);
+          if (kk > last) e[rt][r] = NEG_INF;
+        }
+      }
+      // both half-waves hold the same rows, other keys
+      float m = fmaxf(e[rt][0], e[rt][1]);
+#pragma unroll
+      for (int r = 2; r < 16; ++r) m = fmaxf(m, e[rt][r]);
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+      m = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+      mw[rt] = m == NEG_INF ? 0.f : m * sl2;
+      float z = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        e[rt][r] = __builtin_amdgcn_exp2f(fmaf(e[rt][r], sl2, -mw[rt]));
+        z += e[rt][r];
+      }
+      const auto sz = __builtin_amdgcn_permlane32_swap(__float_as_uint(z), __float_as_uint(z), false, false);
+      z = __uint_as_float(sz[0]) + __uint_as_float(sz[1]);
+      if (hf == 0) sStat[wv][rt * 32 + ln] = make_float2(mw[rt], z);
+    }
+    __syncthreads();
+
+    // ---- publish the slice's statistics and count it in (the stores retire first)
+    if (tid < R) {
+      float M = NEG_INF, Z = 0.f;
+#pragma unroll
+      for (int v = 0; v < kWaves; ++v) combine_ms(M, Z, sStat[v][tid].x, sStat[v][tid].y);
+      store_coherent2(P.stats + ((size_t)job * nsl + jc.slice) * R * 2 + 2 * tid, M, Z);
+    }
+    vmem_release();
+    __syncthreads();
+    if (tid == 0) sFlag = (int)__hip_atomic_fetch_add(&arrive[job], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (sFlag == nsl - 1) {
+      vmem_acquire();
+      fold_job_pairs<R>(P, job, sStat);
+    }
+
+    // ---- the next item's query block loads while this one waits and finishes
+    JobRef jn = jc;
+    advance(jn, dj, ds, nsl, B, Hkv);
+    if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQ, q_of(jn), G, w);
+
+    // ---- wait (bounded) for the job's normalisers
+    if (tid < R) {
+      float lam = load_coherent(P.lam + (size_t)job * R + tid);
+      uint32_t it = 0;
+      while (lam != lam) {
+        __builtin_amdgcn_s_sleep(2);
+        lam = load_coherent(P.lam + (size_t)job * R + tid);
+        if (++it > kSpinLimit) {
+          atomicOr(status, 1u);
+          lam = __builtin_inff();
+        }
+      }
+      sLam[tid] = lam;
+    }
+    __syncthreads();
+
+    // ---- probabilities and their sums over the window rows (across lanes)
+    float alpha[NRT];
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt) alpha[rt] = __builtin_amdgcn_exp2f(mw[rt] - sLam[rt * 32 + ln]);   // +inf -> 0
+    const int sel = rs_sel(lane);
+    if (snap && NG > 1) {
+      // per query head: fold the head's row tiles into e[g] (in place; head g's sources come
+      // after index g, so nothing is overwritten before it is read)
+#pragma unroll
+      for (int g = 0; g < NG; ++g)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float x = alpha[g * NTH] * e[g * NTH][r];
+#pragma unroll
+          for (int u = 1; u < NTH; ++u) x = fmaf(alpha[g * NTH + u], e[g * NTH + u][r], x);
+          e[g][r] = x;
+        }
+      f32x16 (&ev)[NG] = *reinterpret_cast<f32x16(*)[NG]>(&e[0]);
+      reduce_scatter32_v<NG>(ev, lane);
+#pragma unroll
+      for (int i = 0; i < NG / 2; ++i) {
+        const int vi = 32 * i + sel, g = vi >> 4, r = vi & 15;
+        sCol[g][wv * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)] = ev[i >> 4][i & 15];
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float x = alpha[0] * e[0][r];
+#pragma unroll
+        for (int rt = 1; rt < NRT; ++rt) x = fmaf(alpha[rt], e[rt][r], x);
+        e[0][r] = x;
+      }
+      f32x16 (&ev)[1] = *reinterpret_cast<f32x16(*)[1]>(&e[0]);
+      reduce_scatter32_v<1>(ev, lane);
+      if ((lane & 1) == 0) {
+        const int r = sel & 15;
+        sCol[0][wv * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)] = ev[0][0];
+      }
+    }
+    if (t + 1 < T) k_tile(kf, jn);   // the next item's K tile (the other workgroups of the CU cover its latency)
+    __syncthreads();
+    store_scores<NG>(P, snap, job, jc.slice, cbase, sCol, inv_g);
+    jc = jn;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Scoring.  NRT = row tiles (query heads x row tiles per head, padded), NTH = row tiles per head.
+// Workgroup w owns items first = w, w + n_wg, ...; iteration t runs pass A of its item t and
+// pass B of its item t - lag:
+//   A: logits with keys as the MFMA A operand (lane = window row, registers = 16 keys), the
+//      tile row max and sum of exp2 inside the lane, folded over the four waves and published
+//      per slice; the slice counts itself in at the start of the next iteration (after its
+//      stores have completed), and the job's last slice folds the normalisers;
+//   B: the same logits with the queries as the A operand (lane = key, registers = 16 rows),
+//      accumulator started at -normaliser, so exp2 gives probabilities; the column sums over
+//      the window rows stay inside the lane.
+// Pass B re-reads a K tile this workgroup streamed `lag` iterations earlier (L2 / MALL hits);
+// `lag` covers the iterations a job spans, so a workgroup never waits on its own later work.
+// ---------------------------------------------------------------------------------------------
+template <int NRT, int NTH>
+__global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const PrefillLaunch P, int n_wg, int lag) {
+  constexpr int R = NRT * 32;
+  constexpr int NG = NRT / NTH;
+  __shared__ __attribute__((aligned(16))) uint16_t sQA[R * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t sQB[R * kHeadDim];
+  __shared__ float2 sStat[kWaves][R];
+  __shared__ __attribute__((aligned(16))) float sLam[R];   // -normaliser in logit units, pass B item
+  __shared__ float sCol[NG][kSlice];
+  __shared__ int sFold;
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hf = lane >> 5, ln = lane & 31;
+  const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
+  const int nsl = P.n_slices;
+  const int n_jobs = B * P.n_scored * Hkv;
+  const int64_t n_items = (int64_t)n_jobs * nsl;
+  const float sl2 = P.scale_log2;
+  const float inv_g = 1.f / (float)G;
+  const float NEG_INF = -__builtin_inff();
+  uint32_t* status = P.counters;
+  uint32_t* arrive = P.counters + 2;
+  const bool padded_rows = (G * NTH < NRT) || (w != NTH * 32);
+
+  const int64_t first = blockIdx.x;
+  if (first >= n_items) return;
+  const int T = (int)((n_items - 1 - first) / n_wg + 1);
+  const int dj = n_wg / nsl, ds = n_wg - dj * nsl;   // item stride n_wg in (jobs, slices)
+  auto step = [&](JobRef r) {
+    advance(r, dj, ds, nsl, B, Hkv);
+    return r;
+  };
+  auto q_of = [&](const JobRef& j) -> const uint16_t* {
+    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
+    return ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim;
+  };
+  auto k_tile = [&](u32x4 (&dst)[8], const JobRef& j) {
+    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
+    load_k_tile(dst, ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim, j.slice * kSlice + wv * 32 + ln, L, hf);
+  };
+
+  u32x4 kA[8], kB[8];   // each reloaded as soon as its MFMAs have consumed it
+  const JobRef j0 = decode_item(first, nsl, B, Hkv);
+  issue_q_to_lds<NRT, NTH>(sQA, q_of(j0), G, w);
+  k_tile(kA, j0);
+  uint32_t arrived = 0;   // thread 0: arrival count returned for the previous pass A item
+  JobRef ja = j0, jb = j0, jp = j0;   // pass A item t, pass B item t - lag, pass A item t - 1
+
+#pragma unroll 1
+  for (int t = 0; t < T + lag; ++t) {
+    const bool doA = t < T, doB = t >= lag;
+    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // operands of this iteration, stats stores of t-1
+    __syncthreads();
+    const bool had_prev = t >= 1 && t - 1 < T;
+    if (had_prev && tid == 0)
+      arrived = __hip_atomic_fetch_add(&arrive[jp.job], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+    // ============================================================ pass B: window column sums
+    const JobRef jbn = step(jb), jan = step(ja);   // the items after this iteration's
+    if (doB) {
+      const PrefillLayer& ly = P.layer[P.slot_layer[jb.slot]];
+      const bool snap = ly.rule == RKV_SNAPKV;
+      const int cbase = jb.slice * kSlice, key = cbase + wv * 32 + ln;
+      if (tid < R) {
+        float lam = load_coherent(P.lam + (size_t)jb.job * R + tid);
+        uint32_t it = 0;
+        while (lam != lam) {   // not folded yet (bounded wait)
+          __builtin_amdgcn_s_sleep(2);
+          lam = load_coherent(P.lam + (size_t)jb.job * R + tid);
+          if (++it > kSpinLimit) {
+            atomicOr(status, 1u);
+            lam = __builtin_inff();
+          }
+        }
+        sLam[tid] = -lam / sl2;
+      }
+      __syncthreads();
+      // lane = key, registers = rows rt*32 + 8(r/4) + 4hf + r%4; accumulators start at -normaliser
+      const bool edge_tile = cbase + wv * 32 + 32 > L - w;
+      float col[NG];
+#pragma unroll
+      for (int g = 0; g < NG; ++g) col[g] = 0.f;
+#pragma unroll
+      for (int rt = 0; rt < NRT; ++rt) {
+        f32x16 acc;
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float4 lv = *reinterpret_cast<const float4*>(sLam + rt * 32 + 8 * q4 + 4 * hf);
+          acc[4 * q4] = lv.x;
+          acc[4 * q4 + 1] = lv.y;
+          acc[4 * q4 + 2] = lv.z;
+          acc[4 * q4 + 3] = lv.w;
+        }
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q_frag(sQB, rt * 32 + ln, 8 * hf + st), as_bf16x8(kB[st]), acc,
+                                                        0, 0, 0);
+        if (rt == NRT - 1 && t + 1 - lag < T) k_tile(kB, jbn);   // next pass B tile (L2 / MALL)
+        float sum = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float pr = __builtin_amdgcn_exp2f(acc[r] * sl2);
+          if (edge_tile) {
+            const int ii = (rt % NTH) * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
+            if (key >= L || key > L - w + ii) pr = 0.f;
+          }
+          sum += pr;
+        }
+        col[rt / NTH] += sum;
+      }
+      // both half-waves hold the same key, other rows
+      if (snap && NG > 1) {
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(col[g]), __float_as_uint(col[g]), false, false);
+          if (hf == 0) sCol[g][wv * 32 + ln] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+        }
+      } else {
+        float c = col[0];
+#pragma unroll
+        for (int g = 1; g < NG; ++g) c += col[g];
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(c), __float_as_uint(c), false, false);
+        if (hf == 0) sCol[0][wv * 32 + ln] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+      }
+      __syncthreads();
+      if (t + 1 - lag < T) issue_q_to_lds<NRT, NTH>(sQB, q_of(jbn), G, w);   // sQB no longer read
+
+      store_scores<NG>(P, snap, jb.job, jb.slice, cbase, sCol, inv_g);
+    } else if (t + 1 - lag == 0) {
+      issue_q_to_lds<NRT, NTH>(sQB, q_of(j0), G, w);
+      k_tile(kB, j0);
+    }
+
+    // ============================================================ pass A: row statistics
+    if (doA) {
+      const int tile_key0 = ja.slice * kSlice + wv * 32;
+      const bool mask_a = padded_rows || tile_key0 + 32 > L - w;
+#pragma unroll
+      for (int rt = 0; rt < NRT; ++rt) {
+        f32x16 acc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+        for (int st = 0; st < 8; ++st)
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kA[st]), q_frag(sQA, rt * 32 + ln, 8 * hf + st), acc,
+                                                        0, 0, 0);
+        if (rt == NRT - 1 && t + 1 < T) k_tile(kA, jan);   // next pass A tile from HBM
+        // lane = window row ln of row tile rt, registers = keys tile_key0 + 8(r/4) + 4hf + r%4
+        if (mask_a) {
+          const int g = rt / NTH, ii = (rt - g * NTH) * 32 + ln;
+          const int last = (g < G && ii < w) ? min(L - 1, L - w + ii) : -1;
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int kk = tile_key0 + 8 * (r >> 2) + 4 * hf + (r & 3);
+            if (kk > last) acc[r] = NEG_INF;
+          }
+        }
+        // both half-waves hold the same rows, other keys
+        float m = fmaxf(acc[0], acc[1]);
+#pragma unroll
+        for (int r = 2; r < 16; ++r) m = fmaxf(m, acc[r]);
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+        m = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+        const float mw = m == NEG_INF ? 0.f : m * sl2;
+        float z = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z += __builtin_amdgcn_exp2f(fmaf(acc[r], sl2, -mw));
+        const auto sz = __builtin_amdgcn_permlane32_swap(__float_as_uint(z), __float_as_uint(z), false, false);
+        z = __uint_as_float(sz[0]) + __uint_as_float(sz[1]);
+        if (hf == 0) sStat[wv][rt * 32 + ln] = make_float2(mw, z);
+      }
+      __syncthreads();
+      if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQA, q_of(jan), G, w);   // sQA no longer read
+      if (tid < R) {
+        float M = NEG_INF, Z = 0.f;
+#pragma unroll
+        for (int v = 0; v < kWaves; ++v) combine_ms(M, Z, sStat[v][tid].x, sStat[v][tid].y);
+        store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R * 2 + 2 * tid, M, Z);
+      }
+    }
+
+    // ============================================================ the previous item's arrival
+    if (had_prev) {
+      __syncthreads();   // sStat is read above
+      if (tid == 0) sFold = (arrived == (uint32_t)(nsl - 1)) ? jp.job : -1;
+      __syncthreads();
+      if (sFold >= 0) fold_job<R>(P, sFold, sStat);
+    }
+    if (doA) {
+      jp = ja;
+      ja = jan;
+    }
+    if (doB) jb = jbn;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Selection: one workgroup per job.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_slices;
+  const int job = blockIdx.x;
+  const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
+  const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
+  const int bh = s * Hkv + h;
+  const bool snap = ly.rule == RKV_SNAPKV;
   const float NEG_INF = -__builtin_inff();
 
-  // ============================================================== gather / copy items
-  if (type == kItemGather || type == kItemCopy) {
-    const int h = head % Hkv, s = (head / Hkv) % B, li = head / (Hkv * B);
-    const PrefillLayer& ly = P.layer[type == kItemGather ? P.slot_layer[li] : P.unscored_layer[li]];
+  constexpr int kSelFixed = kHistBins * 4 + 64;
+  int* sHist = reinterpret_cast<int*>(smem);
+  int* sScan = sHist + kHistBins;          // 2 * kWaves ints
+  int* sSel = sScan + 8;                   // 2 ints
+  float* sCache = reinterpret_cast<float*>(smem + kSelFixed);
+  const int cache_cap = (kSelectLds - kSelFixed) / 4;
+  float* Srow = P.S + (size_t)job * L;
+  const int n_score = ly.all ? (snap ? L - w : L) : ly.cand_end;
+  const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
+  const bool fix = snap && ph > 0 && n_score > 0 && NC > 1;
+  const int n_edge = fix ? NC * G * E : 0;
+  const bool cached = n_score + n_edge <= cache_cap;
+  float* sEdge = sCache + n_score;
+  const float* Erow = P.edge + (size_t)job * NC * G * E;
+  if (cached) {   // eight loads in flight per thread
+    for (int j0 = tid; j0 < n_score + n_edge; j0 += kThreads * 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kThreads;
+        v[u] = j < n_score ? Srow[j] : (j < n_score + n_edge ? Erow[j - n_score] : 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + u * kThreads;
+        if (j < n_score + n_edge) sCache[j] = v[u];   // sEdge == sCache + n_score
+      }
+    }
+  }
+  __syncthreads();
+  // SnapKV: redo the pooled score of positions within pool_half of an interior slice border
+  if (fix) {
+    const int npre = L - w;
+    for (int e = tid; e < (NC - 1) * twoP; e += kThreads) {
+      const int cb = 1 + e / twoP, o = e - (e / twoP) * twoP;
+      const int bnd = cb * kSlice;
+      const int j = bnd - ph + o;
+      if (j < 0 || j >= npre || j >= n_score) continue;
+      // slice cb-1 holds keys [bnd-2P, bnd) at offsets [2P, 4P); slice cb keys [bnd, bnd+2P) at [0, 2P)
+      const int left = (cb - 1) * G * E, right = cb * G * E;
+      const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
+      float sc = 0.f;
+      for (int g = 0; g < G; ++g) {
+        float m = NEG_INF;
+        for (int t = lo; t <= hi; ++t) {
+          const int ei = (t < bnd) ? left + g * E + twoP + (t - (bnd - twoP)) : right + g * E + (t - bnd);
+          m = fmaxf(m, cached ? sEdge[ei] : Erow[ei]);
+        }
+        sc += m;
+      }
+      if (cached) sCache[j] = sc / (float)G;
+      else Srow[j] = sc / (float)G;
+    }
+  }
+  __syncthreads();
+  auto get = [&](int j) -> float { return cached ? sCache[j] : Srow[j]; };
+  if (ly.score) {
+    float* so = ly.score + (size_t)bh * L;
+    for (int j = tid; j < n_score; j += kThreads) so[j] = get(j);
+  }
+  int32_t* idx = ly.idx + (size_t)bh * ly.n_keep;
+  if (ly.all) {
+    for (int m = tid; m < ly.n_keep; m += kThreads) idx[m] = m;
+  } else {
+    const int n = ly.cand_end, k = ly.k_sel;
+    if (k > 0) {
+      // k-th largest candidate score: three radix passes over the 31 value bits (scores are
+      // >= 0, so the unsigned order of their bit patterns is the numeric order)
+      uint32_t prefix = 0u, pmask = 0u;
+      int kk = k;
+#pragma unroll 1
+      for (int pass = 0; pass < 3; ++pass) {
+        const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+        const int nb = pass == 0 ? 2048 : 1024;
+        for (int b = tid; b < nb; b += kThreads) sHist[b] = 0;
+        __syncthreads();
+        for (int j = tid; j < n; j += kThreads) {
+          const uint32_t x = __float_as_uint(get(j));
+          if ((x & pmask) == prefix) atomicAdd(&sHist[(x >> shift) & (nb - 1)], 1);
+        }
+        __syncthreads();
+        const int per = nb / kThreads;
+        int cnt = 0;
+        for (int i = 0; i < per; ++i) cnt += sHist[nb - 1 - (tid * per + i)];
+        int inc = cnt;  // inclusive scan of cnt over the workgroup
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(inc, o);
+          if (lane >= o) inc += y;
+        }
+        if (lane == 63) sScan[wv] = inc;
+        __syncthreads();
+        int above = inc - cnt;
+        for (int i = 0; i < wv; ++i) above += sScan[i];
+        if (kk > above && kk <= above + cnt) {
+          for (int i = 0; i < per; ++i) {
+            const int b = nb - 1 - (tid * per + i);
+            const int hb = sHist[b];
+            if (kk <= above + hb) {
+              sSel[0] = b;
+              sSel[1] = kk - above;
+              break;
+            }
+            above += hb;
+          }
+        }
+        __syncthreads();
+        prefix |= (uint32_t)sSel[0] << shift;
+        pmask |= (uint32_t)(nb - 1) << shift;
+        kk = sSel[1];
+        __syncthreads();
+      }
+      const uint32_t tau = prefix;
+      const int need = kk;  // ties at tau taken in position order
+      // ordered compaction: wave wv owns a contiguous key range; within it, 64 keys at a time,
+      // ballots give each taken key its rank among the greater / equal keys before it
+      const int per_w = ((n + kWaves - 1) / kWaves + 63) & ~63;
+      const int w0 = min(n, wv * per_w), w1 = min(n, w0 + per_w);
+      const uint64_t lt = (1ull << lane) - 1ull;
+      int cg = 0, ce = 0;
+      for (int j0 = w0; j0 < w1; j0 += 64) {
+        const int j = j0 + lane;
+        const uint32_t x = j < w1 ? __float_as_uint(get(j)) : 0u;
+        cg += __popcll(__ballot(j < w1 && x > tau));
+        ce += __popcll(__ballot(j < w1 && x == tau));
+      }
+      if (lane == 0) {
+        sScan[2 * wv] = cg;
+        sScan[2 * wv + 1] = ce;
+      }
+      __syncthreads();
+      int bg = 0, be = 0;   // greater / equal keys before this wave's range
+      for (int i = 0; i < wv; ++i) {
+        bg += sScan[2 * i];
+        be += sScan[2 * i + 1];
+      }
+      for (int j0 = w0; j0 < w1; j0 += 64) {
+        const int j = j0 + lane;
+        const uint32_t x = j < w1 ? __float_as_uint(get(j)) : 0u;
+        const bool gt = j < w1 && x > tau, eq = j < w1 && x == tau;
+        const uint64_t mg = __ballot(gt), me = __ballot(eq);
+        const int rg = bg + __popcll(mg & lt), re = be + __popcll(me & lt);
+        if (gt) idx[rg + min(re, need)] = j;
+        else if (eq && re < need) idx[rg + re] = j;
+        bg += __popcll(mg);
+        be += __popcll(me);
+      }
+    }
+    const int nf = ly.forced_hi - ly.forced_lo;
+    for (int t = tid; t < nf; t += kThreads) idx[k + t] = ly.forced_lo + t;
+  }
+  if (ly.acc) {
+    // scores of the retained positions (they seed decode-phase accumulation)
+    __syncthreads();
+    const float* accsrc = snap ? P.Su + (size_t)job * L : Srow;
+    float* acc = ly.acc + (size_t)bh * ly.n_keep;
+    for (int m = tid; m < ly.n_keep; m += kThreads) acc[m] = accsrc[idx[m]];
+  }
+}
+
+// Selection with every candidate score held in registers (kSelRegs per thread, 1024 threads):
+// wave wv owns the contiguous key range [w0, w1); its lane l holds keys w0 + 64 i + l.  Dynamic
+// LDS holds the job's slice-edge column sums and the repaired scores next to slice borders.
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+constexpr int kSelRegs = 16;
+constexpr int kSelRegsMaxKeys = kSelRegs * kSelThreads;
+
+__global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillLaunch P) {
+  extern __shared__ __attribute__((aligned(16))) float sDyn[];   // [n_edge] edges, then [n_fix] repaired scores
+  __shared__ int sHist[kHistBins];
+  __shared__ int sScan[2 * kSelWaves];
+  __shared__ int sSel[2];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_slices;
+  const int job = blockIdx.x;
+  const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
+  const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
+  const int bh = s * Hkv + h;
+  const bool snap = ly.rule == RKV_SNAPKV;
+  const float NEG_INF = -__builtin_inff();
+  const float inv_g = 1.f / (float)G;
+  const float* Srow = P.S + (size_t)job * L;
+  const int n = ly.all ? (snap ? L - w : L) : ly.cand_end;   // candidate (and reported) positions
+  const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
+  const bool fix = snap && ph > 0 && n > 0 && NC > 1;
+  const int n_edge = fix ? NC * G * E : 0, n_fix = fix ? (NC - 1) * twoP : 0;
+  float* sEdge = sDyn;
+  float* sFix = sDyn + n_edge;
+
+  // ---- candidate scores into registers, slice-edge sums into LDS
+  const int per_w = ((n + kSelWaves - 1) / kSelWaves + 63) & ~63;
+  const int w0 = min(n, wv * per_w), w1 = min(n, w0 + per_w);
+  float x[kSelRegs];
+#pragma unroll
+  for (int i = 0; i < kSelRegs; ++i) {
+    const int j = w0 + 64 * i + lane;
+    x[i] = j < w1 ? Srow[j] : 0.f;
+  }
+  if (fix) {
+    const float* Erow = P.edge + (size_t)job * NC * G * E;
+    for (int e0 = tid; e0 < n_edge; e0 += kSelThreads * 4) {
+      float v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = e0 + u * kSelThreads < n_edge ? Erow[e0 + u * kSelThreads] : 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (e0 + u * kSelThreads < n_edge) sEdge[e0 + u * kSelThreads] = v[u];
+    }
+  }
+  loads_done();
+  if (fix) {
+    __syncthreads();
+    // SnapKV: redo the pooled score of positions within pool_half of an interior slice border;
+    // slice cb-1 holds keys [bnd-2P, bnd) at edge offsets [2P, 4P), slice cb keys [bnd, bnd+2P) at [0, 2P)
+    const int npre = L - w;
+    for (int e = tid; e < n_fix; e += kSelThreads) {
+      const int cb = 1 + e / twoP, o = e - (cb - 1) * twoP;
+      const int bnd = cb * kSlice, j = bnd - ph + o;
+      float sc = 0.f;
+      if (j >= 0 && j < npre && j < n) {
+        const int left = (cb - 1) * G * E, right = cb * G * E;
+        const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
+        for (int g = 0; g < G; ++g) {
+          float m = NEG_INF;
+          for (int t = lo; t <= hi; ++t) {
+            const int ei = (t < bnd) ? left + g * E + twoP + (t - (bnd - twoP)) : right + g * E + (t - bnd);
+            m = fmaxf(m, sEdge[ei]);
+          }
+          sc += m;
+        }
+      }
+      sFix[e] = sc * inv_g;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSelRegs; ++i) {
+      const int j = w0 + 64 * i + lane;
+      const int cb = (j + ph) / kSlice, o = j + ph - cb * kSlice;
+      if (j < w1 && j < npre && cb >= 1 && cb < NC && o < twoP) x[i] = sFix[(cb - 1) * twoP + o];
+    }
+  }
+  if (ly.score) {
+    float* so = ly.score + (size_t)bh * L;
+#pragma unroll
+    for (int i = 0; i < kSelRegs; ++i) {
+      const int j = w0 + 64 * i + lane;
+      if (j < w1) so[j] = x[i];
+    }
+  }
+  int32_t* idx = ly.idx + (size_t)bh * ly.n_keep;
+  if (ly.all) {
+    for (int m = tid; m < ly.n_keep; m += kSelThreads) idx[m] = m;
+  } else {
+    const int k = ly.k_sel;
+    if (k > 0) {
+      // k-th largest candidate score: three radix passes over the 31 value bits (scores are
+      // >= 0, so the unsigned order of their bit patterns is the numeric order)
+      uint32_t prefix = 0u, pmask = 0u;
+      int kk = k;
+#pragma unroll 1
+      for (int pass = 0; pass < 3; ++pass) {
+        const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+        const int nb = pass == 0 ? 2048 : 1024;
+        for (int b = tid; b < nb; b += kSelThreads) sHist[b] = 0;
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kSelRegs; ++i) {
+          const int j = w0 + 64 * i + lane;
+          const uint32_t u = __float_as_uint(x[i]);
+          if (j < w1 && (u & pmask) == prefix) atomicAdd(&sHist[(u >> shift) & (nb - 1)], 1);
+        }
+        __syncthreads();
+        // bins in descending order: thread tid owns bins nb-1-tid*per .. (per = 2 or 1)
+        const int per = nb / kSelThreads;
+        int cnt = 0;
+        for (int q = 0; q < per; ++q) cnt += sHist[nb - 1 - (tid * per + q)];
+        int inc = cnt;  // inclusive scan of cnt over the workgroup
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const int y = __shfl_up(inc, o);
+          if (lane >= o) inc += y;
+        }
+        if (lane == 63) sScan[wv] = inc;
+        __syncthreads();
+        int above = inc - cnt;
+        for (int q = 0; q < wv; ++q) above += sScan[q];
+        if (kk > above && kk <= above + cnt) {
+          for (int q = 0; q < per; ++q) {
+            const int b = nb - 1 - (tid * per + q);
+            const int hb = sHist[b];
+            if (kk <= above + hb) {
+              sSel[0] = b;
+              sSel[1] = kk - above;
+              break;
+            }
+            above += hb;
+          }
+        }
+        __syncthreads();
+        prefix |= (uint32_t)sSel[0] << shift;
+        pmask |= (uint32_t)(nb - 1) << shift;
+        kk = sSel[1];
+        __syncthreads();
+      }
+      const uint32_t tau = prefix;
+      const int need = kk;  // ties at tau taken in position order
+      // ordered compaction over the waves' contiguous ranges: ballots rank each taken key
+      // among the greater / equal keys before it
+      const uint64_t lt = (1ull << lane) - 1ull;
+      int cg = 0, ce = 0;
+#pragma unroll
+      for (int i = 0; i < kSelRegs; ++i) {
+        const int j = w0 + 64 * i + lane;
+        const uint32_t u = __float_as_uint(x[i]);
+        cg += __popcll(__ballot(j < w1 && u > tau));
+        ce += __popcll(__ballot(j < w1 && u == tau));
+      }
+      if (lane == 0) {
+        sScan[2 * wv] = cg;
+        sScan[2 * wv + 1] = ce;
+      }
+      __syncthreads();
+      int bg = 0, be = 0;
+      for (int q = 0; q < wv; ++q) {
+        bg += sScan[2 * q];
+        be += sScan[2 * q + 1];
+      }
+#pragma unroll
+      for (int i = 0; i < kSelRegs; ++i) {
+        const int j = w0 + 64 * i + lane;
+        const uint32_t u = __float_as_uint(x[i]);
+        const bool gt = j < w1 && u > tau, eq = j < w1 && u == tau;
+        const uint64_t mg = __ballot(gt), me = __ballot(eq);
+        const int rg = bg + __popcll(mg & lt), re = be + __popcll(me & lt);
+        if (gt) idx[rg + min(re, need)] = j;
+        else if (eq && re < need) idx[rg + re] = j;
+        bg += __popcll(mg);
+        be += __popcll(me);
+      }
+    }
+    const int nf = ly.forced_hi - ly.forced_lo;
+    for (int t = tid; t < nf; t += kSelThreads) idx[k + t] = ly.forced_lo + t;
+  }
+  if (ly.acc) {
+    // scores of the retained positions (they seed decode-phase accumulation)
+    __syncthreads();
+    const float* accsrc = snap ? P.Su + (size_t)job * L : Srow;
+    float* acc = ly.acc + (size_t)bh * ly.n_keep;
+    for (int m = tid; m < ly.n_keep; m += kSelThreads) acc[m] = accsrc[idx[m]];
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Gather: copy the retained K / V rows, 16 lanes x 16 B per row, 8 rows in flight per lane group.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void gather_kernel(const PrefillLaunch P, int n_parts, int64_t n_items) {
+  const int tid = threadIdx.x;
+  const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len;
+  const int piece = tid & 15, rsub = tid >> 4;
+  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int part = (int)(item % n_parts);
+    const int64_t gj = item / n_parts;
+    const int h = (int)(gj % Hkv), s = (int)((gj / Hkv) % B), li = (int)(gj / ((int64_t)Hkv * B));
+    const PrefillLayer& ly = P.layer[P.gather_layer[li]];
     const int bh = s * Hkv + h;
     const int n_keep = ly.n_keep;
-    const int r0 = (int)((int64_t)part * n_keep / kGatherParts), r1 = (int)((int64_t)(part + 1) * n_keep / kGatherParts);
-    if (r1 <= r0) return;
-    if (type == kItemGather) {
-      if (tid == 0) wait_at_least(&selDone[head], 1u, status);
-      __syncthreads();
-    }
+    const int r0 = part * kGatherRows, r1 = min(n_keep, r0 + kGatherRows);
+    if (r1 <= r0) continue;
+    const bool scored = ly.slot >= 0;
     int32_t* idx = ly.idx + (size_t)bh * n_keep;
     const size_t hbase = (size_t)bh * L;
-    const int piece = tid & 15, rsub = tid >> 4;
-    constexpr int kRowsPerPass = (kThreads / 16) * 8;   // 16 row groups x 8 rows in flight
-    for (int m0 = r0; m0 < r1; m0 += kRowsPerPass) {
+    for (int m0 = r0; m0 < r1; m0 += 16 * 8) {
       int pos[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int m = m0 + rsub + 16 * u;
         pos[u] = -1;
         if (m < r1) {
-          if (type == kItemGather) pos[u] = load_coherent(idx + m);
+          if (scored) pos[u] = idx[m];
           else pos[u] = ly.all ? m : (m < ly.cand_end ? m : ly.forced_lo + (m - ly.cand_end));
         }
       }
+      loads_done();
       u32x4 kv[8], vv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -342,6 +1185,7 @@ __global__ __launch_bounds__(kThreads, 2) void evict_kernel(const PrefillLaunch 
           vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.v + src));
         }
       }
+      loads_done();
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int m = m0 + rsub + 16 * u;
@@ -349,487 +1193,53 @@ __global__ __launch_bounds__(kThreads, 2) void evict_kernel(const PrefillLaunch 
           const size_t dst = ((size_t)bh * n_keep + m) * kHeadDim + piece * 8;
           __builtin_nontemporal_store(kv[u], reinterpret_cast<u32x4*>(ly.k_out + dst));
           __builtin_nontemporal_store(vv[u], reinterpret_cast<u32x4*>(ly.v_out + dst));
-          if (type == kItemCopy && piece == 0) {
+          if (!scored && piece == 0) {
             idx[m] = pos[u];
             if (ly.acc) ly.acc[(size_t)bh * n_keep + m] = 0.f;
           }
         }
       }
     }
-    return;
-  }
-
-  const int h = head % Hkv, s = (head / Hkv) % B, slot = head / (Hkv * B);
-  const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
-  const int bh = s * Hkv + h;
-  const bool snap = ly.rule == RKV_SNAPKV;
-
-  // ============================================================== select item
-  if (type == kItemSelect) {
-    int* sHist = reinterpret_cast<int*>(smem);
-    int* sScan = sHist + kHistBins;          // kWaves ints
-    int* sSel = sScan + 8;                   // 2 ints
-    float* sCache = reinterpret_cast<float*>(smem + kSelFixed);
-    const int cache_cap = (kLdsBytes - kSelFixed) / 4;
-    float* Srow = P.S + (size_t)head * L;
-    const int n_score = ly.all ? (snap ? L - w : L) : ly.cand_end;
-    const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
-    const bool fix = snap && ph > 0 && n_score > 0 && NC > 1;
-    const int n_edge = fix ? NC * G * E : 0;
-    const bool cached = n_score + n_edge <= cache_cap;
-    float* sEdge = sCache + n_score;          // chunk-edge column sums (cached path)
-    const float* Erow = P.edge + (size_t)head * NC * G * E;
-    // wait (bounded) until every score of the head is written (and the unpooled scores when they
-    // seed acc_out); keep the candidate scores and the chunk-edge values in LDS when they fit
-    const float* Surow = P.Su + (size_t)head * L;
-    const bool need_su = snap && ly.acc != nullptr;
-    for (int j0 = tid; j0 < L; j0 += kThreads * 8) {
-      float x[8], y[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = j0 + u * kThreads;
-        x[u] = j < L ? load_coherent(Srow + j) : 0.f;
-        y[u] = (need_su && j < L) ? load_coherent(Surow + j) : 0.f;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = j0 + u * kThreads;
-        uint32_t it = 0;
-        while (unwritten(x[u]) || unwritten(y[u])) {
-          __builtin_amdgcn_s_sleep(2);
-          x[u] = load_coherent(Srow + j);
-          if (need_su) y[u] = load_coherent(Surow + j);
-          if (++it > kSpinLimit) {
-            atomicOr(status, 1u);
-            x[u] = 0.f;
-            y[u] = 0.f;
-          }
-        }
-        if (cached && j < n_score) sCache[j] = x[u];
-      }
-    }
-    auto edge_at = [&](int e) -> float {
-      float a = load_coherent(Erow + e);
-      uint32_t it = 0;
-      while (unwritten(a)) {
-        __builtin_amdgcn_s_sleep(2);
-        a = load_coherent(Erow + e);
-        if (++it > kSpinLimit) {
-          atomicOr(status, 1u);
-          a = 0.f;
-        }
-      }
-      return a;
-    };
-    if (fix && cached) {
-      for (int e0 = tid; e0 < n_edge; e0 += kThreads * 4) {
-        float a[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) a[u] = e0 + u * kThreads < n_edge ? load_coherent(Erow + e0 + u * kThreads) : 0.f;
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int e = e0 + u * kThreads;
-          if (e < n_edge) sEdge[e] = unwritten(a[u]) ? edge_at(e) : a[u];
-        }
-      }
-    }
-    __syncthreads();
-    // SnapKV: redo the pooled score of positions within pool_half of an interior chunk border
-    if (fix) {
-      const int npre = L - w;
-      for (int e = tid; e < (NC - 1) * twoP; e += kThreads) {
-        const int cb = 1 + e / twoP, o = e - (e / twoP) * twoP;
-        const int bnd = cb * kChunk;
-        const int j = bnd - ph + o;
-        if (j < 0 || j >= npre || j >= n_score) continue;
-        // chunk cb-1 holds keys [bnd-2P, bnd) at offsets [2P, 4P); chunk cb keys [bnd, bnd+2P) at [0, 2P)
-        const int left = (cb - 1) * G * E, right = cb * G * E;
-        const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
-        float sc = 0.f;
-        for (int g = 0; g < G; ++g) {
-          float m = NEG_INF;
-          for (int t = lo; t <= hi; ++t) {
-            const int ei = (t < bnd) ? left + g * E + twoP + (t - (bnd - twoP)) : right + g * E + (t - bnd);
-            m = fmaxf(m, cached ? sEdge[ei] : edge_at(ei));
-          }
-          sc += m;
-        }
-        if (cached) sCache[j] = sc / (float)G;
-        else store_coherent(Srow + j, sc / (float)G);
-      }
-      if (!cached) vmem_release();
-    }
-    __syncthreads();
-    auto get = [&](int j) -> float { return cached ? sCache[j] : load_coherent(Srow + j); };
-    if (ly.score) {
-      float* so = ly.score + (size_t)bh * L;
-      for (int j = tid; j < n_score; j += kThreads) so[j] = get(j);
-    }
-    int32_t* idx = ly.idx + (size_t)bh * ly.n_keep;
-    float* acc = ly.acc ? ly.acc + (size_t)bh * ly.n_keep : nullptr;
-    const float* accsrc = snap ? Surow : Srow;
-    if (ly.all) {
-      for (int m = tid; m < ly.n_keep; m += kThreads) store_coherent(idx + m, m);
-    } else {
-      const int n = ly.cand_end, k = ly.k_sel;
-      if (k > 0) {
-        // k-th largest candidate score: three radix passes over the 31 value bits (scores are
-        // >= 0, so the unsigned order of their bit patterns is the numeric order)
-        uint32_t prefix = 0u, pmask = 0u;
-        int kk = k;
-#pragma unroll 1
-        for (int pass = 0; pass < 3; ++pass) {
-          const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
-          const int nb = pass == 0 ? 2048 : 1024;
-          for (int b = tid; b < nb; b += kThreads) sHist[b] = 0;
-          __syncthreads();
-          for (int j = tid; j < n; j += kThreads) {
-            const uint32_t x = __float_as_uint(get(j));
-            if ((x & pmask) == prefix) atomicAdd(&sHist[(x >> shift) & (nb - 1)], 1);
-          }
-          __syncthreads();
-          const int per = nb / kThreads;
-          int cnt = 0;
-          for (int i = 0; i < per; ++i) cnt += sHist[nb - 1 - (tid * per + i)];
-          int inc = cnt;  // inclusive scan of cnt over the workgroup
-#pragma unroll
-          for (int o = 1; o < 64; o <<= 1) {
-            const int y = __shfl_up(inc, o);
-            if (lane >= o) inc += y;
-          }
-          if (lane == 63) sScan[wv] = inc;
-          __syncthreads();
-          int above = inc - cnt;
-          for (int i = 0; i < wv; ++i) above += sScan[i];
-          if (kk > above && kk <= above + cnt) {
-            for (int i = 0; i < per; ++i) {
-              const int b = nb - 1 - (tid * per + i);
-              const int hb = sHist[b];
-              if (kk <= above + hb) {
-                sSel[0] = b;
-                sSel[1] = kk - above;
-                break;
-              }
-              above += hb;
-            }
-          }
-          __syncthreads();
-          prefix |= (uint32_t)sSel[0] << shift;
-          pmask |= (uint32_t)(nb - 1) << shift;
-          kk = sSel[1];
-          __syncthreads();
-        }
-        const uint32_t tau = prefix;
-        const int need = kk;  // ties at tau taken in position order
-        const int seg = (n + kThreads - 1) / kThreads;
-        const int j0 = min(n, tid * seg), j1 = min(n, j0 + seg);
-        int gt = 0, eq = 0;
-        for (int j = j0; j < j1; ++j) {
-          const uint32_t x = __float_as_uint(get(j));
-          gt += x > tau;
-          eq += x == tau;
-        }
-        const int v = gt | (eq << 16);   // exclusive scan of the packed counts
-        int inc = v;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(inc, o);
-          if (lane >= o) inc += y;
-        }
-        if (lane == 63) sScan[wv] = inc;
-        __syncthreads();
-        int pre = inc - v;
-        for (int i = 0; i < wv; ++i) pre += sScan[i];
-        const int pre_gt = pre & 0xffff, pre_eq = pre >> 16;
-        int out = pre_gt + min(pre_eq, need);
-        int er = pre_eq;
-        for (int j = j0; j < j1; ++j) {
-          const uint32_t x = __float_as_uint(get(j));
-          bool take = x > tau;
-          if (x == tau) {
-            take = er < need;
-            ++er;
-          }
-          if (take) {
-            store_coherent(idx + out, j);
-            ++out;
-          }
-        }
-      }
-      const int nf = ly.forced_hi - ly.forced_lo;
-      for (int t = tid; t < nf; t += kThreads) store_coherent(idx + k + t, ly.forced_lo + t);
-    }
-    vmem_release();
-    __syncthreads();
-    if (tid == 0) __hip_atomic_store(&selDone[head], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (acc) {
-      // scores of the retained positions (they seed decode-phase accumulation)
-      for (int m0 = tid; m0 < ly.n_keep; m0 += kThreads * 8) {
-        int pos[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) pos[u] = m0 + u * kThreads < ly.n_keep ? load_coherent(idx + m0 + u * kThreads) : -1;
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          if (pos[u] >= 0) acc[m0 + u * kThreads] = load_coherent(accsrc + pos[u]);
-      }
-    }
-    return;
-  }
-
-  // ============================================================== stats and score items
-  uint16_t* sQ = reinterpret_cast<uint16_t*>(smem);
-  float* aux = reinterpret_cast<float*>(smem + kQBytes);
-  const int nt_used = G * NTG;
-  const int c = chunk;
-  const size_t head_base = (size_t)bh * L;
-  const uint16_t* khead = ly.k + head_base * kHeadDim;
-  const int wave_key0 = c * kChunk + wv * kKeysPerWave;
-  const bool padded_rows = (nt_used < NT) || (w != NTG * 32);
-
-  u32x4 kf[kKDepth][8];              // ring of key tiles: the current one and kKDepth-1 ahead
-#pragma unroll
-  for (int d = 0; d < kKDepth - 1; ++d) load_k_frag(kf[d], khead, wave_key0 + d * 32 + ln, L, hf);
-  load_q_to_lds<NT, NTG>(sQ, P, ly, s, h);
-  float* sMp = aux + NG * kChunk;     // score items: per-row log-normalisers
-  if (type == kItemScore) {
-    // fold every chunk's (max, sum) of this head into exp2 offsets M + log2(sum) per row,
-    // waiting (bounded) for chunks whose statistics are not written yet
-    constexpr int kGroups = kThreads / R > 0 ? kThreads / R : 1;
-    constexpr int kRowsPerPass = kThreads / kGroups;
-    float* sPart = sMp + R;           // [kGroups][R][2]
-    for (int r0 = 0; r0 < R; r0 += kRowsPerPass) {
-      const int r = r0 + tid % kRowsPerPass;
-      const int j = tid / kRowsPerPass;
-      float M = NEG_INF, Ls = 0.f;
-      const float* st0 = P.stats + (size_t)head * NC * R * 2 + 2 * r;
-      for (int c0 = j; c0 < NC; c0 += kGroups * 8) {
-        float2 v[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int cc = c0 + u * kGroups;
-          v[u] = cc < NC ? load_coherent2(st0 + (size_t)cc * R * 2) : make_float2(NEG_INF, 0.f);
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          uint32_t it = 0;
-          while (unwritten(v[u].x)) {
-            __builtin_amdgcn_s_sleep(2);
-            v[u] = load_coherent2(st0 + (size_t)(c0 + u * kGroups) * R * 2);
-            if (++it > kSpinLimit) {
-              atomicOr(status, 1u);
-              v[u] = make_float2(NEG_INF, 0.f);
-            }
-          }
-          combine_ms(M, Ls, v[u].x, v[u].y);
-        }
-      }
-      sPart[(j * R + r) * 2] = M;
-      sPart[(j * R + r) * 2 + 1] = Ls;
-    }
-    __syncthreads();
-    for (int r = tid; r < R; r += kThreads) {
-      float M = sPart[r * 2], Ls = sPart[r * 2 + 1];
-      for (int j = 1; j < kGroups; ++j) combine_ms(M, Ls, sPart[(j * R + r) * 2], sPart[(j * R + r) * 2 + 1]);
-      // probabilities are exp2(z - M - log2 L); rows without keys (padding) get +inf -> 0
-      sMp[r] = Ls > 0.f ? M + __log2f(Ls) : __builtin_inff();
-    }
-  }
-  __syncthreads();
-
-  if (type == kItemStats) {
-    float run_m[NT], run_l[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) { run_m[t] = NEG_INF; run_l[t] = 0.f; }
-    // one key tile: logits for half of the row tiles at a time, then the running row
-    // max / sum; lane = window row ln of tile t, registers = keys tile_key0 + 8(r/4) + 4hf + r%4
-    auto tile = [&](const u32x4 (&kft)[8], int tile_key0) {
-      const bool need_mask = padded_rows || (tile_key0 + 32 > L - w);
-#pragma unroll
-      for (int half = 0; half < NT / kRowTilesPerPass; ++half) {
-        constexpr int NH = kRowTilesPerPass;
-        f32x16 acc[NH];
-        mfma_tile<NH, false>(acc, kft, sQ, ln, hf, half * NH, nt_used);
-#pragma unroll
-        for (int i = 0; i < NH; ++i) {
-          const int t = half * NH + i;
-          if (t >= nt_used) continue;
-          if (need_mask) mask_rows_lane<NTG>(acc[i], t, ln, hf, tile_key0, G, w, L);
-          float tm = acc[i][0];
-#pragma unroll
-          for (int r = 1; r < 16; ++r) tm = fmaxf(tm, acc[i][r]);
-          if (tm == NEG_INF) continue;
-          const float nm = fmaxf(run_m[t], tm * sl2);
-          float sm = run_l[t] * __builtin_amdgcn_exp2f(run_m[t] - nm);
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sm += __builtin_amdgcn_exp2f(fmaf(acc[i][r], sl2, -nm));
-          run_m[t] = nm;
-          run_l[t] = sm;
-        }
-      }
-    };
-#pragma unroll 1
-    for (int base = 0; base < kTilesPerWave; base += kKDepth) {
-#pragma unroll
-      for (int i = 0; i < kKDepth; ++i) {
-        const int kt = base + i;
-        // keys kKDepth-1 tiles ahead load while this tile is multiplied and exponentiated
-        if (kt + kKDepth - 1 < kTilesPerWave)
-          load_k_frag(kf[(i + kKDepth - 1) % kKDepth], khead, wave_key0 + (kt + kKDepth - 1) * 32 + ln, L, hf);
-        if (wave_key0 + kt * 32 < L) tile(kf[i], wave_key0 + kt * 32);
-      }
-    }
-    // fold the two lanes that share a row, then the four waves
-    float* sRed = aux;  // [kWaves][R][2]
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const float m2 = __shfl_xor(run_m[t], 32), l2 = __shfl_xor(run_l[t], 32);
-      float M = run_m[t], Ls = run_l[t];
-      combine_ms(M, Ls, m2, l2);
-      if (hf == 0) {
-        sRed[(wv * R + t * 32 + ln) * 2] = M;
-        sRed[(wv * R + t * 32 + ln) * 2 + 1] = Ls;
-      }
-    }
-    __syncthreads();
-    float* stat = P.stats + ((size_t)head * NC + c) * R * 2;
-    for (int r = tid; r < R; r += kThreads) {
-      float M = NEG_INF, Ls = 0.f;
-#pragma unroll
-      for (int v = 0; v < kWaves; ++v) combine_ms(M, Ls, sRed[(v * R + r) * 2], sRed[(v * R + r) * 2 + 1]);
-      store_coherent2(stat + 2 * r, M, Ls);
-    }
-    return;
-  }
-
-  // ---------------------------------------------------------------- score item
-  float* sA = aux;  // [NG][kChunk] window column sums of this chunk per query head
-  // one key tile: probabilities for half of the row tiles at a time and their column sums per
-  // query head; lane = key tile_key0 + ln, registers = rows t*32 + 8(r/4) + 4hf + r%4
-  auto tile = [&](const u32x4 (&kft)[8], int tile_key0, int local0) {
-    const int key = tile_key0 + ln;
-    const bool need_mask = padded_rows || (tile_key0 + 32 > L - w);
-    float col[NG];
-#pragma unroll
-    for (int g = 0; g < NG; ++g) col[g] = 0.f;
-#pragma unroll
-    for (int half = 0; half < NT / kRowTilesPerPass; ++half) {
-      constexpr int NH = kRowTilesPerPass;
-      f32x16 acc[NH];
-      mfma_tile<NH, true>(acc, kft, sQ, ln, hf, half * NH, nt_used);
-#pragma unroll
-      for (int i = 0; i < NH; ++i) {
-        const int t = half * NH + i;
-        if (t >= nt_used) continue;
-        float mp[16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float4 v = *reinterpret_cast<const float4*>(sMp + t * 32 + 8 * q + 4 * hf);
-          mp[4 * q] = v.x; mp[4 * q + 1] = v.y; mp[4 * q + 2] = v.z; mp[4 * q + 3] = v.w;
-        }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][r] = __builtin_amdgcn_exp2f(fmaf(acc[i][r], sl2, -mp[r]));
-        if (need_mask) mask_rows_regs<NTG>(acc[i], t, hf, key, G, w, L);
-        float cs = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) cs += acc[i][r];
-        col[t / NTG] += cs;
-      }
-    }
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      const float v = col[g] + __shfl_xor(col[g], 32);
-      if (hf == 0 && g < G) sA[g * kChunk + local0 + ln] = v;
-    }
-  };
-#pragma unroll 1
-  for (int base = 0; base < kTilesPerWave; base += kKDepth) {
-#pragma unroll
-    for (int i = 0; i < kKDepth; ++i) {
-      const int kt = base + i;
-      if (kt + kKDepth - 1 < kTilesPerWave)
-        load_k_frag(kf[(i + kKDepth - 1) % kKDepth], khead, wave_key0 + (kt + kKDepth - 1) * 32 + ln, L, hf);
-      if (wave_key0 + kt * 32 < L) tile(kf[i], wave_key0 + kt * 32, wv * kKeysPerWave + kt * 32);
-    }
-  }
-  __syncthreads();
-
-  // group mean (unpooled), in-chunk max-pool (SnapKV), scores and chunk-edge values
-  const int cbase = c * kChunk;
-  float* Srow = P.S + (size_t)head * L;
-  for (int kl = tid; kl < kChunk; kl += kThreads) {
-    const int key = cbase + kl;
-    if (key >= L) break;
-    float su = 0.f;
-    for (int g = 0; g < G; ++g) su += sA[g * kChunk + kl];
-    su = su / (float)G;
-    if (snap) {
-      const int npre = L - w;
-      float sc = su;
-      if (key < npre) {
-        const int ph = P.pool_half;
-        const int lo = max(key - ph, cbase), hi = min(min(key + ph, cbase + kChunk - 1), npre - 1);
-        sc = 0.f;
-        for (int g = 0; g < G; ++g) {
-          float m = NEG_INF;
-          for (int t = lo; t <= hi; ++t) m = fmaxf(m, sA[g * kChunk + t - cbase]);
-          sc += m;
-        }
-        sc = sc / (float)G;
-      }
-      store_coherent(Srow + key, sc);
-      if (P.want_unpooled) store_coherent(P.Su + (size_t)head * L + key, su);
-    } else {
-      store_coherent(Srow + key, su);
-    }
-  }
-  if (snap && P.pool_half > 0) {
-    const int E = 4 * P.pool_half, twoP = 2 * P.pool_half;
-    float* ed = P.edge + ((size_t)head * NC + c) * G * E;
-    for (int e = tid; e < G * E; e += kThreads) {
-      const int g = e / E, o = e - g * E;
-      const int kl = o < twoP ? o : kChunk - twoP + (o - twoP);
-      store_coherent(ed + e, (cbase + kl < L) ? sA[g * kChunk + kl] : 0.f);
-    }
   }
 }
 
-template <int NT, int NTG>
-int resident_groups() {
+int device_cus() {
   static int cached = -1;
   if (cached < 0) {
-    int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, evict_kernel<NT, NTG>, kThreads, 0) != hipSuccess ||
-        per_cu < 1)
-      per_cu = 1;
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
       cus = 256;
-    cached = per_cu * cus;
+    cached = cus;
   }
   return cached;
 }
 
-template <int NT, int NTG>
-int launch_evict(PrefillLaunch P, hipStream_t st, void* stream) {
-  const int nH = P.batch * P.n_scored * P.n_kv_heads;
-  // Lags between a head's phases, in steps: about one resident round of workgroups between its
-  // stats and score items and between its score and select items (so those items rarely wait,
-  // and the score items still find the head's K in the on-die caches); the gather items only
-  // wait for the one select item.
-  const int per_step = 2 * P.n_chunks + 1 + kGatherParts;
-  const int round = (resident_groups<NT, NTG>() + per_step - 1) / per_step;
-  P.lag_score = round + 1;
-  P.lag_select = round + 1;
-  P.lag_gather = round / 3 + 1;
-  const int64_t scored = nH > 0 ? (int64_t)nH * (2 * P.n_chunks + 1 + kGatherParts) : 0;
-  const int64_t copies = (int64_t)P.n_unscored * P.batch * P.n_kv_heads * kGatherParts;
-  const int64_t total = scored + copies;
-  if (total <= 0) return 0;
-  if (total > 0x7fffffff) return (int)hipErrorInvalidValue;
-  P.n_tickets = (int)total;
+template <typename K>
+int resident_groups(K kernel) {
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess || per_cu < 1) per_cu = 1;
+  return per_cu * device_cus();
+}
+
+template <int NRT, int NTH>
+int launch_score(const PrefillLaunch& P, hipStream_t st, void* stream) {
+  const int64_t n_items = (int64_t)P.batch * P.n_scored * P.n_kv_heads * P.n_slices;
+  if (n_items <= 0) return 0;
+  static const int fused_wg = resident_groups(score_fused_kernel<NRT, NTH>);
+  static const int lagged_wg = resident_groups(score_kernel<NRT, NTH>);
   profile_mark(kStageScore, false, stream);
-  evict_kernel<NT, NTG><<<(unsigned)total, kThreads, 0, st>>>(P);
+  if (P.n_slices <= fused_wg / 2 && !P.force_two_pass) {
+    // every workgroup is resident and a job's slices are all in flight while they wait
+    const int n_wg = (int)std::min<int64_t>(n_items, fused_wg);
+    score_fused_kernel<NRT, NTH><<<n_wg, kThreads, 0, st>>>(P, n_wg);
+  } else {
+    const int n_wg = (int)std::min<int64_t>(n_items, lagged_wg);
+    // pass B trails pass A by `lag` items: at least the iterations one job spans inside a
+    // workgroup plus one for the fold, and enough to absorb the drift between workgroups
+    const int lag = std::max(P.score_lag, (P.n_slices + n_wg - 1) / n_wg + 2);
+    score_kernel<NRT, NTH><<<n_wg, kThreads, 0, st>>>(P, n_wg, lag);
+  }
   profile_mark(kStageScore, true, stream);
   return 0;
 }
@@ -838,26 +1248,55 @@ int launch_evict(PrefillLaunch P, hipStream_t st, void* stream) {
 
 int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int nH = P.batch * P.n_scored * P.n_kv_heads;
+  const int n_jobs = P.batch * P.n_scored * P.n_kv_heads;
   {
-    const int nc = 2 + nH;
-    const int64_t n_fill = nH > 0 ? P.fill_vec4 : 0;
-    int64_t blocks = (std::max<int64_t>(nc, n_fill) + 255) / 256;
-    if (blocks > 4096) blocks = 4096;
+    const int n_lam = n_jobs * row_tiles * 32;
+    const int blocks = std::max(1, std::min(64, (std::max(n_lam, 2 + n_jobs) + 255) / 256));
     profile_mark(kStageZero, false, stream);
-    reset_workspace<<<(unsigned)blocks, 256, 0, st>>>(P.counters, nc, reinterpret_cast<u32x4*>(P.stats), n_fill);
-    profile_mark(kStageZero, true, stream);
+    reset_counters<<<blocks, 256, 0, st>>>(P.counters, 2 + n_jobs, reinterpret_cast<uint32_t*>(P.lam), n_lam);
+    profile_mark(kStageZero, true, stream);   // the status word is cleared even without jobs
   }
-  int err = 0;
-  const int ntg = P.row_tiles_per_group;
-  if (row_tiles == 4 && ntg == 1) err = launch_evict<4, 1>(P, st, stream);
-  else if (row_tiles == 4 && ntg == 2) err = launch_evict<4, 2>(P, st, stream);
-  else if (row_tiles == 4) err = launch_evict<4, 4>(P, st, stream);
-  else if (ntg == 1) err = launch_evict<8, 1>(P, st, stream);
-  else if (ntg == 2) err = launch_evict<8, 2>(P, st, stream);
-  else if (ntg == 4) err = launch_evict<8, 4>(P, st, stream);
-  else err = launch_evict<8, 8>(P, st, stream);
-  if (err) return err;
+  if (n_jobs > 0) {
+    const int ntg = P.row_tiles_per_group;
+    int err = 0;
+    if (row_tiles == 4 && ntg == 1) err = launch_score<4, 1>(P, st, stream);
+    else if (row_tiles == 4 && ntg == 2) err = launch_score<4, 2>(P, st, stream);
+    else if (row_tiles == 4) err = launch_score<4, 4>(P, st, stream);
+    else if (ntg == 1) err = launch_score<8, 1>(P, st, stream);
+    else if (ntg == 2) err = launch_score<8, 2>(P, st, stream);
+    else if (ntg == 4) err = launch_score<8, 4>(P, st, stream);
+    else err = launch_score<8, 8>(P, st, stream);
+    if (err) return err;
+    static bool lds_set = false;
+    if (!lds_set) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
+      if (e == hipSuccess)
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_regs_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
+      if (e != hipSuccess) return (int)e;
+      lds_set = true;
+    }
+    // registers hold every candidate score when the prompt is short enough and the edge sums fit
+    const size_t dyn = sizeof(float) * ((size_t)P.n_slices * P.group * 4 * P.pool_half +
+                                        (size_t)(P.n_slices > 0 ? P.n_slices - 1 : 0) * 2 * P.pool_half);
+    profile_mark(kStageSelect, false, stream);
+    if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - kHistBins * 4 - 256)
+      select_regs_kernel<<<n_jobs, kSelThreads, dyn, st>>>(P);
+    else
+      select_kernel<<<n_jobs, kThreads, kSelectLds, st>>>(P);
+    profile_mark(kStageSelect, true, stream);
+  }
+  int max_keep = 0;
+  for (int i = 0; i < P.n_gather; ++i) max_keep = std::max(max_keep, P.layer[P.gather_layer[i]].n_keep);
+  if (P.n_gather > 0 && max_keep > 0) {
+    const int n_parts = (max_keep + kGatherRows - 1) / kGatherRows;
+    const int64_t n_items = (int64_t)P.n_gather * P.batch * P.n_kv_heads * n_parts;
+    const int grid = (int)std::min<int64_t>(n_items, (int64_t)device_cus() * 32);
+    profile_mark(kStageGather, false, stream);
+    gather_kernel<<<grid, kThreads, 0, st>>>(P, n_parts, n_items);
+    profile_mark(kStageGather, true, stream);
+  }
   return (int)hipGetLastError();
 }
 

@@ -13,10 +13,10 @@ namespace rkv {
 
 constexpr int kHeadDim = 128;      // head_dim the kernels are built for
 constexpr int kMaxLayersPerLaunch = 32;
-constexpr int kChunk = 768;        // keys per scoring work item (4 waves x 6 tiles of 32)
+constexpr int kSlice = 128;        // keys per scoring work item (4 waves x one tile of 32)
 constexpr int kMaxRowTiles = 8;    // G * ceil(w / 32) supported by the scoring kernel
 constexpr int kMaxPoolHalf = 64;   // pool_kernel / 2 supported
-constexpr int kGatherParts = 4;    // gather work items per (sequence, layer, KV head)
+constexpr int kGatherRows = 128;   // retained rows per gather work item
 
 // Per-layer work description of one prefill launch group.
 struct PrefillLayer {
@@ -38,48 +38,41 @@ struct PrefillLayer {
   int32_t all;            // 1: every position kept (FULL or b >= L)
 };
 
-// One launch of the fused eviction kernel over a group of up to 32 layers.
-// Work items, in ticket order (ticket = atomic counter, so items start in this order):
-//   step s: stats items of head s, score items of head s - lag_score, the select item of head
-//   s - lag_score - lag_select and the gather items of head s - lag_score - lag_select -
-//   lag_gather; then the copy items of the layers that are not scored.  Heads are (scored slot, sequence, KV head) triples.
+// One prefill launch group (up to 32 layers).  A scored "job" is a (scored layer slot,
+// sequence, KV head) triple, job = (slot * B + b) * Hkv + h; its keys are cut into n_slices
+// slices of kSlice keys, the scoring work items.
 struct PrefillLaunch {
   PrefillLayer layer[kMaxLayersPerLaunch];
   int32_t n_layers;
-  int32_t n_scored;
+  int32_t n_scored;       // scored layer slots
+  int32_t n_gather;       // layers with retained rows (gather list)
   int32_t batch, seq_len, n_q_heads, n_kv_heads, window;
   int32_t group;          // G = Hq / Hkv
   int32_t row_tiles_per_group;  // ceil(w / 32)
-  int32_t n_chunks;       // ceil(L / kChunk)
+  int32_t n_slices;       // ceil(L / kSlice)
   int32_t pool_half;      // pool_kernel / 2
-  int32_t want_unpooled;  // write the unpooled score array (acc seeding) for SnapKV layers
-  int32_t lag_score;      // steps from a head's stats items to its score items
-  int32_t lag_select;     // steps from its score items to its select item
-  int32_t lag_gather;     // steps from its select item to its gather items
-  int32_t n_unscored;     // layers copied without scoring
-  int32_t n_tickets;      // total work items (= grid size)
+  int32_t want_unpooled;  // write the unpooled group-mean score (acc seeding of SnapKV layers)
   float scale_log2;       // log2(e) / sqrt(d)
+  int32_t score_lag;      // two-pass scoring: items between pass A and pass B of the same item
+  int32_t force_two_pass; // use the two-pass scoring kernel even where the single-pass one applies
   // workspace regions
-  uint32_t* counters;     // [0] status, [1] unused, then per head: selection done
-  // stats .. edge are contiguous; the reset kernel fills them with NaN ("not written yet")
-  float* stats;           // [n_heads][n_chunks][R][2]  chunk row max (log2 units) / sum
-  int64_t fill_vec4;      // 16-byte units from `stats` to the end of `edge`
-  float* S;               // [n_heads][L]  ranking score
-  float* Su;              // [n_heads][L]  unpooled group-mean score (SnapKV layers, if wanted)
-  float* edge;            // [n_heads][n_chunks][G][4 * pool_half] per-query-head A at chunk edges
-  int32_t slot_layer[kMaxLayersPerLaunch];       // scored slot -> layer index in this group
-  int32_t unscored_layer[kMaxLayersPerLaunch];   // unscored layer list
+  uint32_t* counters;     // [0] status, [1] spare, [2, 2+J) slice arrivals, [2+J, 2+2J) normaliser ready
+  float* stats;           // [J][n_slices][R][2]  per-slice row max (log2 units) and sum of exp2
+  float* lam;             // [J][R]  per-row log2 softmax normaliser (+inf for rows without keys)
+  float* S;               // [J][L]  ranking score
+  float* Su;              // [J][L]  unpooled group-mean score (SnapKV layers, if wanted)
+  float* edge;            // [J][n_slices][G][4 * pool_half]  per-query-head column sums at slice edges
+  int32_t slot_layer[kMaxLayersPerLaunch];     // scored slot -> layer index in this group
+  int32_t gather_layer[kMaxLayersPerLaunch];   // layers with retained rows
 };
 
 static_assert(sizeof(PrefillLaunch) <= 4000, "kernel argument block too large");
 
 // Workspace layout for one launch group.
 struct PrefillWorkspace {
-  size_t counters, stats, S, Su, edge, end, total;
+  size_t counters, stats, lam, S, Su, edge, end, total;
 };
-
-PrefillWorkspace prefill_workspace_layout(int n_heads, int n_chunks, int rows, int seq_len, int group,
-                                          int pool_half, bool want_unpooled);
+PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half);
 
 // Error reporting (thread-local last error).
 int fail(int status, const std::string& msg);

@@ -69,7 +69,7 @@ def test_single_layer_1k(rule):
 
 @pytest.mark.parametrize("L", [33, 300, 777, 1000, 2049])
 def test_ragged_lengths(L):
-    """Context lengths that are not multiples of the 256-key chunk (several chunks + a tail)."""
+    """Context lengths that are not multiples of the 128-key slice (several slices + a tail)."""
     b = min(100, L - 1)
     rules = [OP.SNAPKV, OP.H2O, OP.STREAMING]
     run_case(rules, [b, b, b], [[gen(7, 0, l, L)] for l in range(3)], window=32, label=f"L{L}")
@@ -165,3 +165,11 @@ def test_repeat_runs_are_bitwise_identical():
     for key in ("idx", "scores", "acc", "k_out", "v_out"):
         for l in range(3):
             assert torch.equal(a[key][l], b[key][l]), (key, l)
+
+
+def test_two_pass_kernel_matches_oracle(monkeypatch):
+    """The two-pass scoring kernel (used for prompts whose slices do not all fit in the resident
+    workgroups at once) on the 1K case and a ragged length, forced through the test hook."""
+    monkeypatch.setenv("RKV_FORCE_TWO_PASS", "1")
+    run_case([OP.SNAPKV, OP.H2O], [128, 128], [[gen(1, 0, 0, 1024)], [gen(1, 0, 1, 1024)]], window=32, label="tp1k")
+    run_case([OP.SNAPKV, OP.H2O], [100, 100], [[gen(7, 0, 0, 777)], [gen(7, 0, 1, 777)]], window=32, label="tp777")
