@@ -1,0 +1,98 @@
+"""HBM traffic of the scoring kernel from two rocprofv3 counter runs.
+
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir_fetch> -o run -- python3 bench.py \
+        --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir_write> -o run -- (same command)
+    python -m paper_2606_15157_amd.pmc_summary <dir_fetch> <dir_write> <out.json> <out.md>
+
+FETCH_SIZE / WRITE_SIZE (KiB per dispatch) are scaled by what the same counter reads for the
+plain 1 GiB device copy that --copy-calibration runs (bytes known exactly), and the result is
+stored with the hash of the kernel source it was measured on.
+"""
+from __future__ import annotations
+
+import csv
+import glob
+import hashlib
+import json
+import os
+import statistics
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+KERNEL_SRC = os.path.join(ROOT, "paper_2606_15157_amd", "csrc", "prefill.hip")
+SCORE_NAME = "score_fused_kernel<4, 1>"
+COPY_NAME = "__amd_rocclr_copyBuffer"
+COPY_BYTES = 1 << 30
+
+
+def per_dispatch(run_dir: str, counter: str):
+    """{kernel name: [counter value per dispatch]} from a rocprofv3 counter_collection CSV."""
+    path = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not path:
+        raise FileNotFoundError(f"no counter_collection.csv under {run_dir}")
+    acc = {}
+    for row in csv.DictReader(open(path[0])):
+        if row["Counter_Name"] != counter:
+            continue
+        key = (row["Kernel_Name"], row["Dispatch_Id"])
+        acc[key] = acc.get(key, 0.0) + float(row["Counter_Value"])   # sum over XCDs / instances
+    out = {}
+    for (name, _), v in acc.items():
+        out.setdefault(name, []).append(v)
+    return out
+
+
+def pick(d, needle):
+    for name, vals in d.items():
+        if needle in name:
+            return name, vals
+    raise KeyError(needle)
+
+
+def main(argv):
+    fetch_dir, write_dir, out_json, out_md = argv[1:5]
+    fetch = per_dispatch(fetch_dir, "FETCH_SIZE")
+    write = per_dispatch(write_dir, "WRITE_SIZE")
+    _, copy_f = pick(fetch, COPY_NAME)
+    _, copy_w = pick(write, COPY_NAME)
+    cf, cw = max(copy_f), max(copy_w)          # the 1 GiB calibration copy is the largest
+    f_scale, w_scale = COPY_BYTES / cf, COPY_BYTES / cw
+    name, sf = pick(fetch, SCORE_NAME)
+    _, sw = pick(write, SCORE_NAME)
+    read_b = statistics.median(sf) * f_scale
+    write_b = statistics.median(sw) * w_scale
+    rec = {
+        "kernel": name,
+        "kernel_source_sha256": hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest(),
+        "fetch_kib_median": statistics.median(sf),
+        "write_kib_median": statistics.median(sw),
+        "copy_calibration_bytes": COPY_BYTES,
+        "copy_fetch_kib": cf,
+        "copy_write_kib": cw,
+        "fetch_scale": f_scale,
+        "write_scale": w_scale,
+        "hbm_read_bytes_per_launch": read_b,
+        "hbm_write_bytes_per_launch": write_b,
+        "hbm_bytes_per_launch": read_b + write_b,
+        "dispatches": len(sf),
+    }
+    json.dump(rec, open(out_json, "w"), indent=1)
+    with open(out_md, "w") as f:
+        f.write(f"# HBM traffic of {name} (32-layer mixed route, L=8192)\n\n")
+        f.write("Commands (each in its own run, from /tmp with TMPDIR=/tmp):\n\n")
+        f.write("    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <fetch> -o run -- python3 bench.py "
+                "--steps 5 --warmup 2 --no-cpu-baseline --copy-calibration\n")
+        f.write("    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write> -o run -- python3 bench.py "
+                "--steps 5 --warmup 2 --no-cpu-baseline --copy-calibration\n")
+        f.write("    python -m paper_2606_15157_amd.pmc_summary <fetch> <write> <json> <md>\n\n")
+        f.write("| quantity | value |\n|---|---|\n")
+        for k in ("fetch_kib_median", "write_kib_median", "copy_fetch_kib", "copy_write_kib", "fetch_scale",
+                  "write_scale", "hbm_read_bytes_per_launch", "hbm_write_bytes_per_launch", "hbm_bytes_per_launch",
+                  "dispatches"):
+            f.write(f"| {k} | {rec[k]:.6g} |\n" if isinstance(rec[k], float) else f"| {k} | {rec[k]} |\n")
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main(sys.argv)
