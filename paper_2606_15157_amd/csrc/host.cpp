@@ -157,7 +157,7 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
   PrefillWorkspace w{};
   size_t off = 0;
   w.counters = off;
-  off = round_up(off + sizeof(uint32_t) * (2 + 2 * (size_t)n_jobs), 256);
+  off = round_up(off + sizeof(uint32_t) * kCounterStride * (1 + (size_t)n_jobs), 256);
   w.stats = off;
   off = round_up(off + sizeof(float) * 2 * (size_t)n_jobs * n_slices * rows, 256);
   w.lam = off;

@@ -43,6 +43,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;            // 4 waves, one per SIMD
 constexpr int kWaves = kThreads / 64;
@@ -50,6 +51,9 @@ static_assert(kSlice == kWaves * 32, "one 32-key tile per wave");
 constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kHistBins = 2048;
 constexpr int kSelectLds = 128 * 1024;   // dynamic LDS of the select kernel (scores cached up to ~30K keys)
+
+// Cache policy of a device-coherent buffer load (sc1: served from the device-wide coherence point).
+constexpr int kCoherent = 16;
 
 __device__ __forceinline__ void store_coherent(float* p, float v) {
   __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -100,6 +104,8 @@ __device__ __forceinline__ void combine_ms(float& M, float& S, float m, float l)
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+// Index of this wave in the workgroup, as a wave-uniform (scalar) value.
+__device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
 // Waits for every outstanding load of this wave.  Used right after a batch of loads whose values
 // feed predicated stores: with loads still pending at the branch joins, the compiler would wait
@@ -202,7 +208,7 @@ __device__ __forceinline__ void issue_q_to_lds(uint16_t* sQ, const uint16_t* qjo
   constexpr int kPerWave = R * 16 / kThreads;   // instructions per wave
   int lane = threadIdx.x & 63;
   asm volatile("" : "+v"(lane));               // recompute the lane addresses here, do not keep them live
-  const int wv = threadIdx.x >> 6;
+  const int wv = wave_id();
 #pragma unroll
   for (int i = 0; i < kPerWave; ++i) {
     const int base = (i * kWaves + wv) * 64;    // first chunk this instruction writes
@@ -345,43 +351,48 @@ __device__ void fold_job(const PrefillLaunch& P, int job, float2 (*sPart)[R]) {
   }
 }
 
-// Fold used by the single-pass kernel: thread = (row pair, slice group); the statistics of up to
-// 8 slices per thread are loaded together (16 B each) before they are combined.
+// Fold used by the single-pass kernel.  Every slice of the job has published one log2-normaliser
+// per row (its tile max plus log2 of its sum, -inf for no visible key); they are copied into
+// sBuf (the query block's LDS space, R * 256 B, free at this point) by device-coherent LDS DMA,
+// 64 slices per round, and combined per row (thread = row, slice group).  The job's normalisers
+// go to memory and to sLam.
 template <int R>
-__device__ void fold_job_pairs(const PrefillLaunch& P, int job, float2 (*sPart)[R]) {
-  constexpr int kPairs = R / 2;
-  constexpr int kGroups = kThreads / kPairs;     // slice groups
-  static_assert(kGroups >= 1 && kGroups * 2 <= 2 * kWaves, "partials fit the statistics buffer");
-  const int tid = threadIdx.x, nsl = P.n_slices;
-  const int pr = tid % kPairs, j = tid / kPairs;
-  float M0 = -__builtin_inff(), Z0 = 0.f, M1 = -__builtin_inff(), Z1 = 0.f;
-  const float* st = P.stats + (size_t)job * nsl * R * 2 + 4 * pr;
-  for (int c0 = j; c0 < nsl; c0 += kGroups * 8) {
-    float4 v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int cc = c0 + u * kGroups;
-      if (cc < nsl) {
-        const float2 a = load_coherent2(st + (size_t)cc * R * 2), b = load_coherent2(st + (size_t)cc * R * 2 + 2);
-        v[u] = make_float4(a.x, a.y, b.x, b.y);
-      } else {
-        v[u] = make_float4(-__builtin_inff(), 0.f, -__builtin_inff(), 0.f);
-      }
+__device__ void fold_job_fused(const PrefillLaunch& P, int job, uint16_t* sBuf, float2 (*sPart)[R], float* sLam) {
+  constexpr int kGroups = kThreads / R;          // slice groups
+  constexpr int kChunk = 64;                     // slices per LDS round: 64 * R * 4 B = R * 256 B
+  static_assert(kGroups >= 1 && kGroups <= kWaves, "partials fit the statistics buffer");
+  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), nsl = P.n_slices;
+  const int r = tid % R, j = tid / R;
+  const float NEG_INF = -__builtin_inff();
+  const char* src = reinterpret_cast<const char*>(P.stats + (size_t)job * nsl * R);
+  const float* sF = reinterpret_cast<const float*>(sBuf);
+  float M = NEG_INF, Z = 0.f;
+  for (int c0 = 0; c0 < nsl; c0 += kChunk) {
+    const int n = min(kChunk, nsl - c0);
+    const int bytes = n * R * (int)sizeof(float), n_inst = (bytes + 1023) >> 10;   // 1 KiB per wave instruction
+    for (int i = wv; i < n_inst; i += kWaves) {
+      const int o = i * 1024 + lane * 16;
+      const char* g = src + (size_t)c0 * R * sizeof(float) + (o < bytes ? o : 0);
+      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
+                                       (__attribute__((address_space(3))) void*)(sBuf + i * 512), 16, 0, kCoherent);
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      combine_ms(M0, Z0, v[u].x, v[u].y);
-      combine_ms(M1, Z1, v[u].z, v[u].w);
+    loads_done();
+    __syncthreads();
+    for (int c = j; c < n; c += kGroups) {
+      const float x = sF[c * R + r];
+      combine_ms(M, Z, x, x > NEG_INF ? 1.f : 0.f);
     }
+    __syncthreads();
   }
-  sPart[j][2 * pr] = make_float2(M0, Z0);
-  sPart[j][2 * pr + 1] = make_float2(M1, Z1);
+  sPart[j][r] = make_float2(M, Z);
   __syncthreads();
   if (tid < R) {
     float m = sPart[0][tid].x, z = sPart[0][tid].y;
 #pragma unroll
     for (int q = 1; q < kGroups; ++q) combine_ms(m, z, sPart[q][tid].x, sPart[q][tid].y);
-    store_coherent(P.lam + (size_t)job * R + tid, z > 0.f ? m + __log2f(z) : __builtin_inff());
+    const float lam = z > 0.f ? m + __log2f(z) : __builtin_inff();
+    store_coherent(P.lam + (size_t)job * R + tid, lam);
+    sLam[tid] = lam;
   }
 }
 
@@ -407,7 +418,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
   __shared__ float sCol[NG][kSlice];
   __shared__ int sFlag;
 
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hf = lane >> 5, ln = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
   const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
   const int nsl = P.n_slices;
   const int n_jobs = B * P.n_scored * Hkv;
@@ -416,7 +427,6 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
   const float inv_g = 1.f / (float)G;
   const float NEG_INF = -__builtin_inff();
   uint32_t* status = P.counters;
-  uint32_t* arrive = P.counters + 2;
   const bool padded_rows = (G * NTH < NRT) || (w != NTH * 32);
 
   const int64_t first = blockIdx.x;
@@ -491,15 +501,22 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
       float M = NEG_INF, Z = 0.f;
 #pragma unroll
       for (int v = 0; v < kWaves; ++v) combine_ms(M, Z, sStat[v][tid].x, sStat[v][tid].y);
-      store_coherent2(P.stats + ((size_t)job * nsl + jc.slice) * R * 2 + 2 * tid, M, Z);
+      store_coherent(P.stats + ((size_t)job * nsl + jc.slice) * R + tid, Z > 0.f ? M + __log2f(Z) : NEG_INF);
     }
     vmem_release();
     __syncthreads();
-    if (tid == 0) sFlag = (int)__hip_atomic_fetch_add(&arrive[job], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + job);
+    if (tid == 0) sFlag = (int)__hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    if (sFlag == nsl - 1) {
+    const bool folder = sFlag == nsl - 1;
+    if (folder) {
+      // every slice has counted itself in: fold, let the normaliser stores retire, then raise the
+      // counter once more to say the normalisers are there
       vmem_acquire();
-      fold_job_pairs<R>(P, job, sStat);
+      fold_job_fused<R>(P, job, sQ, sStat, sLam);
+      vmem_release();
+      __syncthreads();
+      if (tid == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 
     // ---- the next item's query block loads while this one waits and finishes
@@ -507,19 +524,23 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
     advance(jn, dj, ds, nsl, B, Hkv);
     if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQ, q_of(jn), G, w);
 
-    // ---- wait (bounded) for the job's normalisers
-    if (tid < R) {
-      float lam = load_coherent(P.lam + (size_t)job * R + tid);
-      uint32_t it = 0;
-      while (lam != lam) {
-        __builtin_amdgcn_s_sleep(2);
-        lam = load_coherent(P.lam + (size_t)job * R + tid);
-        if (++it > kSpinLimit) {
-          atomicOr(status, 1u);
-          lam = __builtin_inff();
+    // ---- wait (bounded) for the job's normalisers: one lane polls the job's counter
+    if (!folder) {
+      if (tid == 0) {
+        uint32_t it = 0;
+        while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <= (uint32_t)nsl) {
+          __builtin_amdgcn_s_sleep(1);
+          if (++it > kSpinLimit) {
+            atomicOr(status, 1u);
+            break;
+          }
         }
       }
-      sLam[tid] = lam;
+      __syncthreads();
+      if (tid < R) {
+        const float lam = load_coherent(P.lam + (size_t)job * R + tid);
+        sLam[tid] = lam == lam ? lam : __builtin_inff();   // still "not written" only after a time-out
+      }
     }
     __syncthreads();
 
@@ -594,7 +615,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
   __shared__ float sCol[NG][kSlice];
   __shared__ int sFold;
 
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, hf = lane >> 5, ln = lane & 31;
+  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
   const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
   const int nsl = P.n_slices;
   const int n_jobs = B * P.n_scored * Hkv;
@@ -603,7 +624,6 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
   const float inv_g = 1.f / (float)G;
   const float NEG_INF = -__builtin_inff();
   uint32_t* status = P.counters;
-  uint32_t* arrive = P.counters + 2;
   const bool padded_rows = (G * NTH < NRT) || (w != NTH * 32);
 
   const int64_t first = blockIdx.x;
@@ -637,7 +657,8 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
     __syncthreads();
     const bool had_prev = t >= 1 && t - 1 < T;
     if (had_prev && tid == 0)
-      arrived = __hip_atomic_fetch_add(&arrive[jp.job], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      arrived = __hip_atomic_fetch_add(P.counters + (size_t)kCounterStride * (1 + jp.job), 1u, __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
 
     // ============================================================ pass B: window column sums
     const JobRef jbn = step(jb), jan = step(ja);   // the items after this iteration's
@@ -783,7 +804,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id();
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_slices;
   const int job = blockIdx.x;
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
@@ -965,7 +986,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   __shared__ int sHist[kHistBins];
   __shared__ int sScan[2 * kSelWaves];
   __shared__ int sSel[2];
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id();
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_slices;
   const int job = blockIdx.x;
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
@@ -1251,9 +1272,10 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   const int n_jobs = P.batch * P.n_scored * P.n_kv_heads;
   {
     const int n_lam = n_jobs * row_tiles * 32;
-    const int blocks = std::max(1, std::min(64, (std::max(n_lam, 2 + n_jobs) + 255) / 256));
+    const int n_cnt = kCounterStride * (1 + n_jobs);
+    const int blocks = std::max(1, std::min(64, (std::max(n_lam, n_cnt) + 255) / 256));
     profile_mark(kStageZero, false, stream);
-    reset_counters<<<blocks, 256, 0, st>>>(P.counters, 2 + n_jobs, reinterpret_cast<uint32_t*>(P.lam), n_lam);
+    reset_counters<<<blocks, 256, 0, st>>>(P.counters, n_cnt, reinterpret_cast<uint32_t*>(P.lam), n_lam);
     profile_mark(kStageZero, true, stream);   // the status word is cleared even without jobs
   }
   if (n_jobs > 0) {

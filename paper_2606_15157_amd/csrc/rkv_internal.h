@@ -17,6 +17,7 @@ constexpr int kSlice = 128;        // keys per scoring work item (4 waves x one 
 constexpr int kMaxRowTiles = 8;    // G * ceil(w / 32) supported by the scoring kernel
 constexpr int kMaxPoolHalf = 64;   // pool_kernel / 2 supported
 constexpr int kGatherRows = 128;   // retained rows per gather work item
+constexpr int kCounterStride = 32; // words between per-job counters (one 128-byte line each)
 
 // Per-layer work description of one prefill launch group.
 struct PrefillLayer {
@@ -56,7 +57,8 @@ struct PrefillLaunch {
   int32_t score_lag;      // two-pass scoring: items between pass A and pass B of the same item
   int32_t force_two_pass; // use the two-pass scoring kernel even where the single-pass one applies
   // workspace regions
-  uint32_t* counters;     // [0] status, [1] spare, [2, 2+J) slice arrivals, [2+J, 2+2J) normaliser ready
+  uint32_t* counters;     // [0] status; job j's counter at [kCounterStride * (1 + j)]: slice arrivals,
+                          // one more once the job's normalisers are written (single-pass scoring)
   float* stats;           // [J][n_slices][R][2]  per-slice row max (log2 units) and sum of exp2
   float* lam;             // [J][R]  per-row log2 softmax normaliser (+inf for rows without keys)
   float* S;               // [J][L]  ranking score
