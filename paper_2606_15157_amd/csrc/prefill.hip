@@ -378,10 +378,16 @@ __device__ void fold_job_fused(const PrefillLaunch& P, int job, uint16_t* sBuf, 
     }
     loads_done();
     __syncthreads();
-    for (int c = j; c < n; c += kGroups) {
-      const float x = sF[c * R + r];
-      combine_ms(M, Z, x, x > NEG_INF ? 1.f : 0.f);
+    // this chunk's maximum first, then the sum of exp2 against it (independent terms)
+    float m = NEG_INF;
+#pragma unroll 8
+    for (int c = j; c < n; c += kGroups) m = fmaxf(m, sF[c * R + r]);
+    float z = 0.f;
+    if (m > NEG_INF) {
+#pragma unroll 8
+      for (int c = j; c < n; c += kGroups) z += __builtin_amdgcn_exp2f(sF[c * R + r] - m);
     }
+    combine_ms(M, Z, m, z);
     __syncthreads();
   }
   sPart[j][r] = make_float2(M, Z);
@@ -510,39 +516,43 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
     __syncthreads();
     const bool folder = sFlag == nsl - 1;
     if (folder) {
-      // every slice has counted itself in: fold, let the normaliser stores retire, then raise the
-      // counter once more to say the normalisers are there
+      // every slice has counted itself in: fold (the normalisers go out over their NaN marks)
       vmem_acquire();
       fold_job_fused<R>(P, job, sQ, sStat, sLam);
-      vmem_release();
-      __syncthreads();
-      if (tid == 0) __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-
-    // ---- the next item's query block loads while this one waits and finishes
-    JobRef jn = jc;
-    advance(jn, dj, ds, nsl, B, Hkv);
-    if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQ, q_of(jn), G, w);
-
-    // ---- wait (bounded) for the job's normalisers: one lane polls the job's counter
-    if (!folder) {
-      if (tid == 0) {
-        uint32_t it = 0;
-        while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) <= (uint32_t)nsl) {
-          __builtin_amdgcn_s_sleep(1);
-          if (++it > kSpinLimit) {
-            atomicOr(status, 1u);
-            break;
-          }
+    } else if (wv == 0) {
+      // ---- wait (bounded) for the job's normalisers: wave 0 reads all of them at once until
+      // none is still marked "not written"
+      const float* lj = P.lam + (size_t)job * R;
+      uint32_t it = 0;
+      while (true) {
+        float v[R / 64];
+#pragma unroll
+        for (int u = 0; u < R / 128; ++u) {
+          const float2 x = load_coherent2(lj + 128 * u + 2 * lane);
+          v[2 * u] = x.x;
+          v[2 * u + 1] = x.y;
         }
-      }
-      __syncthreads();
-      if (tid < R) {
-        const float lam = load_coherent(P.lam + (size_t)job * R + tid);
-        sLam[tid] = lam == lam ? lam : __builtin_inff();   // still "not written" only after a time-out
+        bool ok = true;
+#pragma unroll
+        for (int u = 0; u < R / 64; ++u) ok = ok && (v[u] == v[u]);
+        if (__builtin_amdgcn_ballot_w64(!ok) == 0 || ++it > kSpinLimit) {
+          if (!(__builtin_amdgcn_ballot_w64(!ok) == 0) && lane == 0) atomicOr(status, 1u);
+#pragma unroll
+          for (int u = 0; u < R / 128; ++u) {
+            sLam[128 * u + 2 * lane] = v[2 * u] == v[2 * u] ? v[2 * u] : __builtin_inff();
+            sLam[128 * u + 2 * lane + 1] = v[2 * u + 1] == v[2 * u + 1] ? v[2 * u + 1] : __builtin_inff();
+          }
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
       }
     }
     __syncthreads();
+
+    // ---- the next item's query block loads during this one's window sums (sQ is free now)
+    JobRef jn = jc;
+    advance(jn, dj, ds, nsl, B, Hkv);
+    if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQ, q_of(jn), G, w);
 
     // ---- probabilities and their sums over the window rows (across lanes)
     float alpha[NRT];

@@ -57,8 +57,7 @@ struct PrefillLaunch {
   int32_t score_lag;      // two-pass scoring: items between pass A and pass B of the same item
   int32_t force_two_pass; // use the two-pass scoring kernel even where the single-pass one applies
   // workspace regions
-  uint32_t* counters;     // [0] status; job j's counter at [kCounterStride * (1 + j)]: slice arrivals,
-                          // one more once the job's normalisers are written (single-pass scoring)
+  uint32_t* counters;     // [0] status; job j's slice-arrival counter at [kCounterStride * (1 + j)]
   float* stats;           // [J][n_slices][R][2]  per-slice row max (log2 units) and sum of exp2
   float* lam;             // [J][R]  per-row log2 softmax normaliser (+inf for rows without keys)
   float* S;               // [J][L]  ranking score
