@@ -7,24 +7,21 @@
 // A row's softmax is normalised over every key while the window sum runs over rows, so a row's
 // normaliser is known only once every key of the job has been seen.  Work items are (job,
 // slice of 128 keys); each of the four waves of a workgroup takes one 32-key tile of the slice.
-//   scoring kernel (persistent, two passes per item with a fixed lag between them):
-//     pass A streams the K tile from HBM into registers and multiplies it by the job's G*w
-//       query rows (in LDS) on MFMA with the keys as the A operand, so a lane holds one window
-//       row and the row max / sum of exp2 need no cross-lane work; the slice publishes them;
-//     the slice of a job that counts itself in last folds all slices into one log2-normaliser
-//       per row;
-//     pass B, `lag` items later, re-reads the tile (L2 / MALL) and multiplies with the queries
-//       as the A operand, so a lane holds one key; the accumulator starts at -normaliser, exp2
-//       gives probabilities and the window sum over rows stays inside the lane; max-pool inside
-//       the slice (SnapKV) and the group mean give S;
-//   select kernel (one workgroup per job): repairs the pooled score next to slice borders,
-//     finds the k-th largest score with three radix-histogram passes and writes the retained
-//     positions in ascending order;
+//   single-pass scoring kernel (persistent; every slice of a job in flight at once): a slice
+//     streams its K tile from HBM once, keeps the exponentials of its logits in registers,
+//     publishes one log2-normaliser per window row and counts itself in; the job's first slice
+//     folds them into the job's normalisers once all have counted in; every slice then turns its
+//     exponentials into probabilities, sums them over the window rows, pools (SnapKV) and
+//     averages over the query group;
+//   two-pass scoring kernel (prompts too long for every slice of a job to be in flight): pass A
+//     streams the tile and publishes its statistics, pass B re-reads it a fixed number of items
+//     later (L2 / MALL) and recomputes the logits with the normalisers known;
+//   select kernels (one workgroup per job): repair the pooled score next to slice borders, find
+//     the k-th largest score with three radix-histogram passes and write the retained positions
+//     in ascending order;
 //   gather kernel: copies the retained K and V rows.
-// K is read from HBM once; the logits are formed twice (MFMA is not the bound, and no
-// exponentials have to be held across the wait for the normaliser).
 //
-// Data handed between workgroups of one launch goes through agent-scope relaxed atomics
+// Data handed between workgroups of one launch goes through device-coherent loads and stores
 // (they bypass the XCD-local caches); a slice counts itself in only after a vmcnt(0) wait has
 // retired its statistics stores, and normalisers are written once over a NaN "not written"
 // mark, so no agent-scope fence (which would flush and invalidate L2) is needed.  Every wait is
@@ -205,20 +202,25 @@ __device__ __forceinline__ int rs_sel(int lane) {
 template <int NRT, int NTH>
 __device__ __forceinline__ void issue_q_to_lds(uint16_t* sQ, const uint16_t* qjob, int G, int w) {
   constexpr int R = NRT * 32;
-  constexpr int kPerWave = R * 16 / kThreads;   // instructions per wave
-  int lane = threadIdx.x & 63;
-  asm volatile("" : "+v"(lane));               // recompute the lane addresses here, do not keep them live
-  const int wv = wave_id();
+  constexpr int kPerWave = R * 16 / kThreads;   // instructions per wave, 4 rows each
+  constexpr int kHeadRows = NTH * 32;           // padded rows per query head
+  const int lane = threadIdx.x & 63, wv = wave_id();
+  const int lr = lane >> 4;
+  // instruction i fills rows r0 = 4 (4 i + wv) .. r0 + 3: the low four row bits are (4 wv & 15) | lr
+  // for every i, so the chunk swizzle and the lane's byte offset are the same for all of them, and
+  // the four rows never straddle two query heads
+  const int c = (lane & 15) ^ (((4 * wv) & 15) | lr);
+  const uint32_t lane_off = (uint32_t)(lr * kHeadDim + c * 8) * 2u;
+  const uint32_t pad_off = (uint32_t)(c * 8) * 2u;
 #pragma unroll
   for (int i = 0; i < kPerWave; ++i) {
-    const int base = (i * kWaves + wv) * 64;    // first chunk this instruction writes
-    const int x = base + lane;
-    const int row = x >> 4, c = (x & 15) ^ (row & 15);
-    const int g = row / (NTH * 32), ii = row - g * (NTH * 32);
-    const size_t off = (g < G && ii < w) ? (size_t)(g * w + ii) * kHeadDim : 0;
+    const int r0 = 4 * (i * kWaves + wv);
+    const int g = r0 / kHeadRows, ii0 = r0 - g * kHeadRows;
+    const bool ok = g < G && ii0 + lr < w;
+    const uint32_t off = ok ? (uint32_t)((g * w + ii0) * kHeadDim) * 2u + lane_off : pad_off;
     __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(qjob + off + c * 8),
-        (__attribute__((address_space(3))) void*)(sQ + base * 8), 16, 0, 0);
+        (const __attribute__((address_space(1))) void*)(reinterpret_cast<const char*>(qjob) + off),
+        (__attribute__((address_space(3))) void*)(sQ + r0 * kHeadDim), 16, 0, 0);
   }
 }
 __device__ __forceinline__ bf16x8 q_frag(const uint16_t* sQ, int row, int chunk) {
@@ -406,13 +408,16 @@ __device__ void fold_job_fused(const PrefillLaunch& P, int job, uint16_t* sBuf, 
 // Single-pass scoring (prompts whose slices of one job fit in the resident workgroups at once).
 // Workgroup w takes items w, w + n_wg, ...; per item the four waves each multiply one 32-key
 // tile of K (A operand, straight from HBM) by the job's query rows (B operand, LDS):
-//   lane = window row, registers = 16 keys -> tile row max, e = exp2(z - max) and row sums stay
-//   in the lane; the slice publishes (max, sum) per row and counts itself in; the last slice of
-//   the job folds all slices into one log2-normaliser per row (NaN until written);
-//   every slice keeps e in registers, waits for the normalisers, rescales e into probabilities
-//   and sums them over the window rows with a 32-lane reduce-scatter (permlane16 swap + DPP),
-//   per query head for SnapKV, over the group for H2O; pooling and the group mean give S.
-// Three workgroups share a CU, so while one waits for its job's normalisers the others compute.
+//   phase A: lane = window row, registers = 16 keys -> tile row max, e = exp2(z - max) and row
+//     sums stay in the lane; the slice publishes one log2-normaliser per row and counts itself
+//     in; the last slice of the job folds all slices into the job's normalisers (NaN until
+//     written);
+//   phase B: once the job's normalisers are there, e is rescaled into probabilities and summed
+//     over the window rows with a 32-lane reduce-scatter (permlane16 swap + DPP), per query head
+//     for SnapKV, over the group for H2O; pooling and the group mean give S.
+// The job's first slice to count itself in folds the job once it reaches its own wait (it has
+// the most slack, so the fold never lands on the job's straggler).  Three workgroups share a CU
+// (four row tiles), so while one waits the others compute.
 // ---------------------------------------------------------------------------------------------
 template <int NRT, int NTH>
 __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel(const PrefillLaunch P, int n_wg) {
@@ -439,32 +444,22 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
   if (first >= n_items) return;
   const int T = (int)((n_items - 1 - first) / n_wg + 1);
   const int dj = n_wg / nsl, ds = n_wg - dj * nsl;   // item stride n_wg in (jobs, slices)
-  auto q_of = [&](const JobRef& j) -> const uint16_t* {
-    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
-    return ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim;
-  };
-  auto k_tile = [&](u32x4 (&dst)[8], const JobRef& j) {
-    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
-    load_k_tile(dst, ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim, j.slice * kSlice + wv * 32 + ln, L, hf);
-  };
-
   u32x4 kf[8];
-  JobRef jc = decode_item(first, nsl, B, Hkv);
-  issue_q_to_lds<NRT, NTH>(sQ, q_of(jc), G, w);
-  k_tile(kf, jc);
 
-#pragma unroll 1
-  for (int t = 0; t < T; ++t) {
-    const PrefillLayer& ly = P.layer[P.slot_layer[jc.slot]];
-    const bool snap = ly.rule == RKV_SNAPKV;
-    const int job = jc.job, cbase = jc.slice * kSlice, tile_key0 = cbase + wv * 32;
-    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // this item's query block and K tile
+  // the item's query block (LDS DMA) and this wave's K tile (registers)
+  auto issue_loads = [&](const JobRef& j) {
+    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
+    issue_q_to_lds<NRT, NTH>(sQ, ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim, G, w);
+    load_k_tile(kf, ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim, j.slice * kSlice + wv * 32 + ln, L, hf);
+  };
+
+  // ---- phase A: logits and exponentials; lane = window row ln of row tile rt, registers = keys
+  // tile_key0 + 8(r/4) + 4hf + r%4; the tile row maxima (log2 units, 0 for rows with no visible
+  // key) go to mw, the per-wave (max, sum) pairs to sStat
+  auto phase_a = [&](const JobRef& j, f32x16 (&e)[NRT], float (&mw)[NRT]) {
+    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // the item's query block and K tile
     __syncthreads();
-
-    // ---- logits and exponentials: lane = window row ln of row tile rt, registers = keys
-    // tile_key0 + 8(r/4) + 4hf + r%4
-    f32x16 e[NRT];
-    float mw[NRT];   // tile row max in log2 units (0 for rows with no visible key in the tile)
+    const int tile_key0 = j.slice * kSlice + wv * 32;
     const bool mask_a = padded_rows || tile_key0 + 32 > L - w;
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) {
@@ -474,14 +469,13 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
       for (int st = 0; st < 8; ++st)
         e[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[st]), q_frag(sQ, rt * 32 + ln, 8 * hf + st), e[rt],
                                                         0, 0, 0);
-      if (mask_a) {
+      if (__builtin_expect(mask_a, 0)) {
         const int g = rt / NTH, ii = (rt - g * NTH) * 32 + ln;
         const int last = (g < G && ii < w) ? min(L - 1, L - w + ii) : -1;
+        const int lim = last - tile_key0 - 4 * hf;   // register r holds key tile_key0 + 4 hf + 8 (r / 4) + r % 4
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int kk = tile_key0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-          if (kk > last) e[rt][r] = NEG_INF;
-        }
+        for (int r = 0; r < 16; ++r)
+          if (8 * (r >> 2) + (r & 3) > lim) e[rt][r] = NEG_INF;
       }
       // both half-waves hold the same rows, other keys
       float m = fmaxf(e[rt][0], e[rt][1]);
@@ -501,60 +495,79 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
       if (hf == 0) sStat[wv][rt * 32 + ln] = make_float2(mw[rt], z);
     }
     __syncthreads();
+  };
 
-    // ---- publish the slice's statistics and count it in (the stores retire first)
+  // ---- publish the slice's statistics and count it in (the stores retire first).  Returns
+  // whether this slice came first: that workgroup folds the job once it has to wait for it anyway
+  // (the first slice has the most slack, so folding never lands on the job's straggler).
+  auto publish = [&](const JobRef& j) -> bool {
     if (tid < R) {
       float M = NEG_INF, Z = 0.f;
 #pragma unroll
       for (int v = 0; v < kWaves; ++v) combine_ms(M, Z, sStat[v][tid].x, sStat[v][tid].y);
-      store_coherent(P.stats + ((size_t)job * nsl + jc.slice) * R + tid, Z > 0.f ? M + __log2f(Z) : NEG_INF);
+      store_coherent(P.stats + ((size_t)j.job * nsl + j.slice) * R + tid, Z > 0.f ? M + __log2f(Z) : NEG_INF);
     }
     vmem_release();
     __syncthreads();
-    uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + job);
+    uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + j.job);
     if (tid == 0) sFlag = (int)__hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    const bool folder = sFlag == nsl - 1;
-    if (folder) {
-      // every slice has counted itself in: fold (the normalisers go out over their NaN marks)
-      vmem_acquire();
-      fold_job_fused<R>(P, job, sQ, sStat, sLam);
-    } else if (wv == 0) {
-      // ---- wait (bounded) for the job's normalisers: wave 0 reads all of them at once until
-      // none is still marked "not written"
-      const float* lj = P.lam + (size_t)job * R;
+    return sFlag == 0;
+  };
+
+  // ---- the folder: wait (bounded, one lane) until every slice has counted itself in, then fold
+  // (the normalisers go to memory over their NaN marks and to sLam); the query block's LDS space
+  // stages the statistics (the next block loads after the wait)
+  auto fold = [&](const JobRef& j) {
+    if (tid == 0) {
+      uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + j.job);
       uint32_t it = 0;
-      while (true) {
-        float v[R / 64];
-#pragma unroll
-        for (int u = 0; u < R / 128; ++u) {
-          const float2 x = load_coherent2(lj + 128 * u + 2 * lane);
-          v[2 * u] = x.x;
-          v[2 * u + 1] = x.y;
-        }
-        bool ok = true;
-#pragma unroll
-        for (int u = 0; u < R / 64; ++u) ok = ok && (v[u] == v[u]);
-        if (__builtin_amdgcn_ballot_w64(!ok) == 0 || ++it > kSpinLimit) {
-          if (!(__builtin_amdgcn_ballot_w64(!ok) == 0) && lane == 0) atomicOr(status, 1u);
-#pragma unroll
-          for (int u = 0; u < R / 128; ++u) {
-            sLam[128 * u + 2 * lane] = v[2 * u] == v[2 * u] ? v[2 * u] : __builtin_inff();
-            sLam[128 * u + 2 * lane + 1] = v[2 * u + 1] == v[2 * u + 1] ? v[2 * u + 1] : __builtin_inff();
-          }
+      while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)nsl) {
+        __builtin_amdgcn_s_sleep(1);
+        if (++it > kSpinLimit) {
+          atomicOr(status, 1u);
           break;
         }
-        __builtin_amdgcn_s_sleep(1);
       }
     }
     __syncthreads();
+    vmem_acquire();
+    fold_job_fused<R>(P, j.job, sQ, sStat, sLam);
+  };
 
-    // ---- the next item's query block loads during this one's window sums (sQ is free now)
-    JobRef jn = jc;
-    advance(jn, dj, ds, nsl, B, Hkv);
-    if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQ, q_of(jn), G, w);
+  // ---- wait (bounded) for the job's normalisers: wave 0 reads all of them at once until none is
+  // still marked "not written"
+  auto wait_lam = [&](const JobRef& j) {
+    const float* lj = P.lam + (size_t)j.job * R;
+    uint32_t it = 0;
+    while (true) {
+      float v[R / 64];
+#pragma unroll
+      for (int u = 0; u < R / 128; ++u) {
+        const float2 x = load_coherent2(lj + 128 * u + 2 * lane);
+        v[2 * u] = x.x;
+        v[2 * u + 1] = x.y;
+      }
+      bool ok = true;
+#pragma unroll
+      for (int u = 0; u < R / 64; ++u) ok = ok && (v[u] == v[u]);
+      const bool done = __builtin_amdgcn_ballot_w64(!ok) == 0;
+      if (done || ++it > kSpinLimit) {
+        if (!done && lane == 0) atomicOr(status, 1u);
+#pragma unroll
+        for (int u = 0; u < R / 128; ++u) {
+          sLam[128 * u + 2 * lane] = v[2 * u] == v[2 * u] ? v[2 * u] : __builtin_inff();
+          sLam[128 * u + 2 * lane + 1] = v[2 * u + 1] == v[2 * u + 1] ? v[2 * u + 1] : __builtin_inff();
+        }
+        break;
+      }
+      __builtin_amdgcn_s_sleep(1);
+    }
+  };
 
-    // ---- probabilities and their sums over the window rows (across lanes)
+  // ---- phase B: probabilities and their sums over the window rows (across lanes), then scores
+  auto phase_b = [&](const JobRef& j, f32x16 (&e)[NRT], const float (&mw)[NRT]) {
+    const bool snap = P.layer[P.slot_layer[j.slot]].rule == RKV_SNAPKV;
     float alpha[NRT];
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) alpha[rt] = __builtin_amdgcn_exp2f(mw[rt] - sLam[rt * 32 + ln]);   // +inf -> 0
@@ -593,9 +606,24 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
         sCol[0][wv * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)] = ev[0][0];
       }
     }
-    if (t + 1 < T) k_tile(kf, jn);   // the next item's K tile (the other workgroups of the CU cover its latency)
     __syncthreads();
-    store_scores<NG>(P, snap, job, jc.slice, cbase, sCol, inv_g);
+    store_scores<NG>(P, snap, j.job, j.slice, j.slice * kSlice, sCol, inv_g);
+  };
+
+  f32x16 e[NRT];
+  float mw[NRT];
+  JobRef jc = decode_item(first, nsl, B, Hkv);
+  issue_loads(jc);
+#pragma unroll 1
+  for (int t = 0; t < T; ++t) {
+    phase_a(jc, e, mw);
+    if (publish(jc)) fold(jc);
+    else if (wv == 0) wait_lam(jc);
+    __syncthreads();
+    JobRef jn = jc;
+    advance(jn, dj, ds, nsl, B, Hkv);
+    if (t + 1 < T) issue_loads(jn);   // sQ is free; the loads land during phase B
+    phase_b(jc, e, mw);
     jc = jn;
   }
 }
