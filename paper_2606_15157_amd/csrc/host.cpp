@@ -431,6 +431,11 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     }
     P.n_scored = slot;
     P.n_gather = n_gather;
+    P.gather_item0[0] = 0;
+    for (int i = 0; i < n_gather; ++i) {
+      const int64_t rows = (int64_t)shape->batch * shape->n_kv_heads * P.layer[P.gather_layer[i]].n_keep;
+      P.gather_item0[i + 1] = P.gather_item0[i] + (int32_t)((rows + rkv::kGatherRows - 1) / rkv::kGatherRows);
+    }
     P.want_unpooled = want_unpooled ? 1 : 0;
     const int n_jobs = shape->batch * slot * shape->n_kv_heads;
     rkv::PrefillWorkspace W = rkv::prefill_workspace_layout(n_jobs, P.n_slices, ktiles * 32, L, G, P.pool_half);

@@ -1207,55 +1207,57 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
 // ---------------------------------------------------------------------------------------------
 // Gather: copy the retained K / V rows, 16 lanes x 16 B per row, 8 rows in flight per lane group.
 // ---------------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void gather_kernel(const PrefillLaunch P, int n_parts, int64_t n_items) {
-  const int tid = threadIdx.x;
-  const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len;
-  const int piece = tid & 15, rsub = tid >> 4;
-  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
-    const int part = (int)(item % n_parts);
-    const int64_t gj = item / n_parts;
-    const int h = (int)(gj % Hkv), s = (int)((gj / Hkv) % B), li = (int)(gj / ((int64_t)Hkv * B));
+// Gather: the retained K and V rows, bit for bit.  Work items are (gather layer, kGatherRows
+// output rows), flat over the layer's (sequence, KV head, kept row) rows, so an item never spans
+// two layers and the layer is looked up once per item; thread = (row tid / 16 + 16 u, 16-byte
+// piece tid % 16).  Unscored layers (StreamingLLM, Full) also write their closed-form positions
+// and a zero accumulator.
+// ---------------------------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void gather_kernel(const PrefillLaunch P) {
+  constexpr int U = kGatherRows / 16;
+  const int tid = threadIdx.x, piece = tid & 15, rsub = tid >> 4;
+  const int Hkv = P.n_kv_heads, L = P.seq_len, n_gl = P.n_gather;
+  const int n_items = P.gather_item0[n_gl];
+  int li = 0;
+  for (int item = blockIdx.x; item < n_items; item += gridDim.x) {
+    while (li + 1 < n_gl && P.gather_item0[li + 1] <= item) ++li;   // items only grow
     const PrefillLayer& ly = P.layer[P.gather_layer[li]];
-    const int bh = s * Hkv + h;
-    const int n_keep = ly.n_keep;
-    const int r0 = part * kGatherRows, r1 = min(n_keep, r0 + kGatherRows);
-    if (r1 <= r0) continue;
+    const int n_keep = ly.n_keep, rows = P.batch * Hkv * n_keep;
+    const int o0 = (item - P.gather_item0[li]) * kGatherRows;
     const bool scored = ly.slot >= 0;
-    int32_t* idx = ly.idx + (size_t)bh * n_keep;
-    const size_t hbase = (size_t)bh * L;
-    for (int m0 = r0; m0 < r1; m0 += 16 * 8) {
-      int pos[8];
+    int pos[U], bh[U];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int m = m0 + rsub + 16 * u;
-        pos[u] = -1;
-        if (m < r1) {
-          if (scored) pos[u] = idx[m];
-          else pos[u] = ly.all ? m : (m < ly.cand_end ? m : ly.forced_lo + (m - ly.cand_end));
-        }
+    for (int u = 0; u < U; ++u) {
+      const int o = o0 + rsub + 16 * u;
+      pos[u] = -1;
+      bh[u] = 0;
+      if (o < rows) {
+        bh[u] = o / n_keep;
+        const int m = o - bh[u] * n_keep;
+        pos[u] = scored ? ly.idx[o] : (ly.all ? m : (m < ly.cand_end ? m : ly.forced_lo + (m - ly.cand_end)));
       }
-      loads_done();
-      u32x4 kv[8], vv[8];
+    }
+    loads_done();
+    u32x4 kv[U], vv[U];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (pos[u] >= 0) {
-          const size_t src = (hbase + pos[u]) * kHeadDim + piece * 8;
-          kv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.k + src));
-          vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.v + src));
-        }
+    for (int u = 0; u < U; ++u) {
+      if (pos[u] >= 0) {
+        const size_t src = ((size_t)bh[u] * L + pos[u]) * kHeadDim + piece * 8;
+        kv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.k + src));
+        vv[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(ly.v + src));
       }
-      loads_done();
+    }
+    loads_done();
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int m = m0 + rsub + 16 * u;
-        if (pos[u] >= 0) {
-          const size_t dst = ((size_t)bh * n_keep + m) * kHeadDim + piece * 8;
-          __builtin_nontemporal_store(kv[u], reinterpret_cast<u32x4*>(ly.k_out + dst));
-          __builtin_nontemporal_store(vv[u], reinterpret_cast<u32x4*>(ly.v_out + dst));
-          if (!scored && piece == 0) {
-            idx[m] = pos[u];
-            if (ly.acc) ly.acc[(size_t)bh * n_keep + m] = 0.f;
-          }
+    for (int u = 0; u < U; ++u) {
+      if (pos[u] >= 0) {
+        const int o = o0 + rsub + 16 * u;
+        const size_t dst = (size_t)o * kHeadDim + piece * 8;
+        __builtin_nontemporal_store(kv[u], reinterpret_cast<u32x4*>(ly.k_out + dst));
+        __builtin_nontemporal_store(vv[u], reinterpret_cast<u32x4*>(ly.v_out + dst));
+        if (!scored && piece == 0) {
+          ly.idx[o] = pos[u];
+          if (ly.acc) ly.acc[o] = 0.f;
         }
       }
     }
@@ -1347,14 +1349,11 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
       select_kernel<<<n_jobs, kThreads, kSelectLds, st>>>(P);
     profile_mark(kStageSelect, true, stream);
   }
-  int max_keep = 0;
-  for (int i = 0; i < P.n_gather; ++i) max_keep = std::max(max_keep, P.layer[P.gather_layer[i]].n_keep);
-  if (P.n_gather > 0 && max_keep > 0) {
-    const int n_parts = (max_keep + kGatherRows - 1) / kGatherRows;
-    const int64_t n_items = (int64_t)P.n_gather * P.batch * P.n_kv_heads * n_parts;
-    const int grid = (int)std::min<int64_t>(n_items, (int64_t)device_cus() * 32);
+  const int n_gather_items = P.n_gather > 0 ? P.gather_item0[P.n_gather] : 0;
+  if (n_gather_items > 0) {
+    const int grid = std::min(n_gather_items, device_cus() * 8);
     profile_mark(kStageGather, false, stream);
-    gather_kernel<<<grid, kThreads, 0, st>>>(P, n_parts, n_items);
+    gather_kernel<<<grid, kThreads, 0, st>>>(P);
     profile_mark(kStageGather, true, stream);
   }
   return (int)hipGetLastError();

@@ -16,7 +16,7 @@ constexpr int kMaxLayersPerLaunch = 32;
 constexpr int kSlice = 128;        // keys per scoring work item (4 waves x one tile of 32)
 constexpr int kMaxRowTiles = 8;    // G * ceil(w / 32) supported by the scoring kernel
 constexpr int kMaxPoolHalf = 64;   // pool_kernel / 2 supported
-constexpr int kGatherRows = 128;   // retained rows per gather work item
+constexpr int kGatherRows = 64;    // retained rows per gather work item
 constexpr int kCounterStride = 32; // words between per-job counters (one 128-byte line each)
 
 // Per-layer work description of one prefill launch group.
@@ -65,6 +65,7 @@ struct PrefillLaunch {
   float* edge;            // [J][n_slices][G][4 * pool_half]  per-query-head column sums at slice edges
   int32_t slot_layer[kMaxLayersPerLaunch];     // scored slot -> layer index in this group
   int32_t gather_layer[kMaxLayersPerLaunch];   // layers with retained rows
+  int32_t gather_item0[kMaxLayersPerLaunch + 1];  // first gather work item of each gather layer (prefix)
 };
 
 static_assert(sizeof(PrefillLaunch) <= 4000, "kernel argument block too large");
