@@ -322,28 +322,45 @@ __device__ __forceinline__ void store_scores(const PrefillLaunch& P, bool snap, 
   }
 }
 
-// The last slice of a job to count itself in folds every slice's (max, sum) into one
-// log2-normaliser per row (max + log2(sum), +inf for rows without visible keys).  The
-// normalisers start as NaN ("not written") and are read back through coherent loads.
+// Fold used by the two-pass kernel: the job's per-slice log2 normalisers (one per row) are read
+// straight into registers, 16 slices per thread and batch (thread = row pair, slice group), as
+// device-coherent loads, then combined per row (max first, then the sum of exp2 against it) and
+// across the slice groups in LDS.
 template <int R>
-__device__ void fold_job(const PrefillLaunch& P, int job, float2 (*sPart)[R]) {
-  constexpr int kGroups = kThreads / R;
-  static_assert(kGroups >= 1 && kGroups <= kWaves, "rows per workgroup");
+__device__ void fold_job_regs(const PrefillLaunch& P, int job, float2 (*sPart)[R]) {
+  constexpr int kPairs = R / 2;
+  constexpr int kGroups = kThreads / kPairs;   // slice groups
+  constexpr int kBatch = 16;
+  static_assert(kGroups >= 1 && kGroups <= kWaves, "partials fit the statistics buffer");
   const int tid = threadIdx.x, nsl = P.n_slices;
-  const int r = tid % R, j = tid / R;
-  float M = -__builtin_inff(), Z = 0.f;
-  const float* st = P.stats + (size_t)job * nsl * R * 2 + 2 * r;
-  for (int c0 = j; c0 < nsl; c0 += kGroups * 16) {
-    float2 v[16];
+  const int pr = tid % kPairs, j = tid / kPairs;
+  const float NEG_INF = -__builtin_inff();
+  const float* st = P.stats + (size_t)job * nsl * R + 2 * pr;
+  float M0 = NEG_INF, Z0 = 0.f, M1 = NEG_INF, Z1 = 0.f;
+  for (int c0 = j; c0 < nsl; c0 += kGroups * kBatch) {
+    float2 v[kBatch];
 #pragma unroll
-    for (int u = 0; u < 16; ++u) {
-      const int cc = c0 + u * kGroups;
-      v[u] = cc < nsl ? load_coherent2(st + (size_t)cc * R * 2) : make_float2(-__builtin_inff(), 0.f);
+    for (int u = 0; u < kBatch; ++u) {
+      const int c = c0 + u * kGroups;
+      v[u] = c < nsl ? load_coherent2(st + (size_t)c * R) : make_float2(NEG_INF, NEG_INF);
     }
+    float m0 = NEG_INF, m1 = NEG_INF;
 #pragma unroll
-    for (int u = 0; u < 16; ++u) combine_ms(M, Z, v[u].x, v[u].y);
+    for (int u = 0; u < kBatch; ++u) {
+      m0 = fmaxf(m0, v[u].x);
+      m1 = fmaxf(m1, v[u].y);
+    }
+    float z0 = 0.f, z1 = 0.f;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      z0 += m0 > NEG_INF ? __builtin_amdgcn_exp2f(v[u].x - m0) : 0.f;
+      z1 += m1 > NEG_INF ? __builtin_amdgcn_exp2f(v[u].y - m1) : 0.f;
+    }
+    combine_ms(M0, Z0, m0, z0);
+    combine_ms(M1, Z1, m1, z1);
   }
-  sPart[j][r] = make_float2(M, Z);
+  sPart[j][2 * pr] = make_float2(M0, Z0);
+  sPart[j][2 * pr + 1] = make_float2(M1, Z1);
   __syncthreads();
   if (tid < R) {
     float m = sPart[0][tid].x, z = sPart[0][tid].y;
@@ -687,6 +704,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
   k_tile(kA, j0);
   uint32_t arrived = 0;   // thread 0: arrival count returned for the previous pass A item
   JobRef ja = j0, jb = j0, jp = j0;   // pass A item t, pass B item t - lag, pass A item t - 1
+  float lam_pre = 0.f;   // thread tid < R: normaliser of the next pass B item, loaded an iteration early
 
 #pragma unroll 1
   for (int t = 0; t < T + lag; ++t) {
@@ -697,6 +715,13 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
     if (had_prev && tid == 0)
       arrived = __hip_atomic_fetch_add(P.counters + (size_t)kCounterStride * (1 + jp.job), 1u, __ATOMIC_RELAXED,
                                         __HIP_MEMORY_SCOPE_AGENT);
+    // this iteration's pass B normaliser (loaded last iteration) and the next one's, issued now so
+    // that nothing queues in front of it
+    const float lam_cur = lam_pre;
+    if (t + 1 >= lag && t + 1 - lag < T && tid < R) {
+      const JobRef jq = t + 1 == lag ? j0 : step(jb);
+      lam_pre = load_coherent(P.lam + (size_t)jq.job * R + tid);
+    }
 
     // ============================================================ pass B: window column sums
     const JobRef jbn = step(jb), jan = step(ja);   // the items after this iteration's
@@ -705,9 +730,9 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
       const bool snap = ly.rule == RKV_SNAPKV;
       const int cbase = jb.slice * kSlice, key = cbase + wv * 32 + ln;
       if (tid < R) {
-        float lam = load_coherent(P.lam + (size_t)jb.job * R + tid);
+        float lam = lam_cur;
         uint32_t it = 0;
-        while (lam != lam) {   // not folded yet (bounded wait)
+        while (lam != lam) {   // not folded when prefetched (bounded wait)
           __builtin_amdgcn_s_sleep(2);
           lam = load_coherent(P.lam + (size_t)jb.job * R + tid);
           if (++it > kSpinLimit) {
@@ -740,14 +765,17 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
                                                         0, 0, 0);
         if (rt == NRT - 1 && t + 1 - lag < T) k_tile(kB, jbn);   // next pass B tile (L2 / MALL)
         float sum = 0.f;
+        if (__builtin_expect(edge_tile, 0)) {
+          // rows see keys up to L - w + ii; register r holds row ii = (rt % NTH) 32 + 4 hf + 8 (r / 4) + r % 4
+          const int lim = L - w + (rt % NTH) * 32 + 4 * hf - key;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float pr = __builtin_amdgcn_exp2f(acc[r] * sl2);
-          if (edge_tile) {
-            const int ii = (rt % NTH) * 32 + 8 * (r >> 2) + 4 * hf + (r & 3);
-            if (key >= L || key > L - w + ii) pr = 0.f;
+          for (int r = 0; r < 16; ++r) {
+            const float pr = __builtin_amdgcn_exp2f(acc[r] * sl2);
+            sum += (key < L && 8 * (r >> 2) + (r & 3) >= -lim) ? pr : 0.f;
           }
-          sum += pr;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(acc[r] * sl2);
         }
         col[rt / NTH] += sum;
       }
@@ -789,14 +817,13 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
                                                         0, 0, 0);
         if (rt == NRT - 1 && t + 1 < T) k_tile(kA, jan);   // next pass A tile from HBM
         // lane = window row ln of row tile rt, registers = keys tile_key0 + 8(r/4) + 4hf + r%4
-        if (mask_a) {
+        if (__builtin_expect(mask_a, 0)) {
           const int g = rt / NTH, ii = (rt - g * NTH) * 32 + ln;
           const int last = (g < G && ii < w) ? min(L - 1, L - w + ii) : -1;
+          const int lim = last - tile_key0 - 4 * hf;   // register r holds key tile_key0 + 4 hf + 8 (r / 4) + r % 4
 #pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int kk = tile_key0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-            if (kk > last) acc[r] = NEG_INF;
-          }
+          for (int r = 0; r < 16; ++r)
+            if (8 * (r >> 2) + (r & 3) > lim) acc[r] = NEG_INF;
         }
         // both half-waves hold the same rows, other keys
         float m = fmaxf(acc[0], acc[1]);
@@ -818,7 +845,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
         float M = NEG_INF, Z = 0.f;
 #pragma unroll
         for (int v = 0; v < kWaves; ++v) combine_ms(M, Z, sStat[v][tid].x, sStat[v][tid].y);
-        store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R * 2 + 2 * tid, M, Z);
+        store_coherent(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + tid, Z > 0.f ? M + __log2f(Z) : NEG_INF);
       }
     }
 
@@ -827,7 +854,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
       __syncthreads();   // sStat is read above
       if (tid == 0) sFold = (arrived == (uint32_t)(nsl - 1)) ? jp.job : -1;
       __syncthreads();
-      if (sFold >= 0) fold_job<R>(P, sFold, sStat);
+      if (sFold >= 0) fold_job_regs<R>(P, sFold, sStat);
     }
     if (doA) {
       jp = ja;
