@@ -27,8 +27,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0
 L_CTX, N_LAYERS, HQ, HKV, D, W, POOL, AVG_BUDGET, B_MIN = 8192, 32, 32, 8, 128, 32, 7, 512, 48
 WORKLOAD_ID = 2
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_fused_kernel_route8k_traffic.json")
-SCORE_KERNEL = "score_fused_kernel<4, 1>"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_pipe_kernel_route8k_traffic.json")
+SCORE_KERNEL = "score_pipe_kernel<1>"
 COPY_CAL_BYTES = 1 << 30     # plain device copy used to scale the PMC byte counters
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_15157_amd", "csrc", "prefill.hip")
 

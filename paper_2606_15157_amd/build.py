@@ -18,6 +18,10 @@ HIPCC_FLAGS = [
     "-Wall", "-Wno-unused-function",
     # keep the compiler from emitting packed fp32 arithmetic
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep single-lane atomics as written: the atomic optimizer turns them into a wave-wide
+    # form whose result is read back at once, which would wait for the atomic's round trip
+    # where the code only needs the result an iteration later
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
 ]
 
 

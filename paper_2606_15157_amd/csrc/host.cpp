@@ -86,7 +86,7 @@ struct Group {
 // too long for the single-pass one) so that it can be checked on short prompts too.
 int force_two_pass() {
   const char* e = std::getenv("RKV_FORCE_TWO_PASS");
-  return (e && std::atoi(e) != 0) ? 1 : 0;
+  return e ? std::max(0, std::atoi(e)) : 0;
 }
 
 // Two-pass scoring: pass B trails pass A by this many items in each workgroup (RKV_SCORE_LAG
@@ -161,6 +161,8 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
   w.stats = off;
   off = round_up(off + sizeof(float) * 2 * (size_t)n_jobs * n_slices * rows, 256);
   w.lam = off;
+  off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
+  w.ncl = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
   w.S = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * seq_len, 256);
@@ -443,6 +445,7 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     P.counters = (uint32_t*)(base + W.counters);
     P.stats = (float*)(base + W.stats);
     P.lam = (float*)(base + W.lam);
+    P.ncl = (float*)(base + W.ncl);
     P.S = (float*)(base + W.S);
     P.Su = (float*)(base + W.Su);
     P.edge = (float*)(base + W.edge);

@@ -234,6 +234,23 @@ __device__ __forceinline__ void load_k_tile(u32x4 (&kf)[8], const uint16_t* khea
   for (int st = 0; st < 8; ++st) kf[st] = kp[st];
 }
 
+// The item's 128-key K tile in LDS, laid out like the query block (key r's 16-byte chunk c at
+// position 16 r + (c ^ (r & 15))); keys past the prompt repeat its last key (masked later).
+__device__ __forceinline__ void issue_k_to_lds(uint16_t* sK, const uint16_t* khead, int key0, int L) {
+  constexpr int kPerWave = kSlice * 16 / kThreads;   // instructions per wave, 4 keys each
+  const int lane = threadIdx.x & 63, wv = wave_id();
+  const int lr = lane >> 4;
+  const int c = (lane & 15) ^ (((4 * wv) & 15) | lr);
+#pragma unroll
+  for (int i = 0; i < kPerWave; ++i) {
+    const int r0 = 4 * (i * kWaves + wv);
+    const int key = min(key0 + r0 + lr, L - 1);
+    __builtin_amdgcn_global_load_lds(
+        (const __attribute__((address_space(1))) void*)(khead + (size_t)key * kHeadDim + c * 8),
+        (__attribute__((address_space(3))) void*)(sK + r0 * kHeadDim), 16, 0, 0);
+  }
+}
+
 struct JobRef {
   int job, slice, slot, s, h;
 };
@@ -421,6 +438,100 @@ __device__ void fold_job_fused(const PrefillLaunch& P, int job, uint16_t* sBuf, 
   }
 }
 
+// s_waitcnt vmcnt(N) (expcnt and lgkmcnt not waited for).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4) | (15 << 8));
+}
+
+// 16 bytes per lane from global memory into LDS at lds_base + 16 lane (LDS DMA).  Issued as
+// inline assembly so that the compiler does not conservatively wait for it before unrelated
+// LDS reads; the issuing wave waits for it explicitly (vmcnt) before a barrier hands the data
+// on.  lds_base must be wave-uniform.
+__device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base)
+               : "memory", "m0");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
+}
+
+// Work item of the pipelined kernel: the item index it = first + t n_wg names job it / nsl and
+// position s0 = it % nsl, and the item processes slice (s0 + job) % nsl.  The rotation moves a
+// job's last slice (the one holding the observation window, slower because of its masks) to a
+// different workgroup for every job, so no workgroup is every job's straggler.
+struct PipeRef {
+  int job, slice, s0, jm, slot, s, h;   // jm = job % nsl
+};
+__device__ __forceinline__ PipeRef pipe_item(int64_t it, int nsl, int B, int Hkv) {
+  PipeRef r;
+  r.job = (int)(it / nsl);
+  r.s0 = (int)(it - (int64_t)r.job * nsl);
+  r.jm = r.job % nsl;
+  r.slice = r.s0 + r.jm >= nsl ? r.s0 + r.jm - nsl : r.s0 + r.jm;
+  r.h = r.job % Hkv;
+  r.s = (r.job / Hkv) % B;
+  r.slot = r.job / (Hkv * B);
+  return r;
+}
+// Moves an item forward by n_wg items (dj jobs and ds positions) without divisions.
+__device__ __forceinline__ void pipe_advance(PipeRef& r, int dj, int ds, int nsl, int B, int Hkv) {
+  r.s0 += ds;
+  int j = dj;
+  if (r.s0 >= nsl) {
+    r.s0 -= nsl;
+    ++j;
+  }
+  r.job += j;
+  r.jm += j;
+  while (r.jm >= nsl) r.jm -= nsl;
+  r.slice = r.s0 + r.jm >= nsl ? r.s0 + r.jm - nsl : r.s0 + r.jm;
+  r.h += j;
+  while (r.h >= Hkv) {
+    r.h -= Hkv;
+    if (++r.s == B) {
+      r.s = 0;
+      ++r.slot;
+    }
+  }
+}
+
+// Workgroup barrier for data handed over through LDS only: this wave's LDS operations retire
+// (lgkmcnt 0), then s_barrier.  Unlike __syncthreads it does not wait for the wave's vector
+// memory operations (the workgroup-scope release fence does), so prefetches, stores and polls
+// stay in flight across it.  LDS written by LDS DMA is covered by the issuing wave's own vmcnt
+// wait before it reaches the barrier.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // vmcnt 63 (no wait), expcnt 7 (no wait), lgkmcnt 0
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// issue_q_to_lds through dma16: the compiler then inserts no waits for it before unrelated LDS
+// reads; the consumer waits for vmcnt explicitly before its barrier.
+template <int NRT, int NTH>
+__device__ __forceinline__ void issue_q_to_lds_asm(uint16_t* sQ, const uint16_t* qjob, int G, int w) {
+  constexpr int R = NRT * 32;
+  constexpr int kPerWave = R * 16 / kThreads;
+  constexpr int kHeadRows = NTH * 32;
+  const int lane = threadIdx.x & 63, wv = wave_id();
+  const int lr = lane >> 4;
+  const int c = (lane & 15) ^ (((4 * wv) & 15) | lr);
+  const uint32_t lane_off = (uint32_t)(lr * kHeadDim + c * 8) * 2u;
+  const uint32_t pad_off = (uint32_t)(c * 8) * 2u;
+#pragma unroll
+  for (int i = 0; i < kPerWave; ++i) {
+    const int r0 = 4 * (i * kWaves + wv);
+    const int g = r0 / kHeadRows, ii0 = r0 - g * kHeadRows;
+    const bool ok = g < G && ii0 + lr < w;
+    const uint32_t off = ok ? (uint32_t)((g * w + ii0) * kHeadDim) * 2u + lane_off : pad_off;
+    dma16(reinterpret_cast<const char*>(qjob) + off, lds_addr(sQ + r0 * kHeadDim));
+  }
+}
+
 // ---------------------------------------------------------------------------------------------
 // Single-pass scoring (prompts whose slices of one job fit in the resident workgroups at once).
 // Workgroup w takes items w, w + n_wg, ...; per item the four waves each multiply one 32-key
@@ -464,18 +575,18 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
   u32x4 kf[8];
 
   // the item's query block (LDS DMA) and this wave's K tile (registers)
-  auto issue_loads = [&](const JobRef& j) {
+  auto issue_loads = [&](const PipeRef& j) {
     const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
-    issue_q_to_lds<NRT, NTH>(sQ, ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim, G, w);
+    issue_q_to_lds_asm<NRT, NTH>(sQ, ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim, G, w);
     load_k_tile(kf, ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim, j.slice * kSlice + wv * 32 + ln, L, hf);
   };
 
   // ---- phase A: logits and exponentials; lane = window row ln of row tile rt, registers = keys
   // tile_key0 + 8(r/4) + 4hf + r%4; the tile row maxima (log2 units, 0 for rows with no visible
   // key) go to mw, the per-wave (max, sum) pairs to sStat
-  auto phase_a = [&](const JobRef& j, f32x16 (&e)[NRT], float (&mw)[NRT]) {
+  auto phase_a = [&](const PipeRef& j, f32x16 (&e)[NRT], float (&mw)[NRT]) {
     __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // the item's query block and K tile
-    __syncthreads();
+    lds_barrier();
     const int tile_key0 = j.slice * kSlice + wv * 32;
     const bool mask_a = padded_rows || tile_key0 + 32 > L - w;
 #pragma unroll
@@ -511,13 +622,13 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
       z = __uint_as_float(sz[0]) + __uint_as_float(sz[1]);
       if (hf == 0) sStat[wv][rt * 32 + ln] = make_float2(mw[rt], z);
     }
-    __syncthreads();
+    lds_barrier();
   };
 
   // ---- publish the slice's statistics and count it in (the stores retire first).  Returns
   // whether this slice came first: that workgroup folds the job once it has to wait for it anyway
   // (the first slice has the most slack, so folding never lands on the job's straggler).
-  auto publish = [&](const JobRef& j) -> bool {
+  auto publish = [&](const PipeRef& j) -> bool {
     if (tid < R) {
       float M = NEG_INF, Z = 0.f;
 #pragma unroll
@@ -525,17 +636,17 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
       store_coherent(P.stats + ((size_t)j.job * nsl + j.slice) * R + tid, Z > 0.f ? M + __log2f(Z) : NEG_INF);
     }
     vmem_release();
-    __syncthreads();
+    lds_barrier();
     uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + j.job);
     if (tid == 0) sFlag = (int)__hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();
+    lds_barrier();
     return sFlag == 0;
   };
 
   // ---- the folder: wait (bounded, one lane) until every slice has counted itself in, then fold
   // (the normalisers go to memory over their NaN marks and to sLam); the query block's LDS space
   // stages the statistics (the next block loads after the wait)
-  auto fold = [&](const JobRef& j) {
+  auto fold = [&](const PipeRef& j) {
     if (tid == 0) {
       uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + j.job);
       uint32_t it = 0;
@@ -547,14 +658,14 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
         }
       }
     }
-    __syncthreads();
+    lds_barrier();
     vmem_acquire();
     fold_job_fused<R>(P, j.job, sQ, sStat, sLam);
   };
 
   // ---- wait (bounded) for the job's normalisers: wave 0 reads all of them at once until none is
   // still marked "not written"
-  auto wait_lam = [&](const JobRef& j) {
+  auto wait_lam = [&](const PipeRef& j) {
     const float* lj = P.lam + (size_t)j.job * R;
     uint32_t it = 0;
     while (true) {
@@ -583,7 +694,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
   };
 
   // ---- phase B: probabilities and their sums over the window rows (across lanes), then scores
-  auto phase_b = [&](const JobRef& j, f32x16 (&e)[NRT], const float (&mw)[NRT]) {
+  auto phase_b = [&](const PipeRef& j, f32x16 (&e)[NRT], const float (&mw)[NRT]) {
     const bool snap = P.layer[P.slot_layer[j.slot]].rule == RKV_SNAPKV;
     float alpha[NRT];
 #pragma unroll
@@ -623,25 +734,531 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
         sCol[0][wv * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)] = ev[0][0];
       }
     }
-    __syncthreads();
+    lds_barrier();
     store_scores<NG>(P, snap, j.job, j.slice, j.slice * kSlice, sCol, inv_g);
   };
 
   f32x16 e[NRT];
   float mw[NRT];
-  JobRef jc = decode_item(first, nsl, B, Hkv);
+  PipeRef jc = pipe_item(first, nsl, B, Hkv);
   issue_loads(jc);
 #pragma unroll 1
   for (int t = 0; t < T; ++t) {
     phase_a(jc, e, mw);
     if (publish(jc)) fold(jc);
     else if (wv == 0) wait_lam(jc);
-    __syncthreads();
-    JobRef jn = jc;
-    advance(jn, dj, ds, nsl, B, Hkv);
+    lds_barrier();
+    PipeRef jn = jc;
+    pipe_advance(jn, dj, ds, nsl, B, Hkv);
     if (t + 1 < T) issue_loads(jn);   // sQ is free; the loads land during phase B
     phase_b(jc, e, mw);
     jc = jn;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Pipelined scoring against a per-row reference (four row tiles, one eight-wave workgroup per
+// CU, four items in flight).
+//
+// Reference.  The softmax of a window row is shift-invariant, so the exponentials may be taken
+// against any per-row constant c_i that keeps them in range.  c_i is the larger of the row's
+// logit with its own key (position L - w + i, always visible) and with the first key; both are
+// true logits of the row, so e_ij = exp2((z_ij - c_i) log2(e) / sqrt(d)) <= 2^127 unless some
+// key beats the reference by more than 88 (natural log units), and the row sum Z_i >= 1 (the
+// reference key contributes 1).  Then p_ij = e_ij / Z_i: a slice publishes plain row sums, the
+// normaliser is their sum, and no running maximum is needed.  A non-finite Z_i is reported in
+// the status word (bit 1).
+//
+// Layout.  16x16x32 bf16 MFMA with the queries as the A operand: in every 16 x 16 tile lane l
+// holds key l % 16 and rows 4 (l / 16) + 0..3.  Wave wv takes keys 32 (wv % 4) + [0, 32) of the
+// item's 128-key slice (two key sub-tiles) and rows 64 (wv / 4) + [0, 64) (four row sub-tiles):
+// 8 tiles, 32 exponentials per lane.  Sums over window rows are then register-local plus two
+// permlane swaps; sums over keys (row statistics) take four DPP steps inside each row of 16
+// lanes.
+//
+// Schedule of iteration t (item t enters phase A, item t - 3 phase B, each in its own register
+// set; no wait is for an operation issued in the same iteration):
+//   B1    waves 4-7 wait for their LDS DMA of item t (query block, K tile, references)
+//   A     logits, exponentials, per-row partial sums per key tile into sStat
+//   MID   wave 0: last iteration's memory operations have retired -> did item t - 1's arrival
+//         complete its job?  The polled reciprocal row sums of item t - 3 (re-polled while any
+//         is still NaN) go to sAlpha
+//   B1.5
+//   B     item t - 3: probabilities, sums over the window rows per query head (or group) into sColP
+//   B2    the workgroup folds item t - 1's job if it completed it
+//   wave 0: store item t's row sums and count it in (no wait in between: the fold re-reads sums
+//         still marked NaN); poll the reciprocal row sums of item t - 2
+//   waves 0-3: scores of item t - 3;  waves 4-7: LDS DMA of item t + 2
+// Progress: every wait of iteration t is for events that other workgroups produce in
+// iterations <= t - 1 (a job's slices sit in at most two consecutive iterations because a job
+// has no more slices than there are workgroups), so with every workgroup resident nothing waits
+// on a later wait.
+// ---------------------------------------------------------------------------------------------
+constexpr int kPipeWaves = 8;
+constexpr int kPipeThreads = kPipeWaves * 64;
+constexpr int kPipeDepth = 4;
+
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+
+
+// Minus the reference logit of every row of every scored job, and the per-pass resets: the
+// status word, the job's arrival counter, its reciprocal row sums ("not folded": NaN) and its
+// slices' row sums ("not stored": NaN).
+// One workgroup per job; thread = (row, half of the head dimension).
+template <int NTH>
+__global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
+  constexpr int R = 128;
+  const int tid = threadIdx.x, job = blockIdx.x;
+  const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, Hq = P.n_q_heads;
+  const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
+  const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
+  if (job == 0 && tid == 0) P.counters[0] = 0u;
+  if (tid == 0) P.counters[(size_t)kCounterStride * (1 + job)] = 0u;
+  if (tid < R) reinterpret_cast<uint32_t*>(P.lam)[(size_t)job * R + tid] = 0xffffffffu;
+  {
+    // every slice's row sums "not stored yet" (NaN): the fold checks them instead of relying on
+    // a store-before-count ordering
+    u32x4* st = reinterpret_cast<u32x4*>(P.stats + (size_t)job * P.n_slices * R);
+    const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
+    for (int i = tid; i < P.n_slices * R / 4; i += 256) st[i] = nan4;
+  }
+  const int r = tid >> 1, hv = tid & 1;
+  const int g = r / (NTH * 32), ii = r - g * (NTH * 32);
+  const bool valid = g < G && ii < w;
+  float zd = 0.f, zs = 0.f;
+  if (valid) {
+    const uint16_t* q = ly.q + ((size_t)(s * Hq + h * G + g) * w + ii) * kHeadDim + hv * 64;
+    const uint16_t* kh = ly.k + (size_t)(s * Hkv + h) * L * kHeadDim + hv * 64;
+    const uint16_t* kd = kh + (size_t)(L - w + ii) * kHeadDim;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const u32x4 qa = *reinterpret_cast<const u32x4*>(q + 8 * c);
+      const u32x4 da = *reinterpret_cast<const u32x4*>(kd + 8 * c);
+      const u32x4 sa = *reinterpret_cast<const u32x4*>(kh + 8 * c);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float q0 = __uint_as_float(qa[u] << 16), q1 = __uint_as_float(qa[u] & 0xffff0000u);
+        zd = fmaf(q0, __uint_as_float(da[u] << 16), zd);
+        zd = fmaf(q1, __uint_as_float(da[u] & 0xffff0000u), zd);
+        zs = fmaf(q0, __uint_as_float(sa[u] << 16), zs);
+        zs = fmaf(q1, __uint_as_float(sa[u] & 0xffff0000u), zs);
+      }
+    }
+  }
+  zd += __shfl_xor(zd, 1);
+  zs += __shfl_xor(zs, 1);
+  if (hv == 0) P.ncl[(size_t)job * R + r] = valid ? -fmaxf(zd, zs) : 0.f;
+}
+
+// Reduce-scatter of 16 values over the 16 lanes of each row: afterwards lane l holds the sum of
+// value 8 b0 + 4 b1 + 2 b2 + b3 (b_k = bit k of l) over its row.
+__device__ __forceinline__ void reduce_scatter16(float (&v)[16], int lane) {
+  dpp_halve<0x128, 16, 16>(v, (lane >> 3) & 1);   // row_ror:8        -> lane l ^ 8
+  dpp_halve<0x141, 8, 16>(v, (lane >> 2) & 1);    // row_half_mirror  -> 7 - l within 8
+  dpp_halve<0x4E, 4, 16>(v, (lane >> 1) & 1);     // quad_perm [2,3,0,1] -> l ^ 2
+  dpp_halve<0xB1, 2, 16>(v, lane & 1);            // quad_perm [1,0,3,2] -> l ^ 1
+}
+__device__ __forceinline__ int rs16_sel(int lane) {
+  return ((lane & 1) << 3) | (((lane >> 1) & 1) << 2) | (((lane >> 2) & 1) << 1) | ((lane >> 3) & 1);
+}
+__device__ __forceinline__ bf16x8 frag16(const uint16_t* base, int row, int chunk) {
+  return *reinterpret_cast<const bf16x8*>(base + (row * 16 + (chunk ^ (row & 15))) * 8);
+}
+
+template <int NTH>
+__global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const PrefillLaunch P, int n_wg) {
+  constexpr int R = 128;
+  constexpr int NG = 4 / NTH;
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[2][R * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kSlice * kHeadDim];
+  __shared__ __attribute__((aligned(16))) float sNcl[2][R];
+  __shared__ __attribute__((aligned(16))) float sAlpha[R];
+  __shared__ float sStat[4][R];
+  __shared__ float sColP[2][2][kSlice];
+  __shared__ float sFoldP[4][R];
+  __shared__ int sFold;
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), lg = lane >> 4, l16 = lane & 15;
+  const int kt = wv & 3, rh = wv >> 2;
+  const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
+  const int nsl = P.n_slices;
+  const int n_jobs = B * P.n_scored * Hkv;
+  const int64_t n_items = (int64_t)n_jobs * nsl;
+  const float sl2 = P.scale_log2;
+  const float inv_g = 1.f / (float)G;
+  uint32_t* status = P.counters;
+  const bool padded_rows = (G * NTH < 4) || (w != NTH * 32);
+
+  const int64_t first = blockIdx.x;
+  if (first >= n_items) return;
+  const int T = (int)((n_items - 1 - first) / n_wg + 1);
+  const int dj = n_wg / nsl, ds = n_wg - dj * nsl;   // item stride n_wg in (jobs, slices)
+  bool gave_up = false;   // a wait of this wave timed out (status set): no further waits
+
+  // ---- waves 4-7: the item's query block, K tile and reference logits into buffer b.
+  // Instruction u (0..15) of wave 4 + dw moves 1 KiB: rows (u < 8) or keys (u >= 8)
+  // 16 (u % 8) + 4 dw + [0, 4); lane l fills row / key 16 (u % 8) + lrow, chunk position l % 16,
+  // with lrow = 4 dw + l / 16 and source chunk (l % 16) ^ lrow (the swizzle of issue_q_to_lds).
+  // The lane's byte offset is the same for every instruction; wave 4 also moves the references.
+  const int lrow = 4 * (wv & 3) + (lane >> 4);
+  const uint32_t lane_off = (uint32_t)lrow * 256u + (uint32_t)((lane & 15) ^ lrow) * 16u;
+  auto issue_dma = [&](const PipeRef& j, int b) {
+    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
+    const char* qjob = reinterpret_cast<const char*>(ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim);
+    const char* khead = reinterpret_cast<const char*>(ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim);
+    const int key0 = j.slice * kSlice;
+    const uint32_t q_lds = lds_addr(&sQ[b][4 * (wv & 3) * kHeadDim]);
+    const uint32_t k_lds = lds_addr(&sK[b][4 * (wv & 3) * kHeadDim]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int g = u / (2 * NTH), ii0 = 16 * (u % (2 * NTH));
+      uint32_t off = (uint32_t)(g * w + ii0) * 256u + lane_off;
+      if (__builtin_expect(padded_rows, 0)) {
+        const bool ok = g < G && ii0 + lrow < w;
+        off = ok ? off : (uint32_t)((lane & 15) ^ lrow) * 16u;   // padding rows repeat row 0
+      }
+      dma16(qjob + off, q_lds + 16u * kHeadDim * 2u * u);
+    }
+    const bool tail = key0 + kSlice > L;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      size_t off = (size_t)(key0 + 16 * u) * 256u + lane_off;
+      if (__builtin_expect(tail, 0)) {
+        const int key = min(key0 + 16 * u + lrow, L - 1);
+        off = (size_t)key * 256u + (uint32_t)((lane & 15) ^ lrow) * 16u;
+      }
+      dma16(khead + off, k_lds + 16u * kHeadDim * 2u * u);
+    }
+    if (wv == 4) {
+      // the job's 128 reference logits: lanes 0-31 move 16 bytes each (the DMA writes only the
+      // active lanes' 16-byte pieces)
+      const uint32_t n_lds = lds_addr(&sNcl[b][0]);
+      if (lane < 32) dma16(P.ncl + (size_t)j.job * R + 4 * lane, n_lds);
+    }
+  };
+  auto wait_dma = [&](bool next_issued) {
+    // the DMA of the next item (16 instructions, 17 for wave 4) may stay in flight
+    if (next_issued) {
+      if (wv == 4) wait_vmcnt<17>();
+      else wait_vmcnt<16>();
+    } else {
+      wait_vmcnt<0>();
+    }
+  };
+
+  // ---- phase A: e = exp2((z - c) log2(e)/sqrt(d)) for tile (rs, ks): row rh*64 + 16 rs + 4 lg + i,
+  // key key0 + 32 kt + 16 ks + l16; per-row partial sums over this wave's 32 keys into sStat[kt]
+  auto phase_a = [&](const PipeRef& j, int b, f32x4v (&e)[4][2]) {
+    const uint16_t* q = sQ[b];
+    const uint16_t* k = sK[b];
+#pragma unroll
+    for (int rs = 0; rs < 4; ++rs) {
+      const f32x4v c4 = *reinterpret_cast<const f32x4v*>(&sNcl[b][rh * 64 + rs * 16 + 4 * lg]);
+      e[rs][0] = c4;
+      e[rs][1] = c4;
+    }
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      const bf16x8 k0 = frag16(k, kt * 32 + l16, 4 * st + lg);
+      const bf16x8 k1 = frag16(k, kt * 32 + 16 + l16, 4 * st + lg);
+#pragma unroll
+      for (int rs = 0; rs < 4; ++rs) {
+        const bf16x8 qa = frag16(q, rh * 64 + rs * 16 + l16, 4 * st + lg);
+        e[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, k0, e[rs][0], 0, 0, 0);
+        e[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, k1, e[rs][1], 0, 0, 0);
+      }
+      // one k-step's fragments live at a time (the other wave of the SIMD covers the LDS latency)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const int key_w0 = j.slice * kSlice + kt * 32;
+    if (__builtin_expect(padded_rows || key_w0 + 31 > L - w, 0)) {
+      // rare tiles (reaching into the window or past the prompt, or padding rows): logits of
+      // keys a row does not see become -inf.  Lane quantities come from an opaque copy of the
+      // thread index so that the compiler keeps none of this live across the loop.
+      int tv = tid;
+      asm volatile("" : "+v"(tv));
+      const int lgv = (tv & 63) >> 4, kv = key_w0 + (tv & 15);
+#pragma unroll
+      for (int rs = 0; rs < 4; ++rs)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = rh * 64 + rs * 16 + 4 * lgv + i;
+          const int g = row / (NTH * 32), ii = row - g * (NTH * 32);
+          const int last = (g < G && ii < w) ? min(L - 1, L - w + ii) : -1;
+          if (kv > last) e[rs][0][i] = -__builtin_inff();
+          if (kv + 16 > last) e[rs][1][i] = -__builtin_inff();
+        }
+    }
+    float v[16];
+#pragma unroll
+    for (int rs = 0; rs < 4; ++rs)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float x0 = __builtin_amdgcn_exp2f(e[rs][0][i] * sl2);
+        const float x1 = __builtin_amdgcn_exp2f(e[rs][1][i] * sl2);
+        e[rs][0][i] = x0;
+        e[rs][1][i] = x1;
+        v[4 * rs + i] = x0 + x1;
+      }
+    reduce_scatter16(v, lane);
+    const int sel = rs16_sel(l16);
+    sStat[kt][rh * 64 + (sel >> 2) * 16 + 4 * lg + (sel & 3)] = v[0];
+  };
+
+  // ---- phase B: p = e / Z; sums over the window rows into sColP[rh][slot][key]: slot = query
+  // head within the row half (SnapKV, one row tile per head), else 0 (one head per row half, or
+  // the partial group / head sum of this row half)
+  auto phase_b = [&](const PipeRef& j, f32x4v (&e)[4][2]) {
+    const bool snap = P.layer[P.slot_layer[j.slot]].rule == RKV_SNAPKV;
+    f32x4v a4[4];
+#pragma unroll
+    for (int rs = 0; rs < 4; ++rs) a4[rs] = *reinterpret_cast<const f32x4v*>(&sAlpha[rh * 64 + rs * 16 + 4 * lg]);
+    if (snap && NTH == 1) {
+      float c[4] = {0.f, 0.f, 0.f, 0.f};   // (slot, ks) = (0,0) (0,1) (1,0) (1,1)
+#pragma unroll
+      for (int rs = 0; rs < 4; ++rs)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          c[2 * (rs >> 1)] = fmaf(a4[rs][i], e[rs][0][i], c[2 * (rs >> 1)]);
+          c[2 * (rs >> 1) + 1] = fmaf(a4[rs][i], e[rs][1][i], c[2 * (rs >> 1) + 1]);
+        }
+      const auto p0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(c[0]), __float_as_uint(c[1]), false, false);
+      const auto p1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(c[2]), __float_as_uint(c[3]), false, false);
+      const float w0 = __uint_as_float(p0[0]) + __uint_as_float(p0[1]);
+      const float w1 = __uint_as_float(p1[0]) + __uint_as_float(p1[1]);
+      const auto p2 = __builtin_amdgcn_permlane16_swap(__float_as_uint(w0), __float_as_uint(w1), false, false);
+      const float x = __uint_as_float(p2[0]) + __uint_as_float(p2[1]);
+      // lane group lg holds (slot, ks) = (lg & 1, lg >> 1)
+      sColP[rh][lg & 1][kt * 32 + (lg >> 1) * 16 + l16] = x;
+    } else {
+      float c[2] = {0.f, 0.f};
+#pragma unroll
+      for (int rs = 0; rs < 4; ++rs)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          c[0] = fmaf(a4[rs][i], e[rs][0][i], c[0]);
+          c[1] = fmaf(a4[rs][i], e[rs][1][i], c[1]);
+        }
+      const auto p0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(c[0]), __float_as_uint(c[1]), false, false);
+      const float w0 = __uint_as_float(p0[0]) + __uint_as_float(p0[1]);
+      const auto p1 = __builtin_amdgcn_permlane16_swap(__float_as_uint(w0), __float_as_uint(w0), false, false);
+      const float x = __uint_as_float(p1[0]) + __uint_as_float(p1[1]);
+      // lane groups 0, 1 hold ks = 0, groups 2, 3 hold ks = 1 (each twice)
+      if ((lg & 1) == 0) sColP[rh][0][kt * 32 + (lg >> 1) * 16 + l16] = x;
+    }
+  };
+
+  // ---- waves 0-3: scores of item j from sColP (group mean, max-pool inside the slice clipped
+  // to the prefix [0, L - w), unpooled scores, slice-edge column sums); thread = (key, head half)
+  auto col = [&](bool snap, int g, int kl) -> float {
+    if (!snap) return sColP[0][0][kl] + sColP[1][0][kl];
+    if (NTH == 1) return sColP[g >> 1][g & 1][kl];
+    if (NTH == 2) return sColP[g][0][kl];
+    return sColP[0][0][kl] + sColP[1][0][kl];
+  };
+  auto store = [&](const PipeRef& j) {
+    int tid = threadIdx.x;   // opaque per call: no per-thread store address is kept across the loop
+    asm volatile("" : "+v"(tid));
+    const bool snap = P.layer[P.slot_layer[j.slot]].rule == RKV_SNAPKV;
+    const int cbase = j.slice * kSlice, npre = L - w, ph = P.pool_half;
+    float* Srow = P.S + (size_t)j.job * L;
+    const float NEG_INF = -__builtin_inff();
+    if (snap && NTH == 1 && G == 4 && ph == 3) {
+      // the common case: four query heads, one row tile each (heads 2h, 2h + 1 in row half h),
+      // 7-wide pool; thread = (key, row half)
+      const int kl = tid >> 1, h = tid & 1, kk = cbase + kl;
+      const float* c0 = sColP[h][0];
+      const float* c1 = sColP[h][1];
+      float su = 0.f, sc = 0.f;
+      if (kk < L) {
+        const int lo = max(kk - 3, cbase) - cbase, hi = min(min(kk + 3, cbase + kSlice - 1), npre - 1) - cbase;
+        float m0 = NEG_INF, m1 = NEG_INF;
+#pragma unroll
+        for (int u = -3; u <= 3; ++u) {
+          const int q = kl + u;
+          const bool in = q >= lo && q <= hi;
+          const int qc = in ? q : kl;
+          const float a = c0[qc], b = c1[qc];
+          m0 = in ? fmaxf(m0, a) : m0;
+          m1 = in ? fmaxf(m1, b) : m1;
+        }
+        su = c0[kl] + c1[kl];
+        sc = (m0 > NEG_INF ? m0 : 0.f) + (m1 > NEG_INF ? m1 : 0.f);
+      }
+      su += __shfl_xor(su, 1);
+      sc += __shfl_xor(sc, 1);
+      if (h == 0 && kk < L) {
+        su *= inv_g;
+        Srow[kk] = kk < npre ? sc * inv_g : su;
+        if (P.want_unpooled) P.Su[(size_t)j.job * L + kk] = su;
+      }
+      if (tid < 48) {   // slice-edge column sums: head tid / 12, offsets 0..5 and 122..127
+        const int g = tid / 12, o = tid - 12 * g;
+        const int kl2 = o < 6 ? o : kSlice - 12 + o;
+        P.edge[((size_t)j.job * nsl + j.slice) * 48 + tid] = (cbase + kl2 < L) ? sColP[g >> 1][g & 1][kl2] : 0.f;
+      }
+    } else if (snap) {
+      const int kl = tid >> 1, kk = cbase + kl;
+      const int g0 = (tid & 1) * ((G + 1) >> 1), g1 = min(G, g0 + ((G + 1) >> 1));
+      float su = 0.f, sc = 0.f;
+      if (kk < L) {
+        const int lo = max(kk - ph, cbase) - cbase, hi = min(min(kk + ph, cbase + kSlice - 1), npre - 1) - cbase;
+        for (int g = g0; g < g1; ++g) {
+          su += col(true, g, kl);
+          float m = NEG_INF;
+          for (int u = lo; u <= hi; ++u) m = fmaxf(m, col(true, g, u));
+          sc += m;
+        }
+      }
+      su += __shfl_xor(su, 1);
+      sc += __shfl_xor(sc, 1);
+      if ((tid & 1) == 0 && kk < L) {
+        su *= inv_g;
+        Srow[kk] = kk < npre ? sc * inv_g : su;
+        if (P.want_unpooled) P.Su[(size_t)j.job * L + kk] = su;
+      }
+      if (ph > 0) {
+        const int E = 4 * ph, twoP = 2 * ph;
+        float* ed = P.edge + ((size_t)j.job * nsl + j.slice) * G * E;
+        for (int e = tid; e < G * E; e += 256) {
+          const int g = e / E, o = e - g * E;
+          const int kl2 = o < twoP ? o : kSlice - twoP + (o - twoP);
+          ed[e] = (cbase + kl2 < L) ? col(true, g, kl2) : 0.f;
+        }
+      }
+    } else if (tid < kSlice && cbase + tid < L) {
+      Srow[cbase + tid] = col(false, 0, tid) * inv_g;
+    }
+  };
+
+  // ---- the whole workgroup folds a completed job: thread = (row tid % 128, slice group
+  // tid / 128), 16 loads in flight; a batch with sums not landed yet (NaN) is read again as a
+  // whole; the four groups meet in LDS.  The order of the additions is fixed, so results are
+  // reproducible.
+  auto fold = [&](int job) {
+    int tid = threadIdx.x;
+    asm volatile("" : "+v"(tid));
+    const int row = tid & (R - 1), grp = tid >> 7;
+    const float* src = P.stats + (size_t)job * nsl * R + row;
+    float z = 0.f;
+    for (int c0 = grp; c0 < nsl; c0 += 64) {
+      float x[16];
+      uint32_t it = 0;
+      while (true) {
+#pragma unroll
+        for (int u = 0; u < 16; ++u) x[u] = c0 + 4 * u < nsl ? load_coherent(src + (size_t)(c0 + 4 * u) * R) : 0.f;
+        bool missing = false;
+#pragma unroll
+        for (int u = 0; u < 16; ++u) missing = missing || (x[u] != x[u]);
+        if (__builtin_amdgcn_ballot_w64(missing) == 0 || gave_up) break;
+        if (++it > kSpinLimit) {
+          if (lane == 0) atomicOr(status, 1u);
+          gave_up = true;
+        }
+        __builtin_amdgcn_s_sleep(1);
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) z += x[u] == x[u] ? x[u] : 0.f;
+    }
+    sFoldP[grp][row] = z;
+    lds_barrier();
+    if (tid < R) {
+      z = sFoldP[0][tid] + sFoldP[1][tid] + sFoldP[2][tid] + sFoldP[3][tid];
+      const bool bad = !(z < __builtin_inff());
+      if (bad) atomicOr(status, 2u);
+      store_coherent(P.lam + (size_t)job * R + tid, z > 0.f && !bad ? 1.f / z : 0.f);
+    }
+  };
+
+  f32x4v e0[4][2], e1[4][2], e2[4][2], e3[4][2];
+  uint32_t arrival = 0;   // wave 0, lane 0: value returned by the arrival of the latest item
+  float2 al = make_float2(0.f, 0.f);   // wave 0: polled reciprocal row sums of item t - 2
+  PipeRef ja = pipe_item(first, nsl, B, Hkv);   // item t
+  PipeRef j1 = ja, j2 = ja, j3 = ja;              // items t - 1, t - 2, t - 3
+  if (wv >= 4) {
+    issue_dma(ja, 0);
+    if (T > 1) {
+      PipeRef jn = ja;
+      pipe_advance(jn, dj, ds, nsl, B, Hkv);
+      issue_dma(jn, 1);
+    }
+  }
+
+  auto iteration = [&](int t, f32x4v (&ea)[4][2], f32x4v (&eb)[4][2]) {
+    const bool doA = t < T, doB = t >= 3;
+    // B1
+    if (wv >= 4 && doA) wait_dma(t + 1 < T);
+    lds_barrier();
+    // both phases run in every iteration (on stale data at the ends of the pipeline, with their
+    // results unused), so each register set is redefined unconditionally
+    phase_a(ja, t & 1, ea);
+    // MID (wave 0)
+    if (wv == 0) {
+      // everything wave 0 issued last iteration has retired: the arrival of item t - 1 and the
+      // polled reciprocal row sums of item t - 3
+      __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));
+      const uint32_t arr = __builtin_amdgcn_readfirstlane(arrival);
+      if (lane == 0) sFold = (t >= 1 && t - 1 < T && arr == (uint32_t)(nsl - 1)) ? j1.job : -1;
+      if (doB) {
+        uint32_t it = 0;
+        while (true) {
+          const bool ok = (al.x == al.x) && (al.y == al.y);
+          const bool done = __builtin_amdgcn_ballot_w64(!ok) == 0;
+          if (done || gave_up || ++it > kSpinLimit) {
+            if (!done) {
+              if (lane == 0) atomicOr(status, 1u);
+              gave_up = true;   // report once, then stop waiting in this workgroup
+            }
+            sAlpha[2 * lane] = al.x == al.x ? al.x : 0.f;
+            sAlpha[2 * lane + 1] = al.y == al.y ? al.y : 0.f;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+          al = load_coherent2(P.lam + (size_t)j3.job * R + 2 * lane);
+        }
+      }
+    }
+    lds_barrier();   // B1.5
+    phase_b(j3, eb);
+    lds_barrier();   // B2
+    if (sFold >= 0) fold(sFold);   // this workgroup completed item t - 1's job
+    if (wv == 0) {
+      // item t's row sums, then its arrival (the fold checks for sums not yet landed)
+      if (doA) {
+        float2 o;
+        o.x = sStat[0][2 * lane] + sStat[1][2 * lane] + sStat[2][2 * lane] + sStat[3][2 * lane];
+        o.y = sStat[0][2 * lane + 1] + sStat[1][2 * lane + 1] + sStat[2][2 * lane + 1] + sStat[3][2 * lane + 1];
+        store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + 2 * lane, o.x, o.y);
+        if (lane == 0)
+          arrival = __hip_atomic_fetch_add(P.counters + (size_t)kCounterStride * (1 + ja.job), 1u, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+      if (t >= 2 && t - 2 < T) al = load_coherent2(P.lam + (size_t)j2.job * R + 2 * lane);
+    }
+    if (wv < 4) {
+      if (doB) store(j3);
+    } else if (t + 2 < T) {
+      PipeRef jn = ja;
+      pipe_advance(jn, dj, ds, nsl, B, Hkv);
+      pipe_advance(jn, dj, ds, nsl, B, Hkv);
+      issue_dma(jn, t & 1);
+    }
+    j3 = j2;
+    j2 = j1;
+    j1 = ja;
+    pipe_advance(ja, dj, ds, nsl, B, Hkv);
+  };
+
+  const int n_iter = T + 3;
+#pragma unroll 1
+  for (int t = 0; t < n_iter; t += 4) {
+    iteration(t, e0, e1);
+    if (t + 1 == n_iter) break;
+    iteration(t + 1, e1, e2);
+    if (t + 2 == n_iter) break;
+    iteration(t + 2, e2, e3);
+    if (t + 3 == n_iter) break;
+    iteration(t + 3, e3, e0);
   }
 }
 
@@ -668,6 +1285,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
   __shared__ float2 sStat[kWaves][R];
   __shared__ __attribute__((aligned(16))) float sLam[R];   // -normaliser in logit units, pass B item
   __shared__ float sCol[NG][kSlice];
+  __shared__ float sFoldP[4][R];
   __shared__ int sFold;
 
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
@@ -710,7 +1328,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
   for (int t = 0; t < T + lag; ++t) {
     const bool doA = t < T, doB = t >= lag;
     __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // operands of this iteration, stats stores of t-1
-    __syncthreads();
+    lds_barrier();
     const bool had_prev = t >= 1 && t - 1 < T;
     if (had_prev && tid == 0)
       arrived = __hip_atomic_fetch_add(P.counters + (size_t)kCounterStride * (1 + jp.job), 1u, __ATOMIC_RELAXED,
@@ -742,7 +1360,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
         }
         sLam[tid] = -lam / sl2;
       }
-      __syncthreads();
+      lds_barrier();
       // lane = key, registers = rows rt*32 + 8(r/4) + 4hf + r%4; accumulators start at -normaliser
       const bool edge_tile = cbase + wv * 32 + 32 > L - w;
       float col[NG];
@@ -793,7 +1411,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
         const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(c), __float_as_uint(c), false, false);
         if (hf == 0) sCol[0][wv * 32 + ln] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
       }
-      __syncthreads();
+      lds_barrier();
       if (t + 1 - lag < T) issue_q_to_lds<NRT, NTH>(sQB, q_of(jbn), G, w);   // sQB no longer read
 
       store_scores<NG>(P, snap, jb.job, jb.slice, cbase, sCol, inv_g);
@@ -839,7 +1457,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
         z = __uint_as_float(sz[0]) + __uint_as_float(sz[1]);
         if (hf == 0) sStat[wv][rt * 32 + ln] = make_float2(mw, z);
       }
-      __syncthreads();
+      lds_barrier();
       if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQA, q_of(jan), G, w);   // sQA no longer read
       if (tid < R) {
         float M = NEG_INF, Z = 0.f;
@@ -851,9 +1469,9 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
 
     // ============================================================ the previous item's arrival
     if (had_prev) {
-      __syncthreads();   // sStat is read above
+      lds_barrier();   // sStat is read above
       if (tid == 0) sFold = (arrived == (uint32_t)(nsl - 1)) ? jp.job : -1;
-      __syncthreads();
+      lds_barrier();
       if (sFold >= 0) fold_job_regs<R>(P, sFold, sStat);
     }
     if (doA) {
@@ -862,6 +1480,16 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
     }
     if (doB) jb = jbn;
   }
+}
+
+// Ranking key of a score: its bit pattern, whose unsigned order is the numeric order for the
+// non-negative scores the scoring kernels produce.  Patterns with the sign bit set (which no
+// valid score has) rank as +0, so the radix passes, which look at bits 0-30 only, and the
+// comparisons against the k-th key agree for every input and the compaction never writes more
+// than k positions.
+__device__ __forceinline__ uint32_t rank_bits(float v) {
+  const uint32_t u = __float_as_uint(v);
+  return (u >> 31) ? 0u : u;
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -907,7 +1535,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
       }
     }
   }
-  __syncthreads();
+  lds_barrier();
   // SnapKV: redo the pooled score of positions within pool_half of an interior slice border
   if (fix) {
     const int npre = L - w;
@@ -932,7 +1560,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
       else Srow[j] = sc / (float)G;
     }
   }
-  __syncthreads();
+  lds_barrier();
   auto get = [&](int j) -> float { return cached ? sCache[j] : Srow[j]; };
   if (ly.score) {
     float* so = ly.score + (size_t)bh * L;
@@ -953,12 +1581,12 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
         const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
         const int nb = pass == 0 ? 2048 : 1024;
         for (int b = tid; b < nb; b += kThreads) sHist[b] = 0;
-        __syncthreads();
+        lds_barrier();
         for (int j = tid; j < n; j += kThreads) {
-          const uint32_t x = __float_as_uint(get(j));
+          const uint32_t x = rank_bits(get(j));
           if ((x & pmask) == prefix) atomicAdd(&sHist[(x >> shift) & (nb - 1)], 1);
         }
-        __syncthreads();
+        lds_barrier();
         const int per = nb / kThreads;
         int cnt = 0;
         for (int i = 0; i < per; ++i) cnt += sHist[nb - 1 - (tid * per + i)];
@@ -969,7 +1597,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
           if (lane >= o) inc += y;
         }
         if (lane == 63) sScan[wv] = inc;
-        __syncthreads();
+        lds_barrier();
         int above = inc - cnt;
         for (int i = 0; i < wv; ++i) above += sScan[i];
         if (kk > above && kk <= above + cnt) {
@@ -984,11 +1612,11 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
             above += hb;
           }
         }
-        __syncthreads();
+        lds_barrier();
         prefix |= (uint32_t)sSel[0] << shift;
         pmask |= (uint32_t)(nb - 1) << shift;
         kk = sSel[1];
-        __syncthreads();
+        lds_barrier();
       }
       const uint32_t tau = prefix;
       const int need = kk;  // ties at tau taken in position order
@@ -1000,7 +1628,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
       int cg = 0, ce = 0;
       for (int j0 = w0; j0 < w1; j0 += 64) {
         const int j = j0 + lane;
-        const uint32_t x = j < w1 ? __float_as_uint(get(j)) : 0u;
+        const uint32_t x = j < w1 ? rank_bits(get(j)) : 0u;
         cg += __popcll(__ballot(j < w1 && x > tau));
         ce += __popcll(__ballot(j < w1 && x == tau));
       }
@@ -1008,7 +1636,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
         sScan[2 * wv] = cg;
         sScan[2 * wv + 1] = ce;
       }
-      __syncthreads();
+      lds_barrier();
       int bg = 0, be = 0;   // greater / equal keys before this wave's range
       for (int i = 0; i < wv; ++i) {
         bg += sScan[2 * i];
@@ -1016,7 +1644,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
       }
       for (int j0 = w0; j0 < w1; j0 += 64) {
         const int j = j0 + lane;
-        const uint32_t x = j < w1 ? __float_as_uint(get(j)) : 0u;
+        const uint32_t x = j < w1 ? rank_bits(get(j)) : 0u;
         const bool gt = j < w1 && x > tau, eq = j < w1 && x == tau;
         const uint64_t mg = __ballot(gt), me = __ballot(eq);
         const int rg = bg + __popcll(mg & lt), re = be + __popcll(me & lt);
@@ -1031,7 +1659,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
   }
   if (ly.acc) {
     // scores of the retained positions (they seed decode-phase accumulation)
-    __syncthreads();
+    lds_barrier();
     const float* accsrc = snap ? P.Su + (size_t)job * L : Srow;
     float* acc = ly.acc + (size_t)bh * ly.n_keep;
     for (int m = tid; m < ly.n_keep; m += kThreads) acc[m] = accsrc[idx[m]];
@@ -1090,7 +1718,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   }
   loads_done();
   if (fix) {
-    __syncthreads();
+    lds_barrier();
     // SnapKV: redo the pooled score of positions within pool_half of an interior slice border;
     // slice cb-1 holds keys [bnd-2P, bnd) at edge offsets [2P, 4P), slice cb keys [bnd, bnd+2P) at [0, 2P)
     const int npre = L - w;
@@ -1112,7 +1740,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
       }
       sFix[e] = sc * inv_g;
     }
-    __syncthreads();
+    lds_barrier();
 #pragma unroll
     for (int i = 0; i < kSelRegs; ++i) {
       const int j = w0 + 64 * i + lane;
@@ -1143,14 +1771,14 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
         const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
         const int nb = pass == 0 ? 2048 : 1024;
         for (int b = tid; b < nb; b += kSelThreads) sHist[b] = 0;
-        __syncthreads();
+        lds_barrier();
 #pragma unroll
         for (int i = 0; i < kSelRegs; ++i) {
           const int j = w0 + 64 * i + lane;
-          const uint32_t u = __float_as_uint(x[i]);
+          const uint32_t u = rank_bits(x[i]);
           if (j < w1 && (u & pmask) == prefix) atomicAdd(&sHist[(u >> shift) & (nb - 1)], 1);
         }
-        __syncthreads();
+        lds_barrier();
         // bins in descending order: thread tid owns bins nb-1-tid*per .. (per = 2 or 1)
         const int per = nb / kSelThreads;
         int cnt = 0;
@@ -1162,7 +1790,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
           if (lane >= o) inc += y;
         }
         if (lane == 63) sScan[wv] = inc;
-        __syncthreads();
+        lds_barrier();
         int above = inc - cnt;
         for (int q = 0; q < wv; ++q) above += sScan[q];
         if (kk > above && kk <= above + cnt) {
@@ -1177,11 +1805,11 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
             above += hb;
           }
         }
-        __syncthreads();
+        lds_barrier();
         prefix |= (uint32_t)sSel[0] << shift;
         pmask |= (uint32_t)(nb - 1) << shift;
         kk = sSel[1];
-        __syncthreads();
+        lds_barrier();
       }
       const uint32_t tau = prefix;
       const int need = kk;  // ties at tau taken in position order
@@ -1192,7 +1820,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
 #pragma unroll
       for (int i = 0; i < kSelRegs; ++i) {
         const int j = w0 + 64 * i + lane;
-        const uint32_t u = __float_as_uint(x[i]);
+        const uint32_t u = rank_bits(x[i]);
         cg += __popcll(__ballot(j < w1 && u > tau));
         ce += __popcll(__ballot(j < w1 && u == tau));
       }
@@ -1200,7 +1828,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
         sScan[2 * wv] = cg;
         sScan[2 * wv + 1] = ce;
       }
-      __syncthreads();
+      lds_barrier();
       int bg = 0, be = 0;
       for (int q = 0; q < wv; ++q) {
         bg += sScan[2 * q];
@@ -1209,7 +1837,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
 #pragma unroll
       for (int i = 0; i < kSelRegs; ++i) {
         const int j = w0 + 64 * i + lane;
-        const uint32_t u = __float_as_uint(x[i]);
+        const uint32_t u = rank_bits(x[i]);
         const bool gt = j < w1 && u > tau, eq = j < w1 && u == tau;
         const uint64_t mg = __ballot(gt), me = __ballot(eq);
         const int rg = bg + __popcll(mg & lt), re = be + __popcll(me & lt);
@@ -1224,7 +1852,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   }
   if (ly.acc) {
     // scores of the retained positions (they seed decode-phase accumulation)
-    __syncthreads();
+    lds_barrier();
     const float* accsrc = snap ? P.Su + (size_t)job * L : Srow;
     float* acc = ly.acc + (size_t)bh * ly.n_keep;
     for (int m = tid; m < ly.n_keep; m += kSelThreads) acc[m] = accsrc[idx[m]];
@@ -1310,6 +1938,15 @@ int resident_groups(K kernel) {
   return per_cu * device_cus();
 }
 
+// Resident workgroups of the pipelined kernel (one per CU; the same for every NTH).
+int resident_pipe_groups() {
+  int per_cu = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_pipe_kernel<1>, kPipeThreads, 0) != hipSuccess ||
+      per_cu < 1)
+    per_cu = 1;
+  return per_cu * device_cus();
+}
+
 template <int NRT, int NTH>
 int launch_score(const PrefillLaunch& P, hipStream_t st, void* stream) {
   const int64_t n_items = (int64_t)P.batch * P.n_scored * P.n_kv_heads * P.n_slices;
@@ -1317,7 +1954,7 @@ int launch_score(const PrefillLaunch& P, hipStream_t st, void* stream) {
   static const int fused_wg = resident_groups(score_fused_kernel<NRT, NTH>);
   static const int lagged_wg = resident_groups(score_kernel<NRT, NTH>);
   profile_mark(kStageScore, false, stream);
-  if (P.n_slices <= fused_wg / 2 && !P.force_two_pass) {
+  if (P.n_slices <= fused_wg / 2 && P.force_two_pass != 1) {
     // every workgroup is resident and a job's slices are all in flight while they wait
     const int n_wg = (int)std::min<int64_t>(n_items, fused_wg);
     score_fused_kernel<NRT, NTH><<<n_wg, kThreads, 0, st>>>(P, n_wg);
@@ -1337,18 +1974,34 @@ int launch_score(const PrefillLaunch& P, hipStream_t st, void* stream) {
 int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int n_jobs = P.batch * P.n_scored * P.n_kv_heads;
-  {
+  const int ntg = P.row_tiles_per_group;
+  // the pipelined kernel takes four row tiles when every slice of a job fits in the resident
+  // workgroups (RKV_FORCE_TWO_PASS selects the older kernels for tests: 1 two-pass, 2 single-pass)
+  static const int pipe_wg = resident_pipe_groups();
+  const bool pipe = n_jobs > 0 && row_tiles == 4 && P.force_two_pass == 0 && P.n_slices <= pipe_wg;
+  profile_mark(kStageZero, false, stream);
+  if (pipe) {
+    if (ntg == 1) prepare_kernel<1><<<n_jobs, 256, 0, st>>>(P);
+    else if (ntg == 2) prepare_kernel<2><<<n_jobs, 256, 0, st>>>(P);
+    else prepare_kernel<4><<<n_jobs, 256, 0, st>>>(P);
+  } else {
     const int n_lam = n_jobs * row_tiles * 32;
     const int n_cnt = kCounterStride * (1 + n_jobs);
     const int blocks = std::max(1, std::min(64, (std::max(n_lam, n_cnt) + 255) / 256));
-    profile_mark(kStageZero, false, stream);
     reset_counters<<<blocks, 256, 0, st>>>(P.counters, n_cnt, reinterpret_cast<uint32_t*>(P.lam), n_lam);
-    profile_mark(kStageZero, true, stream);   // the status word is cleared even without jobs
   }
+  profile_mark(kStageZero, true, stream);   // the status word is cleared even without jobs
   if (n_jobs > 0) {
-    const int ntg = P.row_tiles_per_group;
     int err = 0;
-    if (row_tiles == 4 && ntg == 1) err = launch_score<4, 1>(P, st, stream);
+    if (pipe) {
+      const int64_t n_items = (int64_t)n_jobs * P.n_slices;
+      const int n_wg = (int)std::min<int64_t>(n_items, pipe_wg);
+      profile_mark(kStageScore, false, stream);
+      if (ntg == 1) score_pipe_kernel<1><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
+      else if (ntg == 2) score_pipe_kernel<2><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
+      else score_pipe_kernel<4><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
+      profile_mark(kStageScore, true, stream);
+    } else if (row_tiles == 4 && ntg == 1) err = launch_score<4, 1>(P, st, stream);
     else if (row_tiles == 4 && ntg == 2) err = launch_score<4, 2>(P, st, stream);
     else if (row_tiles == 4) err = launch_score<4, 4>(P, st, stream);
     else if (ntg == 1) err = launch_score<8, 1>(P, st, stream);

@@ -59,7 +59,9 @@ struct PrefillLaunch {
   // workspace regions
   uint32_t* counters;     // [0] status; job j's slice-arrival counter at [kCounterStride * (1 + j)]
   float* stats;           // [J][n_slices][R][2]  per-slice row max (log2 units) and sum of exp2
-  float* lam;             // [J][R]  per-row log2 softmax normaliser (+inf for rows without keys)
+  float* lam;             // [J][R]  per-row log2 softmax normaliser (+inf for rows without keys); the
+                          //         pipelined kernel keeps the reciprocal row sum 1 / Z here instead
+  float* ncl;             // [J][R]  pipelined kernel: minus the per-row reference logit (0 for padding rows)
   float* S;               // [J][L]  ranking score
   float* Su;              // [J][L]  unpooled group-mean score (SnapKV layers, if wanted)
   float* edge;            // [J][n_slices][G][4 * pool_half]  per-query-head column sums at slice edges
@@ -72,7 +74,7 @@ static_assert(sizeof(PrefillLaunch) <= 4000, "kernel argument block too large");
 
 // Workspace layout for one launch group.
 struct PrefillWorkspace {
-  size_t counters, stats, lam, S, Su, edge, end, total;
+  size_t counters, stats, lam, ncl, S, Su, edge, end, total;
 };
 PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half);
 

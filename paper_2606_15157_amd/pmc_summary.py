@@ -21,7 +21,7 @@ import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 KERNEL_SRC = os.path.join(ROOT, "paper_2606_15157_amd", "csrc", "prefill.hip")
-SCORE_NAME = "score_fused_kernel<4, 1>"
+SCORE_NAME = "score_pipe_kernel<1>"
 COPY_NAME = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
 

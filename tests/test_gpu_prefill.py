@@ -167,9 +167,42 @@ def test_repeat_runs_are_bitwise_identical():
             assert torch.equal(a[key][l], b[key][l]), (key, l)
 
 
-def test_two_pass_kernel_matches_oracle(monkeypatch):
-    """The two-pass scoring kernel (used for prompts whose slices do not all fit in the resident
-    workgroups at once) on the 1K case and a ragged length, forced through the test hook."""
+@pytest.mark.parametrize("mode", ["1", "2"], ids=["two_pass", "single_pass"])
+def test_other_scoring_kernels_match_oracle(monkeypatch, mode):
+    """The two-pass scoring kernel (prompts whose slices do not all fit in the resident
+    workgroups; eight row tiles) and the running-maximum single-pass kernel, forced through the
+    test hook on layouts the pipelined kernel would otherwise take: the 1K case and a ragged
+    length."""
+    monkeypatch.setenv("RKV_FORCE_TWO_PASS", mode)
+    run_case([OP.SNAPKV, OP.H2O], [128, 128], [[gen(1, 0, 0, 1024)], [gen(1, 0, 1, 1024)]], window=32,
+             label=f"k{mode}_1k")
+    run_case([OP.SNAPKV, OP.H2O], [100, 100], [[gen(7, 0, 0, 777)], [gen(7, 0, 1, 777)]], window=32,
+             label=f"k{mode}_777")
+
+
+def test_reference_overflow_is_reported(monkeypatch):
+    """The pipelined kernel takes its exponentials against each row's logit with its own key and
+    with the first key.  One window row (query head 5, row 7) is set to 4 in every dimension and
+    one prefix key (position 300) to 4 in every dimension: that row's logit there is
+    4 * 4 * 128 / sqrt(128) = 181, about 170 natural-log units above its reference, beyond the
+    fp32 exponent range.  The kernel must report the overflow in the status word (bit 1) instead
+    of returning scores silently.  The exact (running-maximum) two-pass kernel, selected through
+    the test hook, still matches the oracle on the same input (the other rows keep ordinary
+    logits, so the scores stay distinct)."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    L, w = 1024, 32
+    x = gen(12, 0, 0, L)
+    q = x["q"].copy()
+    k = x["k"].copy()
+    four = f32_to_bf16_bits(np.full(128, 4.0, np.float32))
+    q[5, 7, :] = four
+    k[:, 300, :] = four
+    y = {"q": q, "k": k, "v": x["v"]}
+    plan = rkv.Plan([OP.SNAPKV], [128], window=w)
+    out = rkv.evict_prefill(plan, [bits_to_torch(q[None])], [bits_to_torch(k[None])],
+                            [bits_to_torch(x["v"][None])])
+    torch.cuda.synchronize()
+    assert rkv.prefill_check(out["workspace"]) & 2, "overflow of the row sum was not reported"
     monkeypatch.setenv("RKV_FORCE_TWO_PASS", "1")
-    run_case([OP.SNAPKV, OP.H2O], [128, 128], [[gen(1, 0, 0, 1024)], [gen(1, 0, 1, 1024)]], window=32, label="tp1k")
-    run_case([OP.SNAPKV, OP.H2O], [100, 100], [[gen(7, 0, 0, 777)], [gen(7, 0, 1, 777)]], window=32, label="tp777")
+    run_case([OP.SNAPKV], [128], [[y]], window=w, label="ref_overflow_two_pass")
