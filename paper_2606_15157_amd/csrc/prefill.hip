@@ -776,23 +776,25 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
 // permlane swaps; sums over keys (row statistics) take four DPP steps inside each row of 16
 // lanes.
 //
+// Normalisers.  Each slice stores its 128 row sums; every workgroup that scores a slice of the
+// job loads all of the job's row sums (at most 64 slices) and sums them itself, so the only
+// cross-workgroup dependency is store -> load, with no counter and no designated folder.
+//
 // Schedule of iteration t (item t enters phase A, item t - 3 phase B, each in its own register
 // set; no wait is for an operation issued in the same iteration):
-//   B1    waves 4-7 wait for their LDS DMA of item t (query block, K tile, references)
+//   B1
 //   A     logits, exponentials, per-row partial sums per key tile into sStat
-//   MID   wave 0: last iteration's memory operations have retired -> did item t - 1's arrival
-//         complete its job?  The polled reciprocal row sums of item t - 3 (re-polled while any
-//         is still NaN) go to sAlpha
+//   MID   every wave: all its earlier memory operations have completed; the row sums of item
+//         t - 3's job (loaded at MID of iteration t - 1; re-read while any is still NaN)
+//         -> reciprocal normalisers in sAlpha; then the loads of item t - 2's row sums
 //   B1.5
 //   B     item t - 3: probabilities, sums over the window rows per query head (or group) into sColP
-//   B2    the workgroup folds item t - 1's job if it completed it
-//   wave 0: store item t's row sums and count it in (no wait in between: the fold re-reads sums
-//         still marked NaN); poll the reciprocal row sums of item t - 2
-//   waves 0-3: scores of item t - 3;  waves 4-7: LDS DMA of item t + 2
-// Progress: every wait of iteration t is for events that other workgroups produce in
-// iterations <= t - 1 (a job's slices sit in at most two consecutive iterations because a job
-// has no more slices than there are workgroups), so with every workgroup resident nothing waits
-// on a later wait.
+//   B2
+//   wave 0: store item t's row sums; waves 0-3: scores of item t - 3; waves 4-7: LDS DMA of
+//         item t + 2 into the buffer item t has just left
+// Progress: the loads of iteration t - 1 are for sums that other workgroups store in iterations
+// <= t - 2 (a job's slices sit in at most two consecutive iterations because a job has no more
+// slices than there are workgroups), so with every workgroup resident no wait is on a later one.
 // ---------------------------------------------------------------------------------------------
 constexpr int kPipeWaves = 8;
 constexpr int kPipeThreads = kPipeWaves * 64;
@@ -802,8 +804,7 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 
 // Minus the reference logit of every row of every scored job, and the per-pass resets: the
-// status word, the job's arrival counter, its reciprocal row sums ("not folded": NaN) and its
-// slices' row sums ("not stored": NaN).
+// status word and the job's slices' row sums ("not stored": NaN).
 // One workgroup per job; thread = (row, half of the head dimension).
 template <int NTH>
 __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
@@ -813,11 +814,8 @@ __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
   const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
   if (job == 0 && tid == 0) P.counters[0] = 0u;
-  if (tid == 0) P.counters[(size_t)kCounterStride * (1 + job)] = 0u;
-  if (tid < R) reinterpret_cast<uint32_t*>(P.lam)[(size_t)job * R + tid] = 0xffffffffu;
   {
-    // every slice's row sums "not stored yet" (NaN): the fold checks them instead of relying on
-    // a store-before-count ordering
+    // every slice's row sums "not stored yet" (NaN): the consumers check them
     u32x4* st = reinterpret_cast<u32x4*>(P.stats + (size_t)job * P.n_slices * R);
     const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
     for (int i = tid; i < P.n_slices * R / 4; i += 256) st[i] = nan4;
@@ -875,8 +873,6 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   __shared__ __attribute__((aligned(16))) float sAlpha[R];
   __shared__ float sStat[4][R];
   __shared__ float sColP[2][2][kSlice];
-  __shared__ float sFoldP[4][R];
-  __shared__ int sFold;
 
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), lg = lane >> 4, l16 = lane & 15;
   const int kt = wv & 3, rh = wv >> 2;
@@ -936,16 +932,6 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       if (lane < 32) dma16(P.ncl + (size_t)j.job * R + 4 * lane, n_lds);
     }
   };
-  auto wait_dma = [&](bool next_issued) {
-    // the DMA of the next item (16 instructions, 17 for wave 4) may stay in flight
-    if (next_issued) {
-      if (wv == 4) wait_vmcnt<17>();
-      else wait_vmcnt<16>();
-    } else {
-      wait_vmcnt<0>();
-    }
-  };
-
   // ---- phase A: e = exp2((z - c) log2(e)/sqrt(d)) for tile (rs, ks): row rh*64 + 16 rs + 4 lg + i,
   // key key0 + 32 kt + 16 ks + l16; per-row partial sums over this wave's 32 keys into sStat[kt]
   auto phase_a = [&](const PipeRef& j, int b, f32x4v (&e)[4][2]) {
@@ -1009,7 +995,8 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   // head within the row half (SnapKV, one row tile per head), else 0 (one head per row half, or
   // the partial group / head sum of this row half)
   auto phase_b = [&](const PipeRef& j, f32x4v (&e)[4][2]) {
-    const bool snap = P.layer[P.slot_layer[j.slot]].rule == RKV_SNAPKV;
+    // the slot is clamped: phase B also runs, with its results unused, for items past the end
+    const bool snap = P.layer[P.slot_layer[min(j.slot, P.n_scored - 1)]].rule == RKV_SNAPKV;
     f32x4v a4[4];
 #pragma unroll
     for (int rs = 0; rs < 4; ++rs) a4[rs] = *reinterpret_cast<const f32x4v*>(&sAlpha[rh * 64 + rs * 16 + 4 * lg]);
@@ -1131,48 +1118,63 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     }
   };
 
-  // ---- the whole workgroup folds a completed job: thread = (row tid % 128, slice group
-  // tid / 128), 16 loads in flight; a batch with sums not landed yet (NaN) is read again as a
-  // whole; the four groups meet in LDS.  The order of the additions is fixed, so results are
+  // ---- normalisers of item j: every workgroup that scores a slice of the job sums the job's
+  // per-slice row sums itself.  Wave wv takes rows 16 wv + [0, 16); lane l reads rows
+  // 16 wv + 4 (l / 16) + [0, 4) of slices (l % 16) + 16 u, u = 0..3 (a job has at most 64 slices
+  // here), as 16-byte loads that bypass the non-coherent cache; the buffer's record count makes
+  // reads past the job's last slice return 0.  The loads are issued one iteration ahead
+  // (load_stats) and checked at the middle of the next (take_stats): a batch with sums not stored
+  // yet (NaN) is read again as a whole.  The order of the additions is fixed, so results are
   // reproducible.
-  auto fold = [&](int job) {
-    int tid = threadIdx.x;
-    asm volatile("" : "+v"(tid));
-    const int row = tid & (R - 1), grp = tid >> 7;
-    const float* src = P.stats + (size_t)job * nsl * R + row;
-    float z = 0.f;
-    for (int c0 = grp; c0 < nsl; c0 += 64) {
-      float x[16];
-      uint32_t it = 0;
-      while (true) {
+  f32x4v sx[4];
+  auto load_stats = [&](int job) {
+    // lane offset from an opaque copy of the thread index: no address is kept across the loop
+    int tv = threadIdx.x;
+    asm volatile("" : "+v"(tv));
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(P.stats + (size_t)job * nsl * R), (short)0, nsl * R * 4, 0x00020000);
+    const int off = ((tv & 15) * R + 16 * (tv >> 6) + 4 * ((tv & 63) >> 4)) * 4;
 #pragma unroll
-        for (int u = 0; u < 16; ++u) x[u] = c0 + 4 * u < nsl ? load_coherent(src + (size_t)(c0 + 4 * u) * R) : 0.f;
-        bool missing = false;
+    for (int u = 0; u < 4; ++u)   // cache policy 16: sc1 (coherent at device scope)
+      sx[u] = __builtin_bit_cast(f32x4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 16 * R * 4, 0, 16));
+  };
+  auto take_stats = [&](const PipeRef& j) {
+    uint32_t it = 0;
+    while (true) {
+      bool missing = false;
 #pragma unroll
-        for (int u = 0; u < 16; ++u) missing = missing || (x[u] != x[u]);
-        if (__builtin_amdgcn_ballot_w64(missing) == 0 || gave_up) break;
-        if (++it > kSpinLimit) {
-          if (lane == 0) atomicOr(status, 1u);
-          gave_up = true;
-        }
-        __builtin_amdgcn_s_sleep(1);
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) missing = missing || (sx[u][i] != sx[u][i]);
+      if (__builtin_amdgcn_ballot_w64(missing) == 0 || gave_up) break;
+      if (++it > kSpinLimit) {
+        if (lane == 0) atomicOr(status, 1u);
+        gave_up = true;   // report once, then stop waiting in this workgroup
+        break;
       }
+      __builtin_amdgcn_s_sleep(1);
+      load_stats(j.job);
+      wait_vmcnt<0>();
+    }
+    f32x4v z;
 #pragma unroll
-      for (int u = 0; u < 16; ++u) z += x[u] == x[u] ? x[u] : 0.f;
+    for (int i = 0; i < 4; ++i) {
+      float a = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a += sx[u][i] == sx[u][i] ? sx[u][i] : 0.f;
+      // over the 16 lanes of the row: rotations by 8, 4, 2, 1
+      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x128, 0xf, 0xf, false));
+      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x124, 0xf, 0xf, false));
+      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x122, 0xf, 0xf, false));
+      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x121, 0xf, 0xf, false));
+      const bool bad = !(a < __builtin_inff());
+      if (bad && l16 == 0) atomicOr(status, 2u);
+      z[i] = a > 0.f && !bad ? 1.f / a : 0.f;
     }
-    sFoldP[grp][row] = z;
-    lds_barrier();
-    if (tid < R) {
-      z = sFoldP[0][tid] + sFoldP[1][tid] + sFoldP[2][tid] + sFoldP[3][tid];
-      const bool bad = !(z < __builtin_inff());
-      if (bad) atomicOr(status, 2u);
-      store_coherent(P.lam + (size_t)job * R + tid, z > 0.f && !bad ? 1.f / z : 0.f);
-    }
+    if (l16 == 0) *reinterpret_cast<f32x4v*>(&sAlpha[16 * wv + 4 * lg]) = z;
   };
 
   f32x4v e0[4][2], e1[4][2], e2[4][2], e3[4][2];
-  uint32_t arrival = 0;   // wave 0, lane 0: value returned by the arrival of the latest item
-  float2 al = make_float2(0.f, 0.f);   // wave 0: polled reciprocal row sums of item t - 2
   PipeRef ja = pipe_item(first, nsl, B, Hkv);   // item t
   PipeRef j1 = ja, j2 = ja, j3 = ja;              // items t - 1, t - 2, t - 3
   if (wv >= 4) {
@@ -1185,55 +1187,31 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   }
 
   auto iteration = [&](int t, f32x4v (&ea)[4][2], f32x4v (&eb)[4][2]) {
-    const bool doA = t < T, doB = t >= 3;
-    // B1
-    if (wv >= 4 && doA) wait_dma(t + 1 < T);
+    const bool doA = t < T, doB = t >= 3 && t - 3 < T;
+    // B1 (the DMA of item t was complete at MID of iteration t - 1; the first iteration waits
+    // for the two DMAs issued before the loop)
+    if (t == 0) wait_vmcnt<0>();
     lds_barrier();
     // both phases run in every iteration (on stale data at the ends of the pipeline, with their
     // results unused), so each register set is redefined unconditionally
     phase_a(ja, t & 1, ea);
-    // MID (wave 0)
-    if (wv == 0) {
-      // everything wave 0 issued last iteration has retired: the arrival of item t - 1 and the
-      // polled reciprocal row sums of item t - 3
-      __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));
-      const uint32_t arr = __builtin_amdgcn_readfirstlane(arrival);
-      if (lane == 0) sFold = (t >= 1 && t - 1 < T && arr == (uint32_t)(nsl - 1)) ? j1.job : -1;
-      if (doB) {
-        uint32_t it = 0;
-        while (true) {
-          const bool ok = (al.x == al.x) && (al.y == al.y);
-          const bool done = __builtin_amdgcn_ballot_w64(!ok) == 0;
-          if (done || gave_up || ++it > kSpinLimit) {
-            if (!done) {
-              if (lane == 0) atomicOr(status, 1u);
-              gave_up = true;   // report once, then stop waiting in this workgroup
-            }
-            sAlpha[2 * lane] = al.x == al.x ? al.x : 0.f;
-            sAlpha[2 * lane + 1] = al.y == al.y ? al.y : 0.f;
-            break;
-          }
-          __builtin_amdgcn_s_sleep(1);
-          al = load_coherent2(P.lam + (size_t)j3.job * R + 2 * lane);
-        }
-      }
-    }
+    // MID: everything this wave issued in earlier iterations has completed (the row sums of item
+    // t - 3's job and the DMA of item t + 1); the row sums become item t - 3's normalisers.  The
+    // row sums of item t - 2's job (consumed at the next MID) are loaded at once, in every
+    // iteration so that the registers have one definition (the job is clamped where the item
+    // lies outside the pipeline)
+    wait_vmcnt<0>();
+    if (doB) take_stats(j3);
+    load_stats(min(j2.job, n_jobs - 1));
     lds_barrier();   // B1.5
     phase_b(j3, eb);
-    lds_barrier();   // B2
-    if (sFold >= 0) fold(sFold);   // this workgroup completed item t - 1's job
-    if (wv == 0) {
-      // item t's row sums, then its arrival (the fold checks for sums not yet landed)
-      if (doA) {
-        float2 o;
-        o.x = sStat[0][2 * lane] + sStat[1][2 * lane] + sStat[2][2 * lane] + sStat[3][2 * lane];
-        o.y = sStat[0][2 * lane + 1] + sStat[1][2 * lane + 1] + sStat[2][2 * lane + 1] + sStat[3][2 * lane + 1];
-        store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + 2 * lane, o.x, o.y);
-        if (lane == 0)
-          arrival = __hip_atomic_fetch_add(P.counters + (size_t)kCounterStride * (1 + ja.job), 1u, __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT);
-      }
-      if (t >= 2 && t - 2 < T) al = load_coherent2(P.lam + (size_t)j2.job * R + 2 * lane);
+    lds_barrier();   // B2: every wave is done with buffer t % 2 and with sColP
+    // wave 0: item t's row sums (the consumers check for sums not stored yet)
+    if (wv == 0 && doA) {
+      float2 o;
+      o.x = sStat[0][2 * lane] + sStat[1][2 * lane] + sStat[2][2 * lane] + sStat[3][2 * lane];
+      o.y = sStat[0][2 * lane + 1] + sStat[1][2 * lane + 1] + sStat[2][2 * lane + 1] + sStat[3][2 * lane + 1];
+      store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + 2 * lane, o.x, o.y);
     }
     if (wv < 4) {
       if (doB) store(j3);
@@ -1249,15 +1227,14 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     pipe_advance(ja, dj, ds, nsl, B, Hkv);
   };
 
-  const int n_iter = T + 3;
+  // T + 3 iterations drain the pipeline; the count is padded to a multiple of four (the padding
+  // iterations store nothing) so that the unrolled body has a single exit at its end
+  const int n_iter = (T + 3 + 3) & ~3;
 #pragma unroll 1
   for (int t = 0; t < n_iter; t += 4) {
     iteration(t, e0, e1);
-    if (t + 1 == n_iter) break;
     iteration(t + 1, e1, e2);
-    if (t + 2 == n_iter) break;
     iteration(t + 2, e2, e3);
-    if (t + 3 == n_iter) break;
     iteration(t + 3, e3, e0);
   }
 }
@@ -1975,10 +1952,12 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const int n_jobs = P.batch * P.n_scored * P.n_kv_heads;
   const int ntg = P.row_tiles_per_group;
-  // the pipelined kernel takes four row tiles when every slice of a job fits in the resident
-  // workgroups (RKV_FORCE_TWO_PASS selects the older kernels for tests: 1 two-pass, 2 single-pass)
+  // the pipelined kernel takes four row tiles when a job has at most 64 slices (8192 keys) and
+  // every slice of a job fits in the resident workgroups (RKV_FORCE_TWO_PASS selects the older
+  // kernels for tests: 1 two-pass, 2 single-pass)
   static const int pipe_wg = resident_pipe_groups();
-  const bool pipe = n_jobs > 0 && row_tiles == 4 && P.force_two_pass == 0 && P.n_slices <= pipe_wg;
+  const bool pipe = n_jobs > 0 && row_tiles == 4 && P.force_two_pass == 0 && P.n_slices <= 64 &&
+                    P.n_slices <= pipe_wg;
   profile_mark(kStageZero, false, stream);
   if (pipe) {
     if (ntg == 1) prepare_kernel<1><<<n_jobs, 256, 0, st>>>(P);
