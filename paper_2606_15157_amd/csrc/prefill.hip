@@ -1139,14 +1139,19 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       sx[u] = __builtin_bit_cast(f32x4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 16 * R * 4, 0, 16));
   };
   auto take_stats = [&](const PipeRef& j) {
+    // lane sums over its four slices, then a reduce-scatter over the 16 lanes of the row group:
+    // lane l ends with the row 4 (l / 16) + bit3(l) + 2 bit2(l) sum.  A slice not stored yet
+    // (NaN) makes its row's sum NaN; the batch is then read again as a whole.
     uint32_t it = 0;
+    float v[4];
     while (true) {
-      bool missing = false;
 #pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) missing = missing || (sx[u][i] != sx[u][i]);
-      if (__builtin_amdgcn_ballot_w64(missing) == 0 || gave_up) break;
+      for (int i = 0; i < 4; ++i) v[i] = (sx[0][i] + sx[1][i]) + (sx[2][i] + sx[3][i]);
+      dpp_halve<0x128, 4, 4>(v, (lane >> 3) & 1);   // row_ror:8       -> lane l ^ 8
+      dpp_halve<0x141, 2, 4>(v, (lane >> 2) & 1);   // row_half_mirror -> 7 - l within 8
+      dpp_halve<0x4E, 1, 4>(v, 0);                  // quad_perm [2,3,0,1]
+      dpp_halve<0xB1, 1, 4>(v, 0);                  // quad_perm [1,0,3,2]
+      if (__builtin_amdgcn_ballot_w64(v[0] != v[0]) == 0 || gave_up) break;
       if (++it > kSpinLimit) {
         if (lane == 0) atomicOr(status, 1u);
         gave_up = true;   // report once, then stop waiting in this workgroup
@@ -1156,22 +1161,13 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       load_stats(j.job);
       wait_vmcnt<0>();
     }
-    f32x4v z;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float a = 0.f;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) a += sx[u][i] == sx[u][i] ? sx[u][i] : 0.f;
-      // over the 16 lanes of the row: rotations by 8, 4, 2, 1
-      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x128, 0xf, 0xf, false));
-      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x124, 0xf, 0xf, false));
-      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x122, 0xf, 0xf, false));
-      a += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(a), 0x121, 0xf, 0xf, false));
-      const bool bad = !(a < __builtin_inff());
-      if (bad && l16 == 0) atomicOr(status, 2u);
-      z[i] = a > 0.f && !bad ? 1.f / a : 0.f;
-    }
-    if (l16 == 0) *reinterpret_cast<f32x4v*>(&sAlpha[16 * wv + 4 * lg]) = z;
+    const float z = v[0];
+    if (z == __builtin_inff() && (l16 & 3) == 0) atomicOr(status, 2u);
+    // z >= 1 for every valid row (the reference key contributes 1); padding rows have z = 0, and
+    // a row left NaN after a time-out gets 0
+    if ((l16 & 3) == 0)
+      sAlpha[16 * wv + 4 * lg + ((l16 >> 3) & 1) + 2 * ((l16 >> 2) & 1)] =
+          z > 0.f && z < __builtin_inff() ? __builtin_amdgcn_rcpf(z) : 0.f;
   };
 
   f32x4v e0[4][2], e1[4][2], e2[4][2], e3[4][2];
