@@ -403,10 +403,26 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     P.force_two_pass = force_two_pass();
     int slot = 0, n_gather = 0;
     bool want_unpooled = false;
+    // scored layers first, so that scored slot s is entry s of the layer table (the pipelined
+    // scoring kernel looks a slot's tensors up with one load)
+    int order[rkv::kMaxLayersPerLaunch];
+    Layout lays[rkv::kMaxLayersPerLaunch];
+    {
+      int n = 0;
+      for (int pass = 0; pass < 2; ++pass)
+        for (int i = 0; i < P.n_layers; ++i) {
+          const int l = g.l0 + i;
+          const bool want = (io->score_out && io->score_out[l]) || (io->acc_out && io->acc_out[l]);
+          const Layout lo = prefill_layout(plan->layers[l], p, L, want);
+          if ((lo.scored != 0) == (pass == 0)) {
+            lays[n] = lo;
+            order[n++] = i;
+          }
+        }
+    }
     for (int i = 0; i < P.n_layers; ++i) {
-      const int l = g.l0 + i;
-      const bool want = (io->score_out && io->score_out[l]) || (io->acc_out && io->acc_out[l]);
-      Layout lo = prefill_layout(plan->layers[l], p, L, want);
+      const int l = g.l0 + order[i];
+      const Layout& lo = lays[i];
       rkv::PrefillLayer& d = P.layer[i];
       d.q = io->q_win ? (const uint16_t*)io->q_win[l] : nullptr;
       d.k = (const uint16_t*)io->k[l];

@@ -899,7 +899,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   const int lrow = 4 * (wv & 3) + (lane >> 4);
   const uint32_t lane_off = (uint32_t)lrow * 256u + (uint32_t)((lane & 15) ^ lrow) * 16u;
   auto issue_dma = [&](const PipeRef& j, int b) {
-    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
+    const PrefillLayer& ly = P.layer[j.slot];
     const char* qjob = reinterpret_cast<const char*>(ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim);
     const char* khead = reinterpret_cast<const char*>(ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim);
     const int key0 = j.slice * kSlice;
@@ -996,7 +996,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   // the partial group / head sum of this row half)
   auto phase_b = [&](const PipeRef& j, f32x4v (&e)[4][2]) {
     // the slot is clamped: phase B also runs, with its results unused, for items past the end
-    const bool snap = P.layer[P.slot_layer[min(j.slot, P.n_scored - 1)]].rule == RKV_SNAPKV;
+    const bool snap = P.layer[min(j.slot, P.n_scored - 1)].rule == RKV_SNAPKV;
     f32x4v a4[4];
 #pragma unroll
     for (int rs = 0; rs < 4; ++rs) a4[rs] = *reinterpret_cast<const f32x4v*>(&sAlpha[rh * 64 + rs * 16 + 4 * lg]);
@@ -1046,7 +1046,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   auto store = [&](const PipeRef& j) {
     int tid = threadIdx.x;   // opaque per call: no per-thread store address is kept across the loop
     asm volatile("" : "+v"(tid));
-    const bool snap = P.layer[P.slot_layer[j.slot]].rule == RKV_SNAPKV;
+    const bool snap = P.layer[j.slot].rule == RKV_SNAPKV;
     const int cbase = j.slice * kSlice, npre = L - w, ph = P.pool_half;
     float* Srow = P.S + (size_t)j.job * L;
     const float NEG_INF = -__builtin_inff();

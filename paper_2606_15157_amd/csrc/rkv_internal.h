@@ -41,7 +41,8 @@ struct PrefillLayer {
 
 // One prefill launch group (up to 32 layers).  A scored "job" is a (scored layer slot,
 // sequence, KV head) triple, job = (slot * B + b) * Hkv + h; its keys are cut into n_slices
-// slices of kSlice keys, the scoring work items.
+// slices of kSlice keys, the scoring work items.  The scored layers come first in `layer`, so
+// slot s is layer[s] (slot_layer[s] == s).
 struct PrefillLaunch {
   PrefillLayer layer[kMaxLayersPerLaunch];
   int32_t n_layers;
