@@ -52,7 +52,7 @@ typedef enum {
 } rkv_status;
 
 /* Operators (Section 2.1 rule families; Section 3.1 r_{l,phi} values). */
-typedef enum { RKV_FULL = 0, RKV_STREAMING = 1, RKV_SNAPKV = 2, RKV_H2O = 3 } rkv_rule;
+typedef enum { RKV_FULL = 0, RKV_STREAMING = 1, RKV_SNAPKV = 2, RKV_H2O = 3, RKV_TOVA = 4 } rkv_rule;
 typedef enum { RKV_PHASE_PREFILL = 0, RKV_PHASE_DECODE = 1 } rkv_phase;
 /* Score transforms T of Section 3.3: identity (attention entropy) or a cap at the
  * across-layer 95th percentile (PPL degradation). */
@@ -109,7 +109,8 @@ typedef struct {
 /* Decode-phase cache of every layer with a decode operator (entries of FULL layers may be NULL).
  *  k_cache[l], v_cache[l]  bf16 [B, Hkv, C_l, d], C_l = the layer's retained decode count.
  *  pos[l]   int32 [B, Hkv, C_l]  position held by each slot (slot order is arbitrary).
- *  acc[l]   fp32  [B, Hkv, C_l]  H2O accumulated attention of each slot. */
+ *  acc[l]   fp32  [B, Hkv, C_l]  H2O accumulated attention of each slot (NULL allowed for
+ *           layers whose decode operator is not H2O). */
 typedef struct {
   void* const* k_cache;
   void* const* v_cache;
@@ -140,9 +141,11 @@ int rkv_allocate_budgets(const double* scores, int32_t n_layers, int32_t transfo
                          int32_t b_min, int32_t* budgets_out);
 
 /* Section 3.1 (Eq. 1) and 3.4: validate and freeze a plan.  Host only.
- * Operators valid in prefill: FULL, STREAMING, SNAPKV, H2O.  In decode: FULL, STREAMING, H2O
- * (SNAPKV compresses the prompt only -> RKV_ERR_PLAN).  Budgets must be >= 0 (>= 2 for a
- * decode H2O layer, >= 1 for decode STREAMING); window >= 1, pool_kernel odd >= 1,
+ * Operators valid in prefill: FULL, STREAMING, SNAPKV, H2O.  In decode: FULL, STREAMING, H2O,
+ * TOVA (SNAPKV compresses the prompt only; TOVA, eviction by the current query's attention, is
+ * a decode operator here, as in the paper's matched study -> RKV_ERR_PLAN otherwise).  Budgets
+ * must be >= 0 (>= 2 for a decode H2O layer, >= 1 for decode STREAMING and TOVA); window >= 1,
+ * pool_kernel odd >= 1,
  * n_sink >= 0, 0 <= recent_num <= recent_den, recent_den >= 1.  *out receives a new plan. */
 int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params* params, rkv_plan** out);
 void rkv_plan_destroy(rkv_plan* plan);
@@ -187,6 +190,11 @@ int rkv_prefill_check(const void* ws, size_t ws_bytes, int32_t* status_out);
  *   group mean (new entry from 0, fp32); among entries with pos <= p - r
  *   (r = floor(C*num/den)) the smallest acc is evicted, ties to the smallest position;
  *   the new token (k, v, pos = p, acc) takes the victim's slot.
+ * TOVA (Section 2.1, attention of the current query): the same C+1 entries and softmax; an
+ *   entry's score is the group mean of its probabilities at this step (nothing accumulates);
+ *   the smallest score among all C+1 entries (the new one included) is evicted, ties to the
+ *   smallest position; the new token (k, v, pos = p) takes the victim's slot.  acc is neither
+ *   read nor written (state->acc[l] may be NULL for such a layer).
  * STREAMING: the slot with the smallest position >= n_sink is replaced by the new token.
  * FULL: the layer is skipped.
  * Errors: as rkv_prefill_evict; RKV_ERR_SHAPE if position < C. */

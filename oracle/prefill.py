@@ -36,7 +36,8 @@ from __future__ import annotations
 import numpy as np
 
 FULL, STREAMING, SNAPKV, H2O = 0, 1, 2, 3
-RULE_NAMES = {FULL: "full", STREAMING: "streaming", SNAPKV: "snapkv", H2O: "h2o"}
+TOVA = 4   # a decode rule only (oracle.decode.tova_step)
+RULE_NAMES = {FULL: "full", STREAMING: "streaming", SNAPKV: "snapkv", H2O: "h2o", TOVA: "tova"}
 
 
 def bf16_to_f64(bits) -> np.ndarray:

@@ -13,11 +13,11 @@ import ctypes as C
 from typing import Sequence
 
 from . import _abi
-from ._abi import FULL, STREAMING, SNAPKV, H2O, PHASE_PREFILL, PHASE_DECODE, T_IDENTITY, T_PPL_CAP  # noqa: F401
+from ._abi import FULL, STREAMING, SNAPKV, H2O, TOVA, PHASE_PREFILL, PHASE_DECODE, T_IDENTITY, T_PPL_CAP  # noqa: F401
 from ._abi import RkvError, check
 
 __all__ = ["Plan", "allocate_budgets", "evict_prefill", "decode_step", "prefill_check", "version",
-           "FULL", "STREAMING", "SNAPKV", "H2O", "RkvError"]
+           "FULL", "STREAMING", "SNAPKV", "H2O", "TOVA", "RkvError"]
 
 
 def version() -> int:
@@ -215,7 +215,8 @@ def decode_step(plan: Plan, state, q, k, v, position: int, *, victim_out=None, s
     """One decode step for every layer with a decode operator.
 
     state: dict of per-layer lists "k_cache", "v_cache" (bf16 [B, Hkv, C_l, d]), "pos" (int32
-    [B, Hkv, C_l]), "acc" (fp32 [B, Hkv, C_l]); updated in place.  q[l]: bf16 [B, Hq, d];
+    [B, Hkv, C_l]), "acc" (fp32 [B, Hkv, C_l]; None allowed for layers whose decode operator is
+    not H2O); updated in place.  q[l]: bf16 [B, Hq, d];
     k[l], v[l]: bf16 [B, Hkv, d].  victim_out: optional per-layer int32 [B, Hkv] tensors.
     """
     n = plan.n_layers

@@ -4,8 +4,10 @@
 // entries (bf16 dot products accumulated in fp32), takes a softmax, and the group mean of the
 // probabilities is added to each entry's fp32 accumulated score.  Among entries outside the
 // protected recent window the smallest accumulated score (ties: smallest position) is
-// evicted and the new token takes its slot.  StreamingLLM: the oldest non-sink slot is
-// replaced.  Keys are read with four lanes per 256-byte row (64 B per lane).
+// evicted and the new token takes its slot.  TOVA: the same probabilities; an entry's score is
+// their group mean at this step alone, every entry (the new one included) is a candidate, and
+// the smallest score is evicted (ties: smallest position).  StreamingLLM: the oldest non-sink
+// slot is replaced.  Keys are read with four lanes per 256-byte row (64 B per lane).
 #include <hip/hip_runtime.h>
 
 #include "rkv_internal.h"
@@ -77,7 +79,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
   const int p = D.position;
   const size_t bh = (size_t)s * Hkv + h;
   int32_t* pos = ly.pos + bh * C;
-  float* acc = ly.acc + bh * C;
+  float* acc = ly.acc ? ly.acc + bh * C : nullptr;   // H2O layers only
   uint16_t* kc = ly.k_cache + bh * C * kHeadDim;
   uint16_t* vc = ly.v_cache + bh * C * kHeadDim;
   const uint16_t* knew = ly.k + bh * kHeadDim;
@@ -157,13 +159,16 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
       for (int e = tid; e <= C; e += kDecThreads) sZ[g * (C + 1) + e] *= inv;
     }
     __syncthreads();
-    const int limit = p - ly.recent;   // candidates: position <= p - r
+    // H2O: candidates have position <= p - r and the score accumulates; TOVA: every entry is a
+    // candidate and the score is this step's alone
+    const bool tova = ly.rule == RKV_TOVA;
+    const int limit = tova ? p : p - ly.recent;
     for (int e = tid; e <= C; e += kDecThreads) {
       float pm = 0.f;
 #pragma unroll
       for (int g = 0; g < G; ++g) pm += sZ[g * (C + 1) + e];
       pm = pm / (float)G;
-      const float a = (e < C ? acc[e] : 0.f) + pm;
+      const float a = (e < C && !tova ? acc[e] : 0.f) + pm;
       sAcc[e] = a;
       const int ps = e < C ? pos[e] : p;
       if (ps <= limit) {
@@ -186,7 +191,8 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
     __syncthreads();
     victim = sVictim;
     if (victim == C) victim = -1;
-    for (int e = tid; e < C; e += kDecThreads) acc[e] = (e == victim) ? sAcc[C] : sAcc[e];
+    if (!tova)
+      for (int e = tid; e < C; e += kDecThreads) acc[e] = (e == victim) ? sAcc[C] : sAcc[e];
   }
   // the new token takes the victim's slot
   if (victim >= 0) {

@@ -17,7 +17,7 @@ thread_local std::string g_error;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-bool rule_valid(int32_t r) { return r >= RKV_FULL && r <= RKV_H2O; }
+bool rule_valid(int32_t r) { return r >= RKV_FULL && r <= RKV_TOVA; }
 
 // Retained positions and selection layout of one layer (prefill phase).
 struct Layout {
@@ -303,6 +303,10 @@ int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params*
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": negative budget");
     if (ly.rule_decode == RKV_SNAPKV)
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": SnapKV compresses the prompt only, not valid in decode");
+    if (ly.rule_prefill == RKV_TOVA)
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": TOVA is a decode operator, not valid in prefill");
+    if (ly.rule_decode == RKV_TOVA && ly.budget_decode < 1)
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": decode TOVA needs budget >= 1");
     if (ly.rule_decode == RKV_H2O && ly.budget_decode < 2)
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": decode H2O needs budget >= 2");
     if (ly.rule_decode == RKV_STREAMING && ly.budget_decode < 1)
@@ -488,7 +492,7 @@ int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_deco
   if (!plan || !state || !input) return rkv::fail(RKV_ERR_INVALID_ARG, "null plan, state or input");
   int st = validate_shape(shape);
   if (st) return st;
-  if (!state->k_cache || !state->v_cache || !state->pos || !state->acc || !input->q || !input->k || !input->v)
+  if (!state->k_cache || !state->v_cache || !state->pos || !input->q || !input->k || !input->v)
     return rkv::fail(RKV_ERR_INVALID_ARG, "state and input arrays are required");
   const rkv_params& p = plan->params;
   const int n = (int)plan->layers.size();
@@ -508,14 +512,15 @@ int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_deco
       if (ly.rule_decode == RKV_FULL) continue;
       const int C = ly.budget_decode;
       if (position < C) return rkv::fail(RKV_ERR_SHAPE, "position must be >= the layer's capacity");
-      if (!state->k_cache[l] || !state->v_cache[l] || !state->pos[l] || !state->acc[l] || !input->q[l] ||
-          !input->k[l] || !input->v[l])
+      const bool need_acc = ly.rule_decode == RKV_H2O;
+      if (!state->k_cache[l] || !state->v_cache[l] || !state->pos[l] || (need_acc && (!state->acc || !state->acc[l])) ||
+          !input->q[l] || !input->k[l] || !input->v[l])
         return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null decode buffer");
       rkv::DecodeLayer& d = D.layer[cnt++];
       d.k_cache = (uint16_t*)state->k_cache[l];
       d.v_cache = (uint16_t*)state->v_cache[l];
       d.pos = state->pos[l];
-      d.acc = state->acc[l];
+      d.acc = need_acc ? state->acc[l] : nullptr;
       d.q = (const uint16_t*)input->q[l];
       d.k = (const uint16_t*)input->k[l];
       d.v = (const uint16_t*)input->v[l];

@@ -97,6 +97,13 @@ def test_plan_validation():
     with pytest.raises(rkv.RkvError) as e:
         rkv.Plan([rkv.H2O], [64], [rkv.H2O], [1])
     assert e.value.status == 3
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan([rkv.TOVA], [64])                                   # TOVA is decode-only
+    assert e.value.status == 3
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan([rkv.H2O], [64], [rkv.TOVA], [0])
+    assert e.value.status == 3
+    rkv.Plan([rkv.H2O] * 2, [64] * 2, [rkv.H2O, rkv.TOVA], [64, 1])   # the paper's H2O / TOVA pair
 
 
 def test_retained_counts_and_workspace():
@@ -168,3 +175,8 @@ def test_decode_argument_errors():
     assert L.rkv_decode_step(plan.handle, C.byref(sh), None, C.byref(inp), 100, None) == 1
     sh2 = _abi.Shape(1, 1, 24, 8, 128)                                                               # G = 3
     assert L.rkv_decode_step(plan.handle, C.byref(sh2), C.byref(st_), C.byref(inp), 100, None) == 4
+    # the accumulator is required for an H2O decode layer (it may be NULL for TOVA layers)
+    st_nacc = _abi.DecodeState(fake, fake, fake, rkv._parr([None]))
+    assert L.rkv_decode_step(plan.handle, C.byref(sh), C.byref(st_nacc), C.byref(inp), 100, None) == 1
+    st_nacc2 = _abi.DecodeState(fake, fake, fake, None)
+    assert L.rkv_decode_step(plan.handle, C.byref(sh), C.byref(st_nacc2), C.byref(inp), 100, None) == 1

@@ -114,3 +114,88 @@ def test_streaming_decode_replaces_oldest_non_sink():
             assert vv[0, h] == cand[np.argmin(pb[cand])]
             assert state["pos"][0].cpu().numpy()[0, h, vv[0, h]] == p
             assert np.array_equal(torch_to_bits(state["k_cache"][0])[0, h, vv[0, h]], d["k"][t][h])
+
+
+def _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers, Hq=32, Hkv=8, seed_workload=5):
+    """Teacher-forced decode steps; every (layer, sequence, KV head) is checked against the oracle
+    step of its rule: the victim must be a candidate whose score is within 1e-3 of the smallest
+    (ties inside that band may resolve either way), and the slots change exactly as the victim
+    says.  Returns the number of victims chosen differently inside the band."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    G = Hq // Hkv
+    recent = C // 2
+    ins = [[decode_steps(seed_workload, s, l, steps=steps) for s in range(B)] for l in range(n_layers)]
+    n_close = 0
+    for t in range(steps):
+        p = L + t
+        before = [snapshot_opt(state, l) for l in range(n_layers)]
+        q = [bits_to_torch(np.stack([ins[l][s]["q"][t] for s in range(B)])) for l in range(n_layers)]
+        k = [bits_to_torch(np.stack([ins[l][s]["k"][t] for s in range(B)])) for l in range(n_layers)]
+        v = [bits_to_torch(np.stack([ins[l][s]["v"][t] for s in range(B)])) for l in range(n_layers)]
+        vic = [torch.empty((B, Hkv), dtype=torch.int32, device="cuda") for _ in range(n_layers)]
+        rkv.decode_step(plan, state, q, k, v, p, victim_out=vic)
+        torch.cuda.synchronize()
+        for l in range(n_layers):
+            after = snapshot_opt(state, l)
+            vv = vic[l].cpu().numpy()
+            for s in range(B):
+                for h in range(Hkv):
+                    kc = OP.bf16_to_f64(before[l]["k"][s, h])
+                    qg = OP.bf16_to_f64(ins[l][s]["q"][t][h * G:(h + 1) * G])
+                    kt = OP.bf16_to_f64(ins[l][s]["k"][t][h])
+                    what = f"step {t} layer {l} seq {s} head {h}"
+                    e = vv[s, h] if vv[s, h] >= 0 else C
+                    if rules_dec[l] == OP.TOVA:
+                        score, v_ora = OD.tova_step(kc, before[l]["pos"][s, h], qg, kt, p)
+                        assert score[e] <= score.min() * (1 + 1e-3) + 1e-30, what + ": victim is not a minimum"
+                        assert after["acc"] is None
+                    else:
+                        score, v_ora, cand = OD.h2o_step(kc, before[l]["pos"][s, h],
+                                                         before[l]["acc"][s, h].astype(np.float64), qg, kt, p, recent)
+                        assert cand[e], what + ": victim is protected"
+                        assert score[e] <= score[cand].min() * (1 + 1e-3) + 1e-30, what + ": victim is not a minimum"
+                        exp_acc = score[:C].copy()
+                        if e < C:
+                            exp_acc[e] = score[C]
+                        check_scores(after["acc"][s, h], exp_acc, what + " acc")
+                    n_close += int(e != v_ora)
+                    pos_exp = before[l]["pos"][s, h].copy()
+                    k_exp = before[l]["k"][s, h].copy()
+                    v_exp = before[l]["v"][s, h].copy()
+                    if e < C:
+                        pos_exp[e] = p
+                        k_exp[e] = ins[l][s]["k"][t][h]
+                        v_exp[e] = ins[l][s]["v"][t][h]
+                    assert np.array_equal(after["pos"][s, h], pos_exp), what
+                    assert np.array_equal(after["k"][s, h], k_exp), what
+                    assert np.array_equal(after["v"][s, h], v_exp), what
+    return n_close
+
+
+def snapshot_opt(state, l):
+    acc = state["acc"][l]
+    return {"k": torch_to_bits(state["k_cache"][l]), "v": torch_to_bits(state["v_cache"][l]),
+            "pos": state["pos"][l].cpu().numpy().copy(), "acc": None if acc is None else acc.cpu().numpy().copy()}
+
+
+@pytest.mark.parametrize("C", [1, 64, 200])
+def test_tova_decode_teacher_forced(C):
+    """TOVA decode on two layers (prefill H2O), accumulator passed as NULL."""
+    B, L, steps, n_layers = 2, 640, 16, 2
+    rules_dec = [OP.TOVA] * n_layers
+    plan, state = prefill_state(rules_dec, C, L, B, n_layers)
+    state["acc"] = [None] * n_layers
+    n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers)
+    print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
+
+
+def test_h2o_tova_composition():
+    """The paper's system composition: H2O decode on layers 0-15, TOVA on 16-31, 512 positions
+    per layer, after an H2O prefill of a 1024-token prompt; every layer checked for 3 steps."""
+    B, L, steps, n_layers, C = 1, 1024, 3, 32, 512
+    rules_dec = [OP.H2O] * 16 + [OP.TOVA] * 16
+    plan, state = prefill_state(rules_dec, C, L, B, n_layers)
+    state["acc"] = [a if r == OP.H2O else None for a, r in zip(state["acc"], rules_dec)]
+    n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers, seed_workload=13)
+    print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
