@@ -75,6 +75,57 @@ def cpu_baseline(xs, rules, budgets, max_seconds=20.0):
     }
 
 
+def decode_measure(dev, steps=10, warmup=2, B=64, C=1024, n_layers=32):
+    """Decode-step throughput at the 64-sequence shape: 32 layers, 32 query / 8 KV heads,
+    capacity 1024 per layer, cache resident in HBM (random bf16 contents: the kernel's work does
+    not depend on the values).  Two plans: H2O on every layer (recent half protected) and the
+    H2O 0-15 / TOVA 16-31 composition.  Algorithmic bytes per step: every cached key row read
+    once (C x 256 B per sequence, layer and KV head), the slot positions read, H2O's accumulated
+    scores read and written, the new query / key read and the new key / value row written."""
+    import torch
+    import paper_2606_15157_amd as rkv
+    g = torch.Generator(device=dev).manual_seed(20260615)
+    kc = [torch.randn((B, HKV, C, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in range(n_layers)]
+    vc = [torch.randn((B, HKV, C, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in range(n_layers)]
+    pos0 = (torch.arange(C, device=dev, dtype=torch.int32) * 8).expand(B, HKV, C).contiguous()
+    acc = [torch.rand((B, HKV, C), generator=g, device=dev) for _ in range(n_layers)]
+    n_in = warmup + steps
+    qs = [[torch.randn((B, HQ, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in range(n_layers)]
+          for _ in range(n_in)]
+    ks = [[torch.randn((B, HKV, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in range(n_layers)]
+          for _ in range(n_in)]
+    out = {}
+    for name, rules in (("h2o", [rkv.H2O] * n_layers),
+                        ("h2o_tova", [rkv.H2O] * (n_layers // 2) + [rkv.TOVA] * (n_layers - n_layers // 2))):
+        plan = rkv.Plan([rkv.H2O] * n_layers, [C] * n_layers, rules, [C] * n_layers, window=W)
+        state = {"k_cache": kc, "v_cache": vc, "pos": [pos0.clone() for _ in range(n_layers)],
+                 "acc": [a if r == rkv.H2O else None for a, r in zip(acc, rules)]}
+        stream = torch.cuda.current_stream(dev)
+        p0 = 8 * C
+        for i in range(warmup):
+            rkv.decode_step(plan, state, qs[i], ks[i], ks[i], p0 + i, stream=stream)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(warmup, n_in):
+            rkv.decode_step(plan, state, qs[i], ks[i], ks[i], p0 + i, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / steps
+        n_h2o = sum(1 for r in rules if r == rkv.H2O)
+        units = B * HKV * n_layers
+        alg = units * C * (D * 2 + 4) + B * HKV * n_h2o * C * 8 + B * n_layers * (HQ + HKV) * D * 2 + units * 2 * D * 2
+        out[name] = {"us_per_step": us, "algorithmic_bytes_per_step": alg, "achieved_GBps": alg / (us * 1e-6) / 1e9,
+                     "hbm_frac": alg / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS,
+                     "sequence_tokens_per_s": B / (us * 1e-6)}
+        log(f"decode {name}: {us:.1f} us/step ({out[name]['achieved_GBps']:.0f} GB/s)")
+    del kc, vc, acc, qs, ks
+    torch.cuda.empty_cache()
+    return {"workload": f"{B} sequences x {n_layers} layers, 32 q / 8 kv heads, d=128, capacity {C} per layer, "
+                        f"{steps} timed steps", **out}
+
+
 def kernel_source_hash():
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
 
@@ -97,6 +148,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (outside the timed region) so a "
                          "rocprofv3 --pmc run of this command can scale FETCH_SIZE / WRITE_SIZE")
@@ -224,6 +276,10 @@ def main():
             "algorithmic_bytes_per_launch": score_bytes,
         },
     }
+    if not args.no_decode:
+        del out, ws, call, q, k, v
+        torch.cuda.empty_cache()
+        rec["decode"] = decode_measure(dev)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         rec["cpu_baseline"] = cpu_baseline(xs, rules, budgets, args.cpu_seconds)
