@@ -151,6 +151,17 @@ int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params*
 void rkv_plan_destroy(rkv_plan* plan);
 int rkv_plan_num_layers(const rkv_plan* plan, int32_t* n_layers);
 
+/* Sections 3.1 and 3.4: the plan is fixed offline and loaded once per run.  A serialized plan is
+ * a little-endian byte record: "RKVP", int32 format version (1), int32 n_layers, the five
+ * rkv_params fields, then per layer (rule_prefill, budget_prefill, rule_decode, budget_decode);
+ * 32 + 16 * n_layers bytes.  Host only.
+ * rkv_plan_serialize: writes the record into buf if cap is large enough and always sets *size
+ *   to the record's length (buf may be NULL to query it); RKV_ERR_INVALID_ARG if cap is too small.
+ * rkv_plan_deserialize: parses and re-validates as rkv_plan_create does (same errors), plus
+ *   RKV_ERR_INVALID_ARG for a wrong magic, version or length.  *out receives a new plan. */
+int rkv_plan_serialize(const rkv_plan* plan, void* buf, size_t cap, size_t* size);
+int rkv_plan_deserialize(const void* buf, size_t size, rkv_plan** out);
+
 /* Retained positions per layer for a prompt of seq_len tokens in `phase`:
  * FULL -> seq_len; otherwise min(budget, seq_len).  counts_out[n_layers] (host). */
 int rkv_plan_retained_counts(const rkv_plan* plan, int32_t phase, int32_t seq_len, int32_t* counts_out);

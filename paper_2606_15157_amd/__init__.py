@@ -56,6 +56,40 @@ class Plan:
         self.rules_decode = rules_decode
         self.window = window
 
+    @classmethod
+    def from_route(cls, rules_prefill, weights, total: int, b_min: int, rules_decode=None, *,
+                   transform: int = T_IDENTITY, **params):
+        """Plan whose per-layer capacities split `total` by allocation `weights` (Eq. 3); decode
+        capacities equal the prefill ones."""
+        budgets = allocate_budgets(weights, total, b_min, transform)
+        return cls(rules_prefill, budgets, rules_decode, budgets if rules_decode is not None else None, **params)
+
+    def to_bytes(self) -> bytes:
+        """The plan's serialized record (rkv_plan_serialize)."""
+        size = C.c_size_t()
+        check(_abi.lib().rkv_plan_serialize(self._h, None, 0, C.byref(size)))
+        buf = C.create_string_buffer(size.value)
+        check(_abi.lib().rkv_plan_serialize(self._h, buf, size.value, C.byref(size)))
+        return buf.raw[:size.value]
+
+    @classmethod
+    def from_bytes(cls, data: bytes) -> "Plan":
+        """A plan from a serialized record, validated by the library (rkv_plan_deserialize)."""
+        import struct
+        handle = C.c_void_p()
+        check(_abi.lib().rkv_plan_deserialize(C.c_char_p(bytes(data)), len(data), C.byref(handle)))
+        words = struct.unpack("<%di" % (len(data) // 4), data)
+        n = words[2]
+        self = cls.__new__(cls)
+        self._h = handle
+        self.n_layers = n
+        self.params = _abi.Params(*words[3:8])
+        lay = words[8:]
+        self.rules_prefill = [lay[4 * i] for i in range(n)]
+        self.rules_decode = [lay[4 * i + 2] for i in range(n)]
+        self.window = words[3]
+        return self
+
     @property
     def handle(self):
         return self._h

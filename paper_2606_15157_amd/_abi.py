@@ -17,6 +17,7 @@ T_IDENTITY, T_PPL_CAP = 0, 1
 
 EXPORTED = [
     "rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_destroy", "rkv_plan_num_layers",
+    "rkv_plan_serialize", "rkv_plan_deserialize",
     "rkv_plan_retained_counts", "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check",
     "rkv_decode_step", "rkv_profile_enable", "rkv_profile_read", "rkv_last_error", "rkv_version",
 ]
@@ -70,6 +71,8 @@ def lib():
         L.rkv_plan_destroy.argtypes = [C.c_void_p]
         L.rkv_plan_destroy.restype = None
         L.rkv_plan_num_layers.argtypes = [C.c_void_p, C.POINTER(C.c_int32)]
+        L.rkv_plan_serialize.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.POINTER(C.c_size_t)]
+        L.rkv_plan_deserialize.argtypes = [C.c_void_p, C.c_size_t, C.POINTER(C.c_void_p)]
         L.rkv_plan_retained_counts.argtypes = [C.c_void_p, C.c_int32, C.c_int32, C.POINTER(C.c_int32)]
         L.rkv_prefill_workspace_size.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(C.c_size_t)]
         L.rkv_prefill_evict.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(PrefillIO), C.c_void_p, C.c_size_t,
@@ -83,6 +86,7 @@ def lib():
         L.rkv_last_error.argtypes = []
         L.rkv_version.argtypes = []
         for name in ("rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_num_layers", "rkv_plan_retained_counts",
+                     "rkv_plan_serialize", "rkv_plan_deserialize",
                      "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check", "rkv_decode_step",
                      "rkv_profile_enable", "rkv_profile_read", "rkv_version"):
             getattr(L, name).restype = C.c_int

@@ -18,6 +18,8 @@ thread_local std::string g_error;
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 bool rule_valid(int32_t r) { return r >= RKV_FULL && r <= RKV_TOVA; }
+constexpr int32_t kPlanMagic = 0x50564b52;   // "RKVP" as little-endian bytes
+constexpr int32_t kPlanFormat = 1;
 
 // Retained positions and selection layout of one layer (prefill phase).
 struct Layout {
@@ -321,6 +323,61 @@ int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params*
 }
 
 void rkv_plan_destroy(rkv_plan* plan) { delete plan; }
+
+int rkv_plan_serialize(const rkv_plan* plan, void* buf, size_t cap, size_t* size) {
+  rkv::clear_error();
+  if (!plan || !size) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  const size_t n = plan->layers.size();
+  const size_t need = 32 + 16 * n;
+  *size = need;
+  if (!buf) return RKV_OK;
+  if (cap < need) return rkv::fail(RKV_ERR_INVALID_ARG, "buffer too small for the serialized plan");
+  std::vector<int32_t> w;
+  w.reserve(need / 4);
+  w.push_back(kPlanMagic);
+  w.push_back(kPlanFormat);
+  w.push_back((int32_t)n);
+  const rkv_params& p = plan->params;
+  for (int32_t v : {p.window, p.pool_kernel, p.n_sink, p.recent_num, p.recent_den}) w.push_back(v);
+  for (const rkv_layer& ly : plan->layers)
+    for (int32_t v : {ly.rule_prefill, ly.budget_prefill, ly.rule_decode, ly.budget_decode}) w.push_back(v);
+  unsigned char* o = static_cast<unsigned char*>(buf);
+  for (size_t i = 0; i < w.size(); ++i) {   // little-endian, independent of the host's byte order
+    const uint32_t u = (uint32_t)w[i];
+    for (int b = 0; b < 4; ++b) o[4 * i + b] = (unsigned char)(u >> (8 * b));
+  }
+  return RKV_OK;
+}
+
+int rkv_plan_deserialize(const void* buf, size_t size, rkv_plan** out) {
+  rkv::clear_error();
+  if (!buf || !out) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (size < 32 || size % 4) return rkv::fail(RKV_ERR_INVALID_ARG, "serialized plan has a bad length");
+  const unsigned char* in = static_cast<const unsigned char*>(buf);
+  auto word = [&](size_t i) {
+    uint32_t u = 0;
+    for (int b = 0; b < 4; ++b) u |= (uint32_t)in[4 * i + b] << (8 * b);
+    return (int32_t)u;
+  };
+  if (word(0) != kPlanMagic) return rkv::fail(RKV_ERR_INVALID_ARG, "not a serialized plan (magic)");
+  if (word(1) != kPlanFormat) return rkv::fail(RKV_ERR_INVALID_ARG, "unknown serialized plan format version");
+  const int32_t n = word(2);
+  if (n < 1 || size != 32 + 16 * (size_t)n) return rkv::fail(RKV_ERR_INVALID_ARG, "serialized plan length does not match its layer count");
+  rkv_params p;
+  p.window = word(3);
+  p.pool_kernel = word(4);
+  p.n_sink = word(5);
+  p.recent_num = word(6);
+  p.recent_den = word(7);
+  std::vector<rkv_layer> layers((size_t)n);
+  for (int32_t l = 0; l < n; ++l) {
+    layers[l].rule_prefill = word(8 + 4 * l);
+    layers[l].budget_prefill = word(9 + 4 * l);
+    layers[l].rule_decode = word(10 + 4 * l);
+    layers[l].budget_decode = word(11 + 4 * l);
+  }
+  return rkv_plan_create(layers.data(), n, &p, out);
+}
 
 int rkv_plan_num_layers(const rkv_plan* plan, int32_t* n_layers) {
   rkv::clear_error();

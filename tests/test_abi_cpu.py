@@ -180,3 +180,39 @@ def test_decode_argument_errors():
     assert L.rkv_decode_step(plan.handle, C.byref(sh), C.byref(st_nacc), C.byref(inp), 100, None) == 1
     st_nacc2 = _abi.DecodeState(fake, fake, fake, None)
     assert L.rkv_decode_step(plan.handle, C.byref(sh), C.byref(st_nacc2), C.byref(inp), 100, None) == 1
+
+
+def test_plan_serialization_round_trip_and_rejects_damage():
+    """A plan is built once and loaded per run (Sections 3.1, 3.4): the serialized record
+    round-trips bit-exactly and a damaged record is rejected with the creation checks."""
+    import struct
+    rules_p = [rkv.STREAMING] * 2 + [rkv.SNAPKV] * 14 + [rkv.H2O] * 12 + [rkv.SNAPKV] * 4
+    rules_d = [rkv.H2O] * 16 + [rkv.TOVA] * 16
+    plan = rkv.Plan.from_route(rules_p, [1.0 + i for i in range(32)], 32 * 512, 48, rules_d, window=32,
+                               pool_kernel=7)
+    blob = plan.to_bytes()
+    assert len(blob) == 32 + 16 * 32 and blob[:4] == b"RKVP"
+    words = struct.unpack("<%di" % (len(blob) // 4), blob)
+    assert words[1] == 1 and words[2] == 32 and words[3:8] == (32, 7, 4, 1, 2)
+    budgets = [words[8 + 4 * i + 1] for i in range(32)]
+    assert sum(budgets) == 32 * 512 and min(budgets) >= 48
+    again = rkv.Plan.from_bytes(blob)
+    assert again.to_bytes() == blob
+    assert again.rules_prefill == rules_p and again.rules_decode == rules_d
+    assert again.retained_counts(8192) == plan.retained_counts(8192)
+    # damaged records
+    for bad, status in ((b"XKVP" + blob[4:], 1),                                  # magic
+                        (blob[:4] + struct.pack("<i", 2) + blob[8:], 1),           # version
+                        (blob[:-4], 1),                                            # length
+                        (blob[:8] + struct.pack("<i", 31) + blob[12:], 1),         # layer count
+                        (blob[:32] + struct.pack("<i", rkv.SNAPKV) + blob[36:40] + struct.pack("<i", rkv.SNAPKV)
+                         + blob[44:], 3)):                                         # SnapKV in decode
+        with pytest.raises(rkv.RkvError) as e:
+            rkv.Plan.from_bytes(bad)
+        assert e.value.status == status
+    # the size query and a short buffer
+    L = _abi.lib()
+    size = C.c_size_t()
+    assert L.rkv_plan_serialize(plan.handle, None, 0, C.byref(size)) == 0 and size.value == len(blob)
+    buf = C.create_string_buffer(16)
+    assert L.rkv_plan_serialize(plan.handle, buf, 16, C.byref(size)) == 1
