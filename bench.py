@@ -126,6 +126,39 @@ def decode_measure(dev, steps=10, warmup=2, B=64, C=1024, n_layers=32):
                         f"{steps} timed steps", **out}
 
 
+def entropy_measure(dev, reps=3, n_layers=32, L=4096):
+    """Entropy profile of a calibration-shaped input: 32 layers, 32 query / 8 KV heads, every
+    query of a 4096-token sequence (random bf16 contents: the work does not depend on them).
+    Algorithmic work: the causal logits, sum over query positions t of (t + 1) keys x 2 d flop
+    per query head, on bf16 MFMA; one exponential per logit."""
+    import torch
+    import paper_2606_15157_amd as rkv
+    g = torch.Generator(device=dev).manual_seed(20260616)
+    q = [torch.randn((1, HQ, L, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in range(n_layers)]
+    k = [torch.randn((1, HKV, L, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in range(n_layers)]
+    stream = torch.cuda.current_stream(dev)
+    rkv.entropy_profile(q, k, stream=stream)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        out = rkv.entropy_profile(q, k, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    if int(out["status"].item()) != 0:
+        raise RuntimeError("entropy profile reported a non-finite row")
+    ms = e0.elapsed_time(e1) / reps
+    flop = n_layers * HQ * (L * (L + 1) // 2) * D * 2
+    tflops = flop / (ms * 1e-3) / 1e12
+    log(f"entropy profile: {ms:.3f} ms ({tflops:.0f} TFLOP/s causal)")
+    del q, k
+    torch.cuda.empty_cache()
+    return {"workload": f"{n_layers} layers, 32 q / 8 kv heads, d=128, every query of a {L}-token sequence",
+            "ms": ms, "algorithmic_flop": flop, "achieved_TFLOPs": tflops, "peak_TFLOPs": 2500.0,
+            "mfma_frac": tflops / 2500.0, "exps_per_s": n_layers * HQ * (L * (L + 1) // 2) / (ms * 1e-3)}
+
+
 def kernel_source_hash():
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
 
@@ -149,6 +182,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
+    ap.add_argument("--no-entropy", action="store_true", help="skip the entropy-profile measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (outside the timed region) so a "
                          "rocprofv3 --pmc run of this command can scale FETCH_SIZE / WRITE_SIZE")
@@ -280,6 +314,8 @@ def main():
         del out, ws, call, q, k, v
         torch.cuda.empty_cache()
         rec["decode"] = decode_measure(dev)
+    if not args.no_entropy:
+        rec["entropy"] = entropy_measure(dev)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         rec["cpu_baseline"] = cpu_baseline(xs, rules, budgets, args.cpu_seconds)

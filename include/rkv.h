@@ -212,6 +212,27 @@ int rkv_prefill_check(const void* ws, size_t ws_bytes, int32_t* status_out);
 int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_decode_state* state,
                     const rkv_decode_input* input, int32_t position, void* stream);
 
+/* Section 3.3: the attention-entropy layer score H_l, the mean over sequences, query heads and
+ * profiled query positions of the Shannon entropy (nats) of each query's causal attention row
+ * softmax_j(q_t . k_j / sqrt(d)), j = 0..t (query head hq reads KV head hq / G).  Entropy
+ * allocation feeds H_l unchanged (identity transform) into rkv_allocate_budgets with b_min 32.
+ * shape: batch B, seq_len L, Hq, Hkv (Hq / Hkv in {1, 2, 4, 8}), head_dim 128.
+ * q[l]: bf16 [B, Hq, n_q, d], the queries of the last n_q positions L - n_q .. L - 1 of layer l
+ *   (n_q = L profiles every query); k[l]: bf16 [B, Hkv, L, d].  Device pointers, host arrays.
+ * rows_out: device fp32 [n_layers, B, Hq, n_q], every profiled row's entropy;
+ * h_out: device fp32 [n_layers]; status: device uint32, set to 0, or 1 when some row is not
+ *   finite (a logit beyond ~88 natural-log units above the larger of the row's logits with
+ *   its own key and with key 0; h_out is then invalid).
+ * ws: caller-owned device workspace of at least rkv_entropy_workspace_size bytes (8-byte
+ *   aligned; per-block partial sums).  Enqueued on `stream`; no allocation.
+ * Errors: RKV_ERR_INVALID_ARG (null pointers, n_layers < 1, n_q outside [1, L]), RKV_ERR_SHAPE,
+ *   RKV_ERR_UNSUPPORTED (head_dim != 128 or Hq / Hkv not in {1, 2, 4, 8}), RKV_ERR_WORKSPACE,
+ *   RKV_ERR_HIP. */
+int rkv_entropy_workspace_size(const rkv_shape* shape, int32_t n_layers, int32_t n_q, size_t* bytes);
+int rkv_entropy_profile(const rkv_shape* shape, int32_t n_layers, int32_t n_q, const void* const* q,
+                        const void* const* k, float* rows_out, float* h_out, uint32_t* status, void* ws,
+                        size_t ws_bytes, void* stream);
+
 /* Kernel timing for benchmarks and tests.  rkv_profile_enable(stage) makes every following
  * launch of that stage record a pair of HIP events around it on the caller's stream
  * (stage: 0 counter reset, 1 scoring, 2 selection, 3 gather, 4 decode; -1 disables).

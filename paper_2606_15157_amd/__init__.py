@@ -17,6 +17,7 @@ from ._abi import FULL, STREAMING, SNAPKV, H2O, TOVA, PHASE_PREFILL, PHASE_DECOD
 from ._abi import RkvError, check
 
 __all__ = ["Plan", "allocate_budgets", "evict_prefill", "decode_step", "prefill_check", "version",
+           "entropy_profile", "entropy_budgets",
            "FULL", "STREAMING", "SNAPKV", "H2O", "TOVA", "RkvError"]
 
 
@@ -243,6 +244,37 @@ def prefill_check(workspace) -> int:
     st = C.c_int32()
     check(_abi.lib().rkv_prefill_check(C.c_void_p(workspace.data_ptr()), workspace.numel(), C.byref(st)))
     return st.value
+
+
+def entropy_profile(q, k, *, stream=None):
+    """Attention-entropy layer scores H_l (Section 3.3): q[l] bf16 [B, Hq, n_q, d] (queries of the
+    last n_q positions), k[l] bf16 [B, Hkv, L, d].  Returns {"h": fp32 [n_layers] (nats),
+    "rows": fp32 [n_layers, B, Hq, n_q], "status": int32 [1] (nonzero: a row was not finite)}.
+    Outputs are valid after the stream is synchronised."""
+    import torch
+    n = len(q)
+    assert n == len(k) and n >= 1
+    B, Hq, n_q, d = q[0].shape
+    Hkv, L = k[0].shape[1], k[0].shape[2]
+    dev = k[0].device
+    rows = torch.empty((n, B, Hq, n_q), dtype=torch.float32, device=dev)
+    h = torch.empty((n,), dtype=torch.float32, device=dev)
+    status = torch.empty((1,), dtype=torch.int32, device=dev)
+    shape = _abi.Shape(B, L, Hq, Hkv, d)
+    nbytes = C.c_size_t()
+    check(_abi.lib().rkv_entropy_workspace_size(C.byref(shape), n, n_q, C.byref(nbytes)))
+    ws = torch.empty((max(nbytes.value, 8) + 7) // 8, dtype=torch.float64, device=dev)
+    check(_abi.lib().rkv_entropy_profile(C.byref(shape), n, n_q, _parr([_ptr(t) for t in q]),
+                                         _parr([_ptr(t) for t in k]), C.c_void_p(rows.data_ptr()),
+                                         C.c_void_p(h.data_ptr()), C.c_void_p(status.data_ptr()),
+                                         C.c_void_p(ws.data_ptr()), ws.numel() * 8,
+                                         C.c_void_p(_stream_handle(stream, dev))))
+    return {"h": h, "rows": rows, "status": status, "workspace": ws}
+
+
+def entropy_budgets(h, total: int, b_min: int = 32):
+    """Entropy allocation: per-layer capacities from H_l by Eq. 3 with the identity transform."""
+    return allocate_budgets([float(x) for x in h], total, b_min, T_IDENTITY)
 
 
 def decode_step(plan: Plan, state, q, k, v, position: int, *, victim_out=None, stream=None):

@@ -19,7 +19,8 @@ EXPORTED = [
     "rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_destroy", "rkv_plan_num_layers",
     "rkv_plan_serialize", "rkv_plan_deserialize",
     "rkv_plan_retained_counts", "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check",
-    "rkv_decode_step", "rkv_profile_enable", "rkv_profile_read", "rkv_last_error", "rkv_version",
+    "rkv_decode_step", "rkv_entropy_workspace_size", "rkv_entropy_profile", "rkv_profile_enable", "rkv_profile_read", "rkv_last_error",
+    "rkv_version",
 ]
 
 
@@ -80,6 +81,10 @@ def lib():
         L.rkv_prefill_check.argtypes = [C.c_void_p, C.c_size_t, C.POINTER(C.c_int32)]
         L.rkv_decode_step.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(DecodeState), C.POINTER(DecodeInput),
                                       C.c_int32, C.c_void_p]
+        L.rkv_entropy_workspace_size.argtypes = [C.POINTER(Shape), C.c_int32, C.c_int32, C.POINTER(C.c_size_t)]
+        L.rkv_entropy_profile.argtypes = [C.POINTER(Shape), C.c_int32, C.c_int32, C.POINTER(C.c_void_p),
+                                          C.POINTER(C.c_void_p), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                          C.c_size_t, C.c_void_p]
         L.rkv_profile_enable.argtypes = [C.c_int32]
         L.rkv_profile_read.argtypes = [C.POINTER(C.c_int32), C.POINTER(C.c_double)]
         L.rkv_last_error.restype = C.c_char_p
@@ -88,6 +93,7 @@ def lib():
         for name in ("rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_num_layers", "rkv_plan_retained_counts",
                      "rkv_plan_serialize", "rkv_plan_deserialize",
                      "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check", "rkv_decode_step",
+                     "rkv_entropy_workspace_size", "rkv_entropy_profile",
                      "rkv_profile_enable", "rkv_profile_read", "rkv_version"):
             getattr(L, name).restype = C.c_int
         _lib = L

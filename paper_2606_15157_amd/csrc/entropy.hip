@@ -1,0 +1,259 @@
+// Attention-entropy layer score for capacity allocation (Section 3.3) on gfx950.
+//
+// H_l is the mean, over sequences, query heads and profiled query positions, of the Shannon
+// entropy (nats) of each query's causal attention row: the softmax of q_t . k_j / sqrt(d) over
+// keys j = 0..t, query head hq reading KV head hq / G.
+//
+// entropy_rows_kernel: one workgroup per (layer, sequence, KV head, block of 32 query
+// positions), one wave per query head of the group.  The wave's query fragments stay in
+// registers; the K tiles of 128 keys stream through LDS (prefetched into registers one tile
+// ahead) and the logits come from 16x16x32 bf16 MFMA, accumulator started at minus a per-row
+// reference c_t = max(logit with key t, logit with key 0) (both true logits of the row), so
+// e = exp2(x) with x = (z - c) log2(e) / sqrt(d) stays finite unless a key beats the reference
+// by more than ~88 natural-log units.  Per row the lane keeps Z = sum e and T = sum e x over its
+// keys; the 16 lanes of a row meet once at the end, and
+//   H = -sum p ln p = ln 2 (log2 Z - T / Z).
+// A non-finite row is written as it is and reported by the averaging kernel.
+// Each workgroup also leaves the double-precision sum of its rows; entropy_mean_kernel (one
+// workgroup per layer) adds those in a fixed order.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include "rkv_internal.h"
+
+namespace rkv {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kEntRows = 32;    // query positions per workgroup (two 16-row MFMA sub-tiles)
+constexpr float kMasked = -1e30f;   // exponent of a key a row does not see: exp2 gives 0, 0 * x = 0
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float x) {
+  return x + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+
+template <int G>
+__global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(const EntropyLaunch E) {
+  constexpr int NW = G > 4 ? G : 4;   // at least four waves share the K tile loads
+  constexpr int NT = 64 * NW;
+  constexpr int PER = kSlice * kHeadDim / 8 / NT;   // 16-byte K chunks per thread per tile
+  __shared__ __attribute__((aligned(16))) uint16_t sK[kSlice * kHeadDim];
+  __shared__ float sC[NW][kEntRows];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, lg = lane >> 4, l16 = lane & 15;
+  const int L = E.seq_len, n_q = E.n_q, Hq = E.n_q_heads, Hkv = E.n_kv_heads;
+  const int nqb = (n_q + kEntRows - 1) / kEntRows;
+  int item = blockIdx.x;
+  const int qb = item % nqb;
+  item /= nqb;
+  const int h = item % Hkv;
+  item /= Hkv;
+  const int b = item % E.batch;
+  const int layer = item / E.batch;
+  const bool compute = wv < G;          // wave-uniform: one wave per query head of the group
+  const int hq = h * G + (compute ? wv : 0);
+  const int i0 = qb * kEntRows;            // first profiled query index of the block
+  const int t0 = L - n_q + i0;             // its position
+  const uint16_t* qrows = E.q[layer] + (size_t)(b * Hq + hq) * n_q * kHeadDim;
+  const uint16_t* khead = E.k[layer] + (size_t)(b * Hkv + h) * L * kHeadDim;
+  if (blockIdx.x == 0 && tid == 0) E.status[0] = 0u;
+
+  // ---- per-row reference: lanes 0..31 of each wave take one row each
+  if (compute && lane < kEntRows) {
+    const int i = i0 + lane;
+    float zd = 0.f, zs = 0.f;
+    if (i < n_q) {
+      const int t = L - n_q + i;
+      const u32x4* qp = reinterpret_cast<const u32x4*>(qrows + (size_t)i * kHeadDim);
+      const u32x4* kd = reinterpret_cast<const u32x4*>(khead + (size_t)t * kHeadDim);
+      const u32x4* ks = reinterpret_cast<const u32x4*>(khead);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const u32x4 qa = qp[c], da = kd[c], sa = ks[c];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float q0 = __uint_as_float(qa[u] << 16), q1 = __uint_as_float(qa[u] & 0xffff0000u);
+          zd = fmaf(q0, __uint_as_float(da[u] << 16), zd);
+          zd = fmaf(q1, __uint_as_float(da[u] & 0xffff0000u), zd);
+          zs = fmaf(q0, __uint_as_float(sa[u] << 16), zs);
+          zs = fmaf(q1, __uint_as_float(sa[u] & 0xffff0000u), zs);
+        }
+      }
+    }
+    sC[wv][lane] = fmaxf(zd, zs);
+  }
+  // ---- query fragments (A operand): row 16 rs + l16, k-chunk 4 st + lg
+  bf16x8 qa[2][4];
+#pragma unroll
+  for (int rs = 0; rs < 2; ++rs) {
+    const int i = i0 + 16 * rs + l16;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (i < n_q) v = *reinterpret_cast<const u32x4*>(qrows + (size_t)i * kHeadDim + 8 * (4 * st + lg));
+      qa[rs][st] = as_bf16x8(v);
+    }
+  }
+  // ---- K tiles: keys [0, t_last] where t_last is the block's last valid position
+  const int t_last = L - n_q + min(i0 + kEntRows, n_q) - 1;
+  const int n_tiles = t_last / kSlice + 1;
+  u32x4 pre[PER];
+  auto fetch = [&](int kt) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
+      const int kk = min(kt * kSlice + key, L - 1);   // keys past the prompt are masked below
+      pre[u] = *reinterpret_cast<const u32x4*>(khead + (size_t)kk * kHeadDim + 8 * ch);
+    }
+  };
+  fetch(0);
+  __syncthreads();   // sC written
+  float cref[2][4];
+#pragma unroll
+  for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cref[rs][i] = sC[wv][16 * rs + 4 * lg + i];
+  const float sl2 = E.scale_log2;
+  float Z[2][4], T[2][4];
+#pragma unroll
+  for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      Z[rs][i] = 0.f;
+      T[rs][i] = 0.f;
+    }
+
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    __syncthreads();   // every wave is done with the previous tile
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
+      *reinterpret_cast<u32x4*>(&sK[(key * 16 + (ch ^ (key & 15))) * 8]) = pre[u];
+    }
+    __syncthreads();
+    if (kt + 1 < n_tiles) fetch(kt + 1);
+    if (!compute) continue;
+    const int k0 = kt * kSlice;
+    f32x4 acc[2][8];
+#pragma unroll
+    for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[rs][ks][i] = -cref[rs][i];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const int key = 16 * ks + l16, ch = 4 * st + lg;
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[(key * 16 + (ch ^ (key & 15))) * 8]);
+        acc[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], kf, acc[0][ks], 0, 0, 0);
+        acc[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], kf, acc[1][ks], 0, 0, 0);
+      }
+      // one k-step's fragments live at a time
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // keys past a row's position (and past the prompt) take no part; only the last tiles need it
+    const bool edge = k0 + kSlice - 1 > t0;
+#pragma unroll
+    for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float x = acc[rs][ks][i] * sl2;
+          if (edge) {
+            const int key = k0 + 16 * ks + l16;
+            const int ir = i0 + 16 * rs + 4 * lg + i;
+            const int t = L - n_q + ir;
+            if (key > t || ir >= n_q) x = kMasked;
+          }
+          const float e = __builtin_amdgcn_exp2f(x);
+          Z[rs][i] += e;
+          T[rs][i] = fmaf(e, x, T[rs][i]);
+        }
+  }
+  // ---- the 16 lanes of each row (one DPP row) add up; lane l16 == 0 writes the entropy and
+  // adds it to the workgroup's partial sum (fixed order: lanes, then waves)
+  double part = 0.0;
+#pragma unroll
+  for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float z = Z[rs][i], tt = T[rs][i];
+      z = dpp_add<0x128>(z);   // row_ror:8
+      z = dpp_add<0x124>(z);   // row_ror:4
+      z = dpp_add<0x122>(z);   // row_ror:2
+      z = dpp_add<0x121>(z);   // row_ror:1
+      tt = dpp_add<0x128>(tt);
+      tt = dpp_add<0x124>(tt);
+      tt = dpp_add<0x122>(tt);
+      tt = dpp_add<0x121>(tt);
+      const int ir = i0 + 16 * rs + 4 * lg + i;
+      if (compute && l16 == 0 && ir < n_q) {
+        const float H = 0.6931471805599453f * (__builtin_log2f(z) - tt / z);
+        E.rows[((size_t)(layer * E.batch + b) * Hq + hq) * n_q + ir] = H;
+        part += (double)H;
+      }
+    }
+  __shared__ double sPart[NW];
+#pragma unroll
+  for (int o = 16; o < 64; o <<= 1) part += __shfl_xor(part, o);   // lanes 0, 16, 32, 48
+  if (lane == 0) sPart[wv] = part;
+  __syncthreads();
+  if (tid == 0) {
+    double t = 0.0;
+    for (int w = 0; w < G; ++w) t += sPart[w];
+    E.partial[blockIdx.x] = t;   // blocks of one layer are consecutive
+  }
+}
+
+__global__ __launch_bounds__(256) void entropy_mean_kernel(const EntropyLaunch E) {
+  __shared__ double sSum[256];
+  __shared__ int sBad;
+  const int tid = threadIdx.x, layer = blockIdx.x;
+  const size_t n = (size_t)E.batch * E.n_q_heads * E.n_q;
+  const int nb = E.batch * E.n_kv_heads * ((E.n_q + kEntRows - 1) / kEntRows);   // row blocks per layer
+  const double* part = E.partial + (size_t)layer * nb;
+  if (tid == 0) sBad = 0;
+  __syncthreads();
+  double s = 0.0;
+  for (int r = tid; r < nb; r += 256) s += part[r];
+  // a non-finite row makes its block's partial sum non-finite
+  if (!(fabs(s) < __builtin_inf())) sBad = 1;
+  sSum[tid] = s;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) {
+    if (tid < o) sSum[tid] += sSum[tid + o];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    E.h[layer] = (float)(sSum[0] / (double)n);
+    if (sBad) atomicOr(E.status, 1u);
+  }
+}
+
+}  // namespace
+
+int launch_entropy(const EntropyLaunch& E, void* stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int G = E.n_q_heads / E.n_kv_heads;
+  const unsigned grid = (unsigned)(E.n_layers * E.batch * E.n_kv_heads * ((E.n_q + kEntRows - 1) / kEntRows));
+  switch (G) {
+    case 1: entropy_rows_kernel<1><<<grid, 256, 0, st>>>(E); break;
+    case 2: entropy_rows_kernel<2><<<grid, 256, 0, st>>>(E); break;
+    case 4: entropy_rows_kernel<4><<<grid, 256, 0, st>>>(E); break;
+    case 8: entropy_rows_kernel<8><<<grid, 512, 0, st>>>(E); break;
+    default: return (int)hipErrorInvalidValue;
+  }
+  entropy_mean_kernel<<<E.n_layers, 256, 0, st>>>(E);
+  return (int)hipGetLastError();
+}
+
+}  // namespace rkv

@@ -543,6 +543,67 @@ int rkv_prefill_check(const void* ws, size_t ws_bytes, int32_t* status_out) {
   return RKV_OK;
 }
 
+namespace {
+size_t entropy_blocks_per_layer(const rkv_shape* s, int32_t n_q) {
+  return (size_t)s->batch * s->n_kv_heads * (size_t)((n_q + 31) / 32);
+}
+}  // namespace
+
+int rkv_entropy_workspace_size(const rkv_shape* shape, int32_t n_layers, int32_t n_q, size_t* bytes) {
+  rkv::clear_error();
+  if (!bytes) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (n_layers < 1) return rkv::fail(RKV_ERR_INVALID_ARG, "n_layers must be >= 1");
+  int st = validate_shape(shape);
+  if (st) return st;
+  if (n_q < 1 || n_q > shape->seq_len) return rkv::fail(RKV_ERR_INVALID_ARG, "n_q must lie in [1, seq_len]");
+  *bytes = sizeof(double) * (size_t)n_layers * entropy_blocks_per_layer(shape, n_q);
+  return RKV_OK;
+}
+
+int rkv_entropy_profile(const rkv_shape* shape, int32_t n_layers, int32_t n_q, const void* const* q,
+                        const void* const* k, float* rows_out, float* h_out, uint32_t* status, void* ws,
+                        size_t ws_bytes, void* stream) {
+  rkv::clear_error();
+  if (!shape || !q || !k || !rows_out || !h_out || !status) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  size_t need = 0;
+  int st0 = rkv_entropy_workspace_size(shape, n_layers, n_q, &need);
+  if (st0) return st0;
+  if (!ws || ws_bytes < need || ((uintptr_t)ws & 7))
+    return rkv::fail(RKV_ERR_WORKSPACE, "entropy workspace missing, too small or not 8-byte aligned");
+  if (n_layers < 1) return rkv::fail(RKV_ERR_INVALID_ARG, "n_layers must be >= 1");
+  int st = validate_shape(shape);
+  if (st) return st;
+  const int L = shape->seq_len;
+  if (n_q < 1 || n_q > L) return rkv::fail(RKV_ERR_INVALID_ARG, "n_q must lie in [1, seq_len]");
+  const int G = shape->n_q_heads / shape->n_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return rkv::fail(RKV_ERR_UNSUPPORTED, "entropy profile needs n_q_heads / n_kv_heads in {1, 2, 4, 8}");
+  const size_t per_layer = (size_t)shape->batch * shape->n_q_heads * n_q;
+  for (int l0 = 0; l0 < n_layers; l0 += rkv::kMaxLayersPerLaunch) {
+    rkv::EntropyLaunch E;
+    std::memset(&E, 0, sizeof(E));
+    E.n_layers = std::min(n_layers - l0, rkv::kMaxLayersPerLaunch);
+    for (int i = 0; i < E.n_layers; ++i) {
+      if (!q[l0 + i] || !k[l0 + i]) return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l0 + i) + ": null q or k");
+      E.q[i] = (const uint16_t*)q[l0 + i];
+      E.k[i] = (const uint16_t*)k[l0 + i];
+    }
+    E.batch = shape->batch;
+    E.seq_len = L;
+    E.n_q_heads = shape->n_q_heads;
+    E.n_kv_heads = shape->n_kv_heads;
+    E.n_q = n_q;
+    E.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
+    E.rows = rows_out + (size_t)l0 * per_layer;
+    E.h = h_out + l0;
+    E.status = status;
+    E.partial = static_cast<double*>(ws) + (size_t)l0 * entropy_blocks_per_layer(shape, n_q);
+    int err = rkv::launch_entropy(E, stream);
+    if (err) return rkv::fail(RKV_ERR_HIP, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)err));
+  }
+  return RKV_OK;
+}
+
 int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_decode_state* state,
                     const rkv_decode_input* input, int32_t position, void* stream) {
   rkv::clear_error();

@@ -103,6 +103,20 @@ static_assert(sizeof(DecodeLaunch) <= 4000, "kernel argument block too large");
 
 int launch_decode(const DecodeLaunch& D, int max_capacity, void* stream);
 
+// Attention-entropy layer score (entropy.hip): up to kMaxLayersPerLaunch layers per launch.
+struct EntropyLaunch {
+  const uint16_t* q[kMaxLayersPerLaunch];   // [B, Hq, n_q, d]: positions L - n_q .. L - 1
+  const uint16_t* k[kMaxLayersPerLaunch];   // [B, Hkv, L, d]
+  int32_t n_layers, batch, seq_len, n_q_heads, n_kv_heads, n_q;
+  float scale_log2;
+  float* rows;        // [n_layers, B, Hq, n_q] row entropies (nats)
+  float* h;           // [n_layers] mean row entropy
+  double* partial;    // [n_layers, B * Hkv * ceil(n_q / 32)] per-workgroup sums of row entropies
+  uint32_t* status;   // 0, or 1 if some row entropy is not finite
+};
+
+int launch_entropy(const EntropyLaunch& E, void* stream);
+
 // Stage timing with HIP events (enabled through rkv_profile_enable).
 enum Stage { kStageZero = 0, kStageScore = 1, kStageSelect = 2, kStageGather = 3, kStageDecode = 4 };
 void profile_mark(int stage, bool end, void* stream);

@@ -216,3 +216,21 @@ def test_plan_serialization_round_trip_and_rejects_damage():
     assert L.rkv_plan_serialize(plan.handle, None, 0, C.byref(size)) == 0 and size.value == len(blob)
     buf = C.create_string_buffer(16)
     assert L.rkv_plan_serialize(plan.handle, buf, 16, C.byref(size)) == 1
+
+
+def test_entropy_profile_argument_errors():
+    L = _abi.lib()
+    sh = _abi.Shape(1, 256, 32, 8, 128)
+    size = C.c_size_t()
+    assert L.rkv_entropy_workspace_size(C.byref(sh), 2, 64, C.byref(size)) == 0
+    assert size.value == 8 * 2 * 1 * 8 * 2          # doubles x layers x B x Hkv x query blocks
+    assert L.rkv_entropy_workspace_size(C.byref(sh), 2, 300, C.byref(size)) == 1   # n_q > L
+    assert L.rkv_entropy_workspace_size(C.byref(sh), 0, 64, C.byref(size)) == 1    # no layers
+    fake = rkv._parr([FAKE, FAKE])
+    args = (C.byref(sh), 2, 64, fake, fake, C.c_void_p(FAKE), C.c_void_p(FAKE), C.c_void_p(FAKE))
+    assert L.rkv_entropy_profile(*args, None, 0, None) == 5                          # no workspace
+    assert L.rkv_entropy_profile(*args, C.c_void_p(FAKE), 16, None) == 5             # too small
+    sh3 = _abi.Shape(1, 256, 24, 8, 128)                                             # G = 3
+    assert L.rkv_entropy_workspace_size(C.byref(sh3), 2, 64, C.byref(size)) == 0
+    assert L.rkv_entropy_profile(C.byref(sh3), 2, 64, fake, fake, C.c_void_p(FAKE), C.c_void_p(FAKE),
+                                 C.c_void_p(FAKE), C.c_void_p(FAKE), 1 << 20, None) == 4
