@@ -25,6 +25,10 @@ Readings taken where the paper is silent:
   * H2O prefill: the same window sum with no pooling, group mean; r = floor(b *
     num / den) most recent positions kept (num/den = 1/2 by default) and the
     top-(b-r) of [0, L-r);
+  * H2O with full-span accumulation (H2O_FULL): the same with every prompt
+    position as a query (the window is the whole prompt, so q holds L rows):
+    S[j] is the group mean of the attention key j receives from all queries
+    t >= j, H2O's accumulated attention over the prompt; same selection as H2O;
   * StreamingLLM: s0 = min(n_sink, b) first positions and the b-s0 last;
   * any rule with b >= L keeps all L positions;
   * top-k order: value descending, then position ascending; the selection is
@@ -37,7 +41,9 @@ import numpy as np
 
 FULL, STREAMING, SNAPKV, H2O = 0, 1, 2, 3
 TOVA = 4   # a decode rule only (oracle.decode.tova_step)
-RULE_NAMES = {FULL: "full", STREAMING: "streaming", SNAPKV: "snapkv", H2O: "h2o", TOVA: "tova"}
+H2O_FULL = 5
+RULE_NAMES = {FULL: "full", STREAMING: "streaming", SNAPKV: "snapkv", H2O: "h2o", TOVA: "tova",
+              H2O_FULL: "h2o_full"}
 
 
 def bf16_to_f64(bits) -> np.ndarray:
@@ -127,7 +133,7 @@ def rule_layout(rule: int, b: int, L: int, w: int, n_sink: int = 4, num: int = 1
         if b <= w:
             return (0, 0, L - b, L)
         return (L - w, b - w, L - w, L)
-    if rule == H2O:
+    if rule in (H2O, H2O_FULL):
         r = h2o_recent(b, num, den)
         return (L - r, b - r, L - r, L)
     raise ValueError("unknown rule")
@@ -137,7 +143,8 @@ def evict_layer(rule: int, b: int, q_bits, k_bits, v_bits, *, window: int, pool_
                 n_sink: int = 4, recent_num: int = 1, recent_den: int = 2):
     """Prompt compression of one (sequence, layer).
 
-    q_bits [Hq, w, d], k_bits / v_bits [Hkv, L, d] as bf16 bit patterns (uint16).
+    q_bits [Hq, w, d] ([Hq, L, d] for H2O_FULL: every position's query), k_bits / v_bits
+    [Hkv, L, d] as bf16 bit patterns (uint16).
     Returns dict:
       idx    [Hkv, b_eff] int64, ascending retained positions
       k_out, v_out [Hkv, b_eff, d] uint16 (bit copies of the retained rows)
@@ -153,7 +160,9 @@ def evict_layer(rule: int, b: int, q_bits, k_bits, v_bits, *, window: int, pool_
         raise ValueError("window must be in [1, L]")
     b_eff = L if rule == FULL else min(b, L)
     layout = rule_layout(rule, b, L, w, n_sink, recent_num, recent_den)
-    scored = rule in (SNAPKV, H2O)
+    scored = rule in (SNAPKV, H2O, H2O_FULL)
+    if rule == H2O_FULL and np.asarray(q_bits).shape[1] != L:
+        raise ValueError("H2O_FULL takes the queries of all L positions")
 
     A = None
     if scored:

@@ -284,3 +284,50 @@ def test_planted_structure_is_found_on_the_single_layer_workload():
         kept = set(out["idx"][h].tolist())
         assert 0 in kept
         assert len(kept & set(x["hh"][h].tolist())) >= 12
+
+
+# ----------------------------------------------------------------------------- H2O, full span
+
+def test_full_span_uniform_keys_harmonic_and_total():
+    """H2O_FULL with equal keys: query t spreads 1/(t+1) over keys 0..t, so key j receives
+    H_L - H_j; the scores of a head total L (one unit per query)."""
+    L, d = 40, 4
+    rng = np.random.default_rng(3)
+    q = bits(rng.standard_normal((8, L, d)))
+    k = bits(np.tile(rng.standard_normal(d), (2, L, 1)))
+    v = bits(rng.standard_normal((2, L, d)))
+    out = P.evict_layer(P.H2O_FULL, 10, q, k, v, window=1)
+    expect = np.array([harmonic(L) - harmonic(j) for j in range(L)])
+    r = P.h2o_recent(10, 1, 2)
+    np.testing.assert_allclose(out["scores"], np.tile(expect[:L - r], (2, 1)), rtol=1e-12)
+    full = P.evict_layer(P.H2O_FULL, L, q, k, v, window=1)
+    np.testing.assert_allclose(full["scores"].sum(axis=1), L, rtol=1e-12)
+
+
+def test_full_span_brute_force_and_h2o_selection():
+    """Explicit loops over queries and keys (math.exp, no oracle helper) against the oracle's
+    full-span scores, and the selection: r recent plus the top-(b-r) of [0, L-r)."""
+    L, d, Hq, Hkv, b = 12, 4, 4, 2, 7
+    rng = np.random.default_rng(4)
+    q = bits(1.5 * rng.standard_normal((Hq, L, d)))
+    k = bits(rng.standard_normal((Hkv, L, d)))
+    v = bits(rng.standard_normal((Hkv, L, d)))
+    out = P.evict_layer(P.H2O_FULL, b, q, k, v, window=1)
+    qf, kf = P.bf16_to_f64(q), P.bf16_to_f64(k)
+    G = Hq // Hkv
+    S = np.zeros((Hkv, L))
+    for hq in range(Hq):
+        for t in range(L):
+            logits = [sum(qf[hq, t, c] * kf[hq // G, j, c] for c in range(d)) / math.sqrt(d) for j in range(t + 1)]
+            m = max(logits)
+            ex = [math.exp(x - m) for x in logits]
+            tot = sum(ex)
+            for j in range(t + 1):
+                S[hq // G, j] += ex[j] / tot / G
+    r = b // 2
+    np.testing.assert_allclose(out["scores"], S[:, :L - r], rtol=1e-12)
+    for h in range(Hkv):
+        order = sorted(range(L - r), key=lambda j: (-np.float32(S[h, j]), j))[:b - r]
+        assert out["idx"][h].tolist() == sorted(order) + list(range(L - r, L))
+    with pytest.raises(ValueError):
+        P.evict_layer(P.H2O_FULL, b, q[:, :5], k, v, window=5)   # needs every position's query
