@@ -159,6 +159,48 @@ def entropy_measure(dev, reps=3, n_layers=32, L=4096):
             "mfma_frac": tflops / 2500.0, "exps_per_s": n_layers * HQ * (L * (L + 1) // 2) / (ms * 1e-3)}
 
 
+def fullspan_measure(dev, reps=3):
+    """The 8K route with its H2O layers (16-27) accumulating over every prompt query instead of
+    the window (their queries: all 8192 positions).  Same budgets; random bf16 inputs.  The
+    full-span layers dominate: two passes over the causal logits each,
+    2 x sum_t (t + 1) x 2 d flop per query head."""
+    import torch
+    import paper_2606_15157_amd as rkv
+    from synth.workloads import mixed_route, pyramid_weights
+    rules = [rkv.H2O_FULL if r == rkv.H2O else r for r in mixed_route(N_LAYERS)]
+    budgets = rkv.allocate_budgets(pyramid_weights(N_LAYERS), N_LAYERS * AVG_BUDGET, B_MIN)
+    g = torch.Generator(device=dev).manual_seed(20260617)
+    q = [torch.randn((1, HQ, L_CTX if r == rkv.H2O_FULL else W, D), generator=g, device=dev, dtype=torch.bfloat16)
+         for r in rules]
+    k = [torch.randn((1, HKV, L_CTX, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in rules]
+    v = [torch.randn((1, HKV, L_CTX, D), generator=g, device=dev, dtype=torch.bfloat16) for _ in rules]
+    plan = rkv.Plan(rules, budgets, window=W, pool_kernel=POOL)
+    out = rkv.alloc_outputs(plan, 1, HKV, L_CTX, D, dev)
+    ws = rkv.alloc_workspace(plan, 1, L_CTX, HQ, HKV, dev)
+    call = rkv.PreparedPrefill(plan, q, k, v, out, ws)
+    stream = torch.cuda.current_stream(dev)
+    call(stream)
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        call(stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    if rkv.prefill_check(ws) != 0:
+        raise RuntimeError("full-span pass reported a failure")
+    ms = e0.elapsed_time(e1) / reps
+    n_full = sum(1 for r in rules if r == rkv.H2O_FULL)
+    flop = n_full * HQ * (L_CTX * (L_CTX + 1) // 2) * D * 2 * 2
+    log(f"full-span route: {ms:.3f} ms per pass ({flop / (ms * 1e-3) / 1e12:.0f} TFLOP/s on the full-span logits)")
+    del q, k, v, out, ws, call
+    torch.cuda.empty_cache()
+    return {"workload": "32-layer mixed route at L=8192 with H2O layers 16-27 accumulating over all 8192 queries",
+            "ms_per_pass": ms, "full_span_flop": flop, "achieved_TFLOPs": flop / (ms * 1e-3) / 1e12,
+            "peak_TFLOPs": 2500.0, "layer_tokens_per_s": N_LAYERS * L_CTX / (ms * 1e-3)}
+
+
 def kernel_source_hash():
     return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
 
@@ -183,6 +225,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
     ap.add_argument("--no-entropy", action="store_true", help="skip the entropy-profile measurement")
+    ap.add_argument("--no-fullspan", action="store_true", help="skip the full-span H2O route measurement")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (outside the timed region) so a "
                          "rocprofv3 --pmc run of this command can scale FETCH_SIZE / WRITE_SIZE")
@@ -316,6 +359,8 @@ def main():
         rec["decode"] = decode_measure(dev)
     if not args.no_entropy:
         rec["entropy"] = entropy_measure(dev)
+    if not args.no_fullspan:
+        rec["h2o_full_span"] = fullspan_measure(dev)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         rec["cpu_baseline"] = cpu_baseline(xs, rules, budgets, args.cpu_seconds)

@@ -52,7 +52,7 @@ typedef enum {
 } rkv_status;
 
 /* Operators (Section 2.1 rule families; Section 3.1 r_{l,phi} values). */
-typedef enum { RKV_FULL = 0, RKV_STREAMING = 1, RKV_SNAPKV = 2, RKV_H2O = 3, RKV_TOVA = 4 } rkv_rule;
+typedef enum { RKV_FULL = 0, RKV_STREAMING = 1, RKV_SNAPKV = 2, RKV_H2O = 3, RKV_TOVA = 4, RKV_H2O_FULL = 5 } rkv_rule;
 typedef enum { RKV_PHASE_PREFILL = 0, RKV_PHASE_DECODE = 1 } rkv_phase;
 /* Score transforms T of Section 3.3: identity (attention entropy) or a cap at the
  * across-layer 95th percentile (PPL degradation). */
@@ -83,8 +83,9 @@ typedef struct {
 typedef struct rkv_plan rkv_plan;
 
 /* Per-layer device pointers of one prefill call (host arrays of n_layers pointers).
- *  q_win[l]     bf16 [B, Hq, w, d]   queries of positions L-w..L-1 (post-RoPE); may be NULL
- *               for layers whose prefill operator does not score (FULL, STREAMING).
+ *  q_win[l]     bf16 [B, Hq, w, d]   queries of positions L-w..L-1 (post-RoPE); [B, Hq, L, d],
+ *               every position, for an H2O_FULL layer; may be NULL for layers whose prefill
+ *               operator does not score (FULL, STREAMING).
  *  k[l], v[l]   bf16 [B, Hkv, L, d]  the prompt's keys and values.
  *  k_out[l], v_out[l]  bf16 [B, Hkv, n_l, d]  compacted cache, n_l = retained count
  *               (rkv_plan_retained_counts); row m holds position idx_out[l][..., m].
@@ -141,7 +142,7 @@ int rkv_allocate_budgets(const double* scores, int32_t n_layers, int32_t transfo
                          int32_t b_min, int32_t* budgets_out);
 
 /* Section 3.1 (Eq. 1) and 3.4: validate and freeze a plan.  Host only.
- * Operators valid in prefill: FULL, STREAMING, SNAPKV, H2O.  In decode: FULL, STREAMING, H2O,
+ * Operators valid in prefill: FULL, STREAMING, SNAPKV, H2O, H2O_FULL.  In decode: FULL, STREAMING, H2O,
  * TOVA (SNAPKV compresses the prompt only; TOVA, eviction by the current query's attention, is
  * a decode operator here, as in the paper's matched study -> RKV_ERR_PLAN otherwise).  Budgets
  * must be >= 0 (>= 2 for a decode H2O layer, >= 1 for decode STREAMING and TOVA); window >= 1,
@@ -177,6 +178,9 @@ int rkv_prefill_workspace_size(const rkv_plan* plan, const rkv_shape* shape, siz
  *             keep top-(b-w) of S plus the window [L-w, L) (b <= w: the last b positions);
  *   H2O:      S[h,j] = mean_g A[hG+g, j]; r = floor(b*num/den);
  *             keep top-(b-r) of S over [0, L-r) plus [L-r, L);
+ *   H2O_FULL: H2O whose accumulation spans every prompt query (q_win[l] then holds all L
+ *             positions, bf16 [B, Hq, L, d]): S[h,j] = mean_g sum_{t>=j} softmax_j(Q[hG+g,t] .
+ *             K[h,.] / sqrt(d)) over keys <= t; the same selection as H2O;
  *   STREAMING: keep [0, min(n_sink,b)) plus the last b - min(n_sink,b) positions;
  *   FULL, or b >= L: keep everything.
  * Top-k order is (score descending, position ascending) on fp32 scores.  K/V rows are

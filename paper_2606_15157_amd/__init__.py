@@ -13,12 +13,12 @@ import ctypes as C
 from typing import Sequence
 
 from . import _abi
-from ._abi import FULL, STREAMING, SNAPKV, H2O, TOVA, PHASE_PREFILL, PHASE_DECODE, T_IDENTITY, T_PPL_CAP  # noqa: F401
+from ._abi import FULL, STREAMING, SNAPKV, H2O, TOVA, H2O_FULL, PHASE_PREFILL, PHASE_DECODE, T_IDENTITY, T_PPL_CAP  # noqa: F401
 from ._abi import RkvError, check
 
 __all__ = ["Plan", "allocate_budgets", "evict_prefill", "decode_step", "prefill_check", "version",
            "entropy_profile", "entropy_budgets",
-           "FULL", "STREAMING", "SNAPKV", "H2O", "TOVA", "RkvError"]
+           "FULL", "STREAMING", "SNAPKV", "H2O", "TOVA", "H2O_FULL", "RkvError"]
 
 
 def version() -> int:
@@ -142,7 +142,8 @@ def evict_prefill(plan: Plan, q_win, k, v, *, out=None, workspace=None, score_ou
                   stream=None):
     """Compress every layer's prompt cache.
 
-    q_win[l]: bf16 [B, Hq, w, d] (None allowed for FULL / STREAMING layers);
+    q_win[l]: bf16 [B, Hq, w, d] ([B, Hq, L, d] for H2O_FULL layers; None allowed for FULL /
+    STREAMING layers);
     k[l], v[l]: bf16 [B, Hkv, L, d].  Returns dict of per-layer lists: k_out, v_out (bf16
     [B, Hkv, n_l, d]), idx (int32 [B, Hkv, n_l], ascending), and optionally scores (fp32
     [B, Hkv, L]) and acc (fp32 [B, Hkv, n_l]).  Outputs are valid after the stream syncs.
@@ -160,9 +161,10 @@ def evict_prefill(plan: Plan, q_win, k, v, *, out=None, workspace=None, score_ou
     for t in list(k) + list(v):
         if tuple(t.shape) != (B, Hkv, L, d):
             raise ValueError("every k / v must have shape [B, Hkv, L, d]")
-    for q in q_win:
-        if q is not None and tuple(q.shape) != (B, Hq, plan.window, d):
-            raise ValueError("q_win must have shape [B, Hq, w, d]")
+    for q, r in zip(q_win, plan.rules_prefill):
+        rows = L if r == H2O_FULL else plan.window
+        if q is not None and tuple(q.shape) != (B, Hq, rows, d):
+            raise ValueError("q_win must have shape [B, Hq, w, d] ([B, Hq, L, d] for H2O_FULL layers)")
     counts = plan.retained_counts(L)
     if out is None:
         out = {

@@ -11,7 +11,7 @@ RKV_OK = 0
 STATUS_NAMES = {0: "RKV_OK", 1: "RKV_ERR_INVALID_ARG", 2: "RKV_ERR_SHAPE", 3: "RKV_ERR_PLAN",
                 4: "RKV_ERR_UNSUPPORTED", 5: "RKV_ERR_WORKSPACE", 6: "RKV_ERR_HIP", 7: "RKV_ERR_DEVICE"}
 
-FULL, STREAMING, SNAPKV, H2O, TOVA = 0, 1, 2, 3, 4
+FULL, STREAMING, SNAPKV, H2O, TOVA, H2O_FULL = 0, 1, 2, 3, 4, 5
 PHASE_PREFILL, PHASE_DECODE = 0, 1
 T_IDENTITY, T_PPL_CAP = 0, 1
 

@@ -1,0 +1,326 @@
+// H2O prefill with full-span accumulation on gfx950: the score of key j is the group mean of the
+// attention it receives from every prompt query t >= j (H2O's accumulated attention, Section 2.1),
+//   S[h, j] = (1/G) sum_g sum_{t >= j} softmax_j(q[hG+g, t] . k[h, .] / sqrt(d)) over keys <= t.
+// Two passes over the causal logits, no atomics, fixed summation order:
+//
+// fullspan_rows_kernel: one workgroup per (job, 32 query positions), one wave per query head of
+//   the group.  The wave's query fragments stay in registers, 128-key tiles stream through LDS,
+//   bf16 MFMA logits are taken against a fixed per-row reference c_t = max(logit with key t,
+//   logit with key 0); the row's log2 normaliser Lambda_t = c_t log2(e)/sqrt(d) + log2(sum_j
+//   exp2(x_tj - c_t log2(e)/sqrt(d))) goes to the workspace.  A non-finite normaliser (a key
+//   beyond ~88 natural-log units above the reference) sets status bit 1.
+// fullspan_cols_kernel: one workgroup per (job, 128-key block), four waves of 32 keys each; the
+//   wave's key fragments stay in registers, 128-row query tiles (G heads x 128/G positions) at or
+//   after the block stream through LDS with their normalisers, and each lane sums
+//   p = exp2(x - Lambda_t) over its rows; the four lane groups meet once at the end.
+// Jobs here are the full-span ones: job = (slot * B + b) * Hkv + h with slot >= n_window.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+
+#include "rkv_internal.h"
+
+namespace rkv {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kFsRows = 32;          // query positions per row-pass workgroup
+constexpr float kMasked = -1e30f;    // exponent of a hidden key: exp2 gives 0
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float x) {
+  return x + __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
+}
+
+// LDS position of 16-byte chunk `ch` of row `row` of a 128 x 128 bf16 tile (XOR swizzle: the
+// 16 rows a fragment read touches hit distinct banks)
+__device__ __forceinline__ int swz(int row, int ch) { return (row * 16 + (ch ^ (row & 15))) * 8; }
+
+template <int G>
+__global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void fullspan_rows_kernel(const PrefillLaunch P) {
+  constexpr int NW = G > 4 ? G : 4;
+  constexpr int NT = 64 * NW;
+  constexpr int PER = kSlice * kHeadDim / 8 / NT;
+  __shared__ __attribute__((aligned(16))) uint16_t sK[kSlice * kHeadDim];
+  __shared__ float sC[NW][kFsRows];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, lg = lane >> 4, l16 = lane & 15;
+  const int L = P.seq_len, Hq = P.n_q_heads, Hkv = P.n_kv_heads, B = P.batch;
+  const int nqb = (L + kFsRows - 1) / kFsRows;
+  const int jf = blockIdx.x / nqb, qb = blockIdx.x - jf * nqb;
+  const int job = B * Hkv * P.n_window + jf;
+  const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
+  const PrefillLayer& ly = P.layer[slot];
+  const bool compute = wv < G;
+  const int g = compute ? wv : 0, hq = h * G + g;
+  const int t0 = qb * kFsRows;
+  const uint16_t* qrows = ly.q + (size_t)(s * Hq + hq) * L * kHeadDim;
+  const uint16_t* khead = ly.k + (size_t)(s * Hkv + h) * L * kHeadDim;
+  float* lam = P.lamf + ((size_t)jf * G + g) * L;
+
+  if (compute && lane < kFsRows) {
+    const int t = t0 + lane;
+    float zd = 0.f, zs = 0.f;
+    if (t < L) {
+      const u32x4* qp = reinterpret_cast<const u32x4*>(qrows + (size_t)t * kHeadDim);
+      const u32x4* kd = reinterpret_cast<const u32x4*>(khead + (size_t)t * kHeadDim);
+      const u32x4* ks = reinterpret_cast<const u32x4*>(khead);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const u32x4 qa = qp[c], da = kd[c], sa = ks[c];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float q0 = __uint_as_float(qa[u] << 16), q1 = __uint_as_float(qa[u] & 0xffff0000u);
+          zd = fmaf(q0, __uint_as_float(da[u] << 16), zd);
+          zd = fmaf(q1, __uint_as_float(da[u] & 0xffff0000u), zd);
+          zs = fmaf(q0, __uint_as_float(sa[u] << 16), zs);
+          zs = fmaf(q1, __uint_as_float(sa[u] & 0xffff0000u), zs);
+        }
+      }
+    }
+    sC[wv][lane] = fmaxf(zd, zs);
+  }
+  bf16x8 qa[2][4];
+#pragma unroll
+  for (int rs = 0; rs < 2; ++rs) {
+    const int t = t0 + 16 * rs + l16;
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (t < L) v = *reinterpret_cast<const u32x4*>(qrows + (size_t)t * kHeadDim + 8 * (4 * st + lg));
+      qa[rs][st] = as_bf16x8(v);
+    }
+  }
+  const int t_last = min(t0 + kFsRows, L) - 1;
+  const int n_tiles = t_last / kSlice + 1;
+  u32x4 pre[PER];
+  auto fetch = [&](int kt) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
+      const int kk = min(kt * kSlice + key, L - 1);
+      pre[u] = *reinterpret_cast<const u32x4*>(khead + (size_t)kk * kHeadDim + 8 * ch);
+    }
+  };
+  fetch(0);
+  __syncthreads();
+  float cref[2][4], Z[2][4];
+#pragma unroll
+  for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      cref[rs][i] = sC[wv][16 * rs + 4 * lg + i];
+      Z[rs][i] = 0.f;
+    }
+  const float sl2 = P.scale_log2;
+  for (int kt = 0; kt < n_tiles; ++kt) {
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
+      *reinterpret_cast<u32x4*>(&sK[swz(key, ch)]) = pre[u];
+    }
+    __syncthreads();
+    if (kt + 1 < n_tiles) fetch(kt + 1);
+    if (!compute) continue;
+    const int k0 = kt * kSlice;
+    f32x4 acc[2][8];
+#pragma unroll
+    for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[rs][ks][i] = -cref[rs][i];
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[swz(16 * ks + l16, 4 * st + lg)]);
+        acc[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], kf, acc[0][ks], 0, 0, 0);
+        acc[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], kf, acc[1][ks], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const bool edge = k0 + kSlice - 1 > t0;
+#pragma unroll
+    for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float x = acc[rs][ks][i] * sl2;
+          if (edge) {
+            const int key = k0 + 16 * ks + l16, t = t0 + 16 * rs + 4 * lg + i;
+            if (key > t || t >= L) x = kMasked;
+          }
+          Z[rs][i] += __builtin_amdgcn_exp2f(x);
+        }
+  }
+  if (!compute) return;
+#pragma unroll
+  for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float z = Z[rs][i];
+      z = dpp_add<0x128>(z);
+      z = dpp_add<0x124>(z);
+      z = dpp_add<0x122>(z);
+      z = dpp_add<0x121>(z);
+      const int t = t0 + 16 * rs + 4 * lg + i;
+      if (l16 == 0 && t < L) {
+        const float lm = cref[rs][i] * sl2 + __builtin_log2f(z);
+        if (!(z < __builtin_inff())) atomicOr(P.counters, 2u);
+        lam[t] = lm;
+      }
+    }
+}
+
+template <int G>
+__global__ __launch_bounds__(256, 2) void fullspan_cols_kernel(const PrefillLaunch P) {
+  constexpr int NT = 256;
+  constexpr int PT = 128 / G;                      // query positions per 128-row tile
+  constexpr int PER = 128 * kHeadDim / 8 / NT;     // 16-byte chunks of the query tile per thread
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[128 * kHeadDim];
+  __shared__ float sLam[128];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, lg = lane >> 4, l16 = lane & 15;
+  const int L = P.seq_len, Hq = P.n_q_heads, Hkv = P.n_kv_heads, B = P.batch;
+  const int nkb = (L + kSlice - 1) / kSlice;
+  const int jf = blockIdx.x / nkb, kb = blockIdx.x - jf * nkb;
+  const int job = B * Hkv * P.n_window + jf;
+  const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
+  const PrefillLayer& ly = P.layer[slot];
+  const int j0 = kb * kSlice;
+  const uint16_t* khead = ly.k + (size_t)(s * Hkv + h) * L * kHeadDim;
+  const uint16_t* qbase = ly.q + (size_t)(s * Hq + h * G) * L * kHeadDim;   // the group's first head
+  const float* lamj = P.lamf + (size_t)jf * G * L;
+
+  // this wave's 32 keys as B-operand fragments: key j0 + 32 wv + 16 ks + l16, chunk 4 st + lg
+  bf16x8 kf[2][4];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int key = min(j0 + 32 * wv + 16 * ks + l16, L - 1);   // keys past the prompt are unused
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+      kf[ks][st] = as_bf16x8(*reinterpret_cast<const u32x4*>(khead + (size_t)key * kHeadDim + 8 * (4 * st + lg)));
+  }
+  // query tiles: positions [t0, t0 + PT) of every head of the group, from the tile holding j0
+  const int tfirst = (j0 / PT) * PT;
+  const int n_tiles = (L - tfirst + PT - 1) / PT;
+  u32x4 pre[PER];
+  float lpre = 0.f;
+  auto fetch = [&](int it) {
+    const int t0 = tfirst + it * PT;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, row = c >> 4, ch = c & 15;
+      const int gg = row / PT, t = min(t0 + (row - gg * PT), L - 1);
+      pre[u] = *reinterpret_cast<const u32x4*>(qbase + ((size_t)gg * L + t) * kHeadDim + 8 * ch);
+    }
+    if (tid < 128) {
+      const int gg = tid / PT, t = t0 + (tid - gg * PT);
+      lpre = t < L ? lamj[(size_t)gg * L + t] : 0.f;
+    }
+  };
+  fetch(0);
+  const float sl2 = P.scale_log2;
+  float col[2] = {0.f, 0.f};
+  for (int it = 0; it < n_tiles; ++it) {
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, row = c >> 4, ch = c & 15;
+      *reinterpret_cast<u32x4*>(&sQ[swz(row, ch)]) = pre[u];
+    }
+    if (tid < 128) sLam[tid] = lpre;
+    __syncthreads();
+    if (it + 1 < n_tiles) fetch(it + 1);
+    const int t0 = tfirst + it * PT;
+    f32x4 acc[8][2];
+#pragma unroll
+    for (int rs = 0; rs < 8; ++rs)
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) acc[rs][ks] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < 4; ++st) {
+#pragma unroll
+      for (int rs = 0; rs < 8; ++rs) {
+        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(&sQ[swz(16 * rs + l16, 4 * st + lg)]);
+        acc[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[0][st], acc[rs][0], 0, 0, 0);
+        acc[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[1][st], acc[rs][1], 0, 0, 0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    // rows 16 rs + 4 lg + i: head (row / PT), position t0 + row % PT; hidden keys and rows past
+    // the prompt contribute 0
+    const bool edge = t0 < j0 + kSlice - 1 || t0 + PT > L;
+#pragma unroll
+    for (int rs = 0; rs < 8; ++rs) {
+      const f32x4 lm = *reinterpret_cast<const f32x4*>(&sLam[16 * rs + 4 * lg]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          float x = fmaf(acc[rs][ks][i], sl2, -lm[i]);
+          if (edge) {
+            const int row = 16 * rs + 4 * lg + i, t = t0 + row % PT;
+            const int key = j0 + 32 * wv + 16 * ks + l16;
+            if (key > t || t >= L) x = kMasked;
+          }
+          col[ks] += __builtin_amdgcn_exp2f(x);
+        }
+      }
+    }
+  }
+  // sum over the four lane groups (rows 4 lg + i): lanes l, l ^ 32, then l ^ 16
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const auto p0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(col[ks]), __float_as_uint(col[ks]), false, false);
+    float c = __uint_as_float(p0[0]) + __uint_as_float(p0[1]);
+    const auto p1 = __builtin_amdgcn_permlane16_swap(__float_as_uint(c), __float_as_uint(c), false, false);
+    c = __uint_as_float(p1[0]) + __uint_as_float(p1[1]);
+    col[ks] = c;
+  }
+  // lane group ks writes key sub-tile ks
+  if (lg < 2) {
+    const int j = j0 + 32 * wv + 16 * lg + l16;
+    if (j < L) P.S[(size_t)job * L + j] = (lg == 0 ? col[0] : col[1]) * (1.f / (float)G);
+  }
+}
+
+}  // namespace
+
+int launch_fullspan(const PrefillLaunch& P, void* stream) {
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const int n_full = P.batch * (P.n_scored - P.n_window) * P.n_kv_heads;
+  if (n_full <= 0) return 0;
+  const int L = P.seq_len, G = P.group;
+  const unsigned g_rows = (unsigned)(n_full * ((L + kFsRows - 1) / kFsRows));
+  const unsigned g_cols = (unsigned)(n_full * ((L + kSlice - 1) / kSlice));
+  switch (G) {
+    case 1:
+      fullspan_rows_kernel<1><<<g_rows, 256, 0, st>>>(P);
+      fullspan_cols_kernel<1><<<g_cols, 256, 0, st>>>(P);
+      break;
+    case 2:
+      fullspan_rows_kernel<2><<<g_rows, 256, 0, st>>>(P);
+      fullspan_cols_kernel<2><<<g_cols, 256, 0, st>>>(P);
+      break;
+    case 4:
+      fullspan_rows_kernel<4><<<g_rows, 256, 0, st>>>(P);
+      fullspan_cols_kernel<4><<<g_cols, 256, 0, st>>>(P);
+      break;
+    case 8:
+      fullspan_rows_kernel<8><<<g_rows, 512, 0, st>>>(P);
+      fullspan_cols_kernel<8><<<g_cols, 256, 0, st>>>(P);
+      break;
+    default:
+      return (int)hipErrorInvalidValue;
+  }
+  return (int)hipGetLastError();
+}
+
+}  // namespace rkv

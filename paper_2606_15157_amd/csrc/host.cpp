@@ -17,7 +17,7 @@ thread_local std::string g_error;
 
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-bool rule_valid(int32_t r) { return r >= RKV_FULL && r <= RKV_TOVA; }
+bool rule_valid(int32_t r) { return r >= RKV_FULL && r <= RKV_H2O_FULL; }
 constexpr int32_t kPlanMagic = 0x50564b52;   // "RKVP" as little-endian bytes
 constexpr int32_t kPlanFormat = 1;
 
@@ -31,7 +31,7 @@ struct Layout {
 Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L, bool want_scores = true) {
   Layout o{};
   const int32_t b = ly.budget_prefill;
-  o.scored = (ly.rule_prefill == RKV_SNAPKV || ly.rule_prefill == RKV_H2O) ? 1 : 0;
+  o.scored = (ly.rule_prefill == RKV_SNAPKV || ly.rule_prefill == RKV_H2O || ly.rule_prefill == RKV_H2O_FULL) ? 1 : 0;
   if (ly.rule_prefill == RKV_FULL || b >= L) {
     o.n_keep = L; o.all = 1; o.cand_end = 0; o.k_sel = 0; o.forced_lo = 0; o.forced_hi = L;
     if (o.scored && !want_scores) o.scored = 0;
@@ -49,7 +49,8 @@ Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L, bool 
       else { o.cand_end = L - p.window; o.k_sel = b - p.window; o.forced_lo = L - p.window; }
       o.forced_hi = L;
       break;
-    case RKV_H2O: {
+    case RKV_H2O:
+    case RKV_H2O_FULL: {
       int32_t r = (int32_t)(((int64_t)b * p.recent_num) / p.recent_den);
       o.cand_end = L - r; o.k_sel = b - r; o.forced_lo = L - r; o.forced_hi = L;
       break;
@@ -81,7 +82,7 @@ int row_tiles(const rkv_params& p, const rkv_shape* s) {
 int kernel_row_tiles(int nt) { return nt <= 4 ? 4 : 8; }
 
 struct Group {
-  int l0, l1, n_scored;
+  int l0, l1, n_scored, n_full;   // n_full: scored layers with full-span accumulation
 };
 
 // Test hook: RKV_FORCE_TWO_PASS=1 selects the two-pass scoring kernel (normally used for prompts
@@ -107,9 +108,13 @@ std::vector<Group> layer_groups(const rkv_plan* plan, int32_t L) {
   int n = (int)plan->layers.size();
   for (int l0 = 0; l0 < n; l0 += rkv::kMaxLayersPerLaunch) {
     int l1 = std::min(n, l0 + rkv::kMaxLayersPerLaunch);
-    int sc = 0;
-    for (int l = l0; l < l1; ++l) sc += prefill_layout(plan->layers[l], plan->params, L).scored;
-    g.push_back({l0, l1, sc});
+    int sc = 0, nf = 0;
+    for (int l = l0; l < l1; ++l) {
+      const int scd = prefill_layout(plan->layers[l], plan->params, L).scored;
+      sc += scd;
+      nf += scd && plan->layers[l].rule_prefill == RKV_H2O_FULL;
+    }
+    g.push_back({l0, l1, sc, nf});
   }
   return g;
 }
@@ -120,7 +125,8 @@ size_t group_workspace(const rkv_plan* plan, const rkv_shape* s, const Group& g)
   const int nt = kernel_row_tiles(row_tiles(plan->params, s));
   const int n_jobs = s->batch * g.n_scored * s->n_kv_heads;
   const int n_slices = (L + rkv::kSlice - 1) / rkv::kSlice;
-  return rkv::prefill_workspace_layout(n_jobs, n_slices, nt * 32, L, G, plan->params.pool_kernel / 2).total;
+  return rkv::prefill_workspace_layout(n_jobs, n_slices, nt * 32, L, G, plan->params.pool_kernel / 2,
+                                       s->batch * g.n_full * s->n_kv_heads).total;
 }
 
 }  // namespace
@@ -155,7 +161,8 @@ int fail(int status, const std::string& msg) {
 
 void clear_error() { g_error.clear(); }
 
-PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half) {
+PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half,
+                                          int n_full_jobs) {
   PrefillWorkspace w{};
   size_t off = 0;
   w.counters = off;
@@ -166,6 +173,8 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
   off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
   w.ncl = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
+  w.lamf = off;
+  off = round_up(off + sizeof(float) * (size_t)n_full_jobs * group * seq_len, 256);
   w.S = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * seq_len, 256);
   w.Su = off;
@@ -307,6 +316,8 @@ int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params*
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": SnapKV compresses the prompt only, not valid in decode");
     if (ly.rule_prefill == RKV_TOVA)
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": TOVA is a decode operator, not valid in prefill");
+    if (ly.rule_decode == RKV_H2O_FULL)
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": full-span accumulation is a prefill rule (decode uses RKV_H2O)");
     if (ly.rule_decode == RKV_TOVA && ly.budget_decode < 1)
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": decode TOVA needs budget >= 1");
     if (ly.rule_decode == RKV_H2O && ly.budget_decode < 2)
@@ -468,16 +479,21 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     // scoring kernel looks a slot's tensors up with one load)
     int order[rkv::kMaxLayersPerLaunch];
     Layout lays[rkv::kMaxLayersPerLaunch];
+    int n_window = 0;
     {
+      // window-scored layers, then full-span H2O, then the unscored ones
       int n = 0;
-      for (int pass = 0; pass < 2; ++pass)
+      for (int pass = 0; pass < 3; ++pass)
         for (int i = 0; i < P.n_layers; ++i) {
           const int l = g.l0 + i;
           const bool want = (io->score_out && io->score_out[l]) || (io->acc_out && io->acc_out[l]);
           const Layout lo = prefill_layout(plan->layers[l], p, L, want);
-          if ((lo.scored != 0) == (pass == 0)) {
+          const bool full = plan->layers[l].rule_prefill == RKV_H2O_FULL;
+          const int cls = !lo.scored ? 2 : (full ? 1 : 0);
+          if (cls == pass) {
             lays[n] = lo;
             order[n++] = i;
+            n_window += pass == 0;
           }
         }
     }
@@ -509,6 +525,7 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
       if (lo.n_keep > 0) P.gather_layer[n_gather++] = i;
     }
     P.n_scored = slot;
+    P.n_window = n_window;
     P.n_gather = n_gather;
     P.gather_item0[0] = 0;
     for (int i = 0; i < n_gather; ++i) {
@@ -517,12 +534,15 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     }
     P.want_unpooled = want_unpooled ? 1 : 0;
     const int n_jobs = shape->batch * slot * shape->n_kv_heads;
-    rkv::PrefillWorkspace W = rkv::prefill_workspace_layout(n_jobs, P.n_slices, ktiles * 32, L, G, P.pool_half);
+    const int n_full_jobs = shape->batch * (slot - n_window) * shape->n_kv_heads;
+    rkv::PrefillWorkspace W = rkv::prefill_workspace_layout(n_jobs, P.n_slices, ktiles * 32, L, G, P.pool_half,
+                                                            n_full_jobs);
     char* base = (char*)ws;
     P.counters = (uint32_t*)(base + W.counters);
     P.stats = (float*)(base + W.stats);
     P.lam = (float*)(base + W.lam);
     P.ncl = (float*)(base + W.ncl);
+    P.lamf = (float*)(base + W.lamf);
     P.S = (float*)(base + W.S);
     P.Su = (float*)(base + W.Su);
     P.edge = (float*)(base + W.edge);

@@ -560,7 +560,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
   const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
   const int nsl = P.n_slices;
-  const int n_jobs = B * P.n_scored * Hkv;
+  const int n_jobs = B * P.n_window * Hkv;
   const int64_t n_items = (int64_t)n_jobs * nsl;
   const float sl2 = P.scale_log2;
   const float inv_g = 1.f / (float)G;
@@ -878,7 +878,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   const int kt = wv & 3, rh = wv >> 2;
   const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
   const int nsl = P.n_slices;
-  const int n_jobs = B * P.n_scored * Hkv;
+  const int n_jobs = B * P.n_window * Hkv;
   const int64_t n_items = (int64_t)n_jobs * nsl;
   const float sl2 = P.scale_log2;
   const float inv_g = 1.f / (float)G;
@@ -996,7 +996,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   // the partial group / head sum of this row half)
   auto phase_b = [&](const PipeRef& j, f32x4v (&e)[4][2]) {
     // the slot is clamped: phase B also runs, with its results unused, for items past the end
-    const bool snap = P.layer[min(j.slot, P.n_scored - 1)].rule == RKV_SNAPKV;
+    const bool snap = P.layer[min(j.slot, P.n_window - 1)].rule == RKV_SNAPKV;
     f32x4v a4[4];
 #pragma unroll
     for (int rs = 0; rs < 4; ++rs) a4[rs] = *reinterpret_cast<const f32x4v*>(&sAlpha[rh * 64 + rs * 16 + 4 * lg]);
@@ -1264,7 +1264,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
   const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
   const int nsl = P.n_slices;
-  const int n_jobs = B * P.n_scored * Hkv;
+  const int n_jobs = B * P.n_window * Hkv;
   const int64_t n_items = (int64_t)n_jobs * nsl;
   const float sl2 = P.scale_log2;
   const float inv_g = 1.f / (float)G;
@@ -1922,7 +1922,7 @@ int resident_pipe_groups() {
 
 template <int NRT, int NTH>
 int launch_score(const PrefillLaunch& P, hipStream_t st, void* stream) {
-  const int64_t n_items = (int64_t)P.batch * P.n_scored * P.n_kv_heads * P.n_slices;
+  const int64_t n_items = (int64_t)P.batch * P.n_window * P.n_kv_heads * P.n_slices;
   if (n_items <= 0) return 0;
   static const int fused_wg = resident_groups(score_fused_kernel<NRT, NTH>);
   static const int lagged_wg = resident_groups(score_kernel<NRT, NTH>);
@@ -1946,7 +1946,9 @@ int launch_score(const PrefillLaunch& P, hipStream_t st, void* stream) {
 
 int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int n_jobs = P.batch * P.n_scored * P.n_kv_heads;
+  // window-scored jobs (the scoring kernels below), then every scored job (selection)
+  const int n_jobs = P.batch * P.n_window * P.n_kv_heads;
+  const int n_sel = P.batch * P.n_scored * P.n_kv_heads;
   const int ntg = P.row_tiles_per_group;
   // the pipelined kernel takes four row tiles when a job has at most 64 slices (8192 keys) and
   // every slice of a job fits in the resident workgroups (RKV_FORCE_TWO_PASS selects the older
@@ -1984,6 +1986,15 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
     else if (ntg == 4) err = launch_score<8, 4>(P, st, stream);
     else err = launch_score<8, 8>(P, st, stream);
     if (err) return err;
+  }
+  if (n_sel > n_jobs) {
+    // H2O layers with full-span accumulation: their own two passes, then the shared selection
+    profile_mark(kStageScore, false, stream);
+    int err = launch_fullspan(P, stream);
+    profile_mark(kStageScore, true, stream);
+    if (err) return err;
+  }
+  if (n_sel > 0) {
     static bool lds_set = false;
     if (!lds_set) {
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
@@ -1999,9 +2010,9 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
                                         (size_t)(P.n_slices > 0 ? P.n_slices - 1 : 0) * 2 * P.pool_half);
     profile_mark(kStageSelect, false, stream);
     if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - kHistBins * 4 - 256)
-      select_regs_kernel<<<n_jobs, kSelThreads, dyn, st>>>(P);
+      select_regs_kernel<<<n_sel, kSelThreads, dyn, st>>>(P);
     else
-      select_kernel<<<n_jobs, kThreads, kSelectLds, st>>>(P);
+      select_kernel<<<n_sel, kThreads, kSelectLds, st>>>(P);
     profile_mark(kStageSelect, true, stream);
   }
   const int n_gather_items = P.n_gather > 0 ? P.gather_item0[P.n_gather] : 0;

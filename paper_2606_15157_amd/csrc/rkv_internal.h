@@ -41,12 +41,14 @@ struct PrefillLayer {
 
 // One prefill launch group (up to 32 layers).  A scored "job" is a (scored layer slot,
 // sequence, KV head) triple, job = (slot * B + b) * Hkv + h; its keys are cut into n_slices
-// slices of kSlice keys, the scoring work items.  The scored layers come first in `layer`, so
-// slot s is layer[s] (slot_layer[s] == s).
+// slices of kSlice keys, the scoring work items.  The scored layers come first in `layer`
+// (window-scored ones, then H2O with full-span accumulation), so slot s is layer[s]
+// (slot_layer[s] == s).
 struct PrefillLaunch {
   PrefillLayer layer[kMaxLayersPerLaunch];
   int32_t n_layers;
   int32_t n_scored;       // scored layer slots
+  int32_t n_window;       // of which window-scored (slots 0 .. n_window-1; the rest: H2O full span)
   int32_t n_gather;       // layers with retained rows (gather list)
   int32_t batch, seq_len, n_q_heads, n_kv_heads, window;
   int32_t group;          // G = Hq / Hkv
@@ -63,6 +65,7 @@ struct PrefillLaunch {
   float* lam;             // [J][R]  per-row log2 softmax normaliser (+inf for rows without keys); the
                           //         pipelined kernel keeps the reciprocal row sum 1 / Z here instead
   float* ncl;             // [J][R]  pipelined kernel: minus the per-row reference logit (0 for padding rows)
+  float* lamf;            // [J_full][G][L]  full-span H2O: log2 normaliser of every query row
   float* S;               // [J][L]  ranking score
   float* Su;              // [J][L]  unpooled group-mean score (SnapKV layers, if wanted)
   float* edge;            // [J][n_slices][G][4 * pool_half]  per-query-head column sums at slice edges
@@ -75,9 +78,10 @@ static_assert(sizeof(PrefillLaunch) <= 4000, "kernel argument block too large");
 
 // Workspace layout for one launch group.
 struct PrefillWorkspace {
-  size_t counters, stats, lam, ncl, S, Su, edge, end, total;
+  size_t counters, stats, lam, ncl, lamf, S, Su, edge, end, total;
 };
-PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half);
+PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half,
+                                          int n_full_jobs);
 
 // Error reporting (thread-local last error).
 int fail(int status, const std::string& msg);
@@ -85,6 +89,7 @@ void clear_error();
 
 // Kernel launchers (prefill.hip / decode.hip).  Return a hipError_t as int.
 int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream);
+int launch_fullspan(const PrefillLaunch& P, void* stream);   // fullspan.hip
 
 struct DecodeLayer {
   uint16_t* k_cache; uint16_t* v_cache; int32_t* pos; float* acc;

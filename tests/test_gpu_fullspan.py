@@ -1,0 +1,83 @@
+"""GPU parity of H2O prefill with full-span accumulation (every prompt query) against the oracle."""
+import numpy as np
+import pytest
+
+from oracle import prefill as OP
+from parity import bits_to_torch, check_gather, check_retained, check_scores, torch_to_bits
+from synth import prefill_layer
+
+pytestmark = pytest.mark.gpu
+
+
+def run_route(rules, budgets, layers, *, window, L):
+    """layers[l][s]: dict with q (w rows, or L rows for H2O_FULL), k, v bits."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    plan = rkv.Plan(rules, budgets, window=window)
+    q = [bits_to_torch(np.stack([x["q"] for x in seqs])) for seqs in layers]
+    k = [bits_to_torch(np.stack([x["k"] for x in seqs])) for seqs in layers]
+    v = [bits_to_torch(np.stack([x["v"] for x in seqs])) for seqs in layers]
+    out = rkv.evict_prefill(plan, q, k, v, score_out=True, acc_out=True)
+    torch.cuda.synchronize()
+    assert rkv.prefill_check(out["workspace"]) == 0
+    for l, seqs in enumerate(layers):
+        idx = out["idx"][l].cpu().numpy()
+        sc = out["scores"][l].cpu().numpy()
+        acc = out["acc"][l].cpu().numpy()
+        ko, vo = torch_to_bits(out["k_out"][l]), torch_to_bits(out["v_out"][l])
+        for s, x in enumerate(seqs):
+            ora = OP.evict_layer(rules[l], budgets[l], x["q"], x["k"], x["v"], window=window)
+            Hkv = x["k"].shape[0]
+            for h in range(Hkv):
+                what = f"layer {l} ({OP.RULE_NAMES[rules[l]]}) seq {s} head {h}"
+                if ora["scores"] is not None:
+                    n = ora["scores"].shape[1]
+                    check_scores(sc[s, h, :n], ora["scores"][h], what)
+                check_retained(idx[s, h], ora, h, L, what)
+                check_gather(ko[s, h], vo[s, h], x["k"][h], x["v"][h], idx[s, h], what)
+                if rules[l] in (OP.H2O, OP.H2O_FULL):
+                    check_scores(acc[s, h], ora["acc"][h], what + " acc")
+    return out
+
+
+def gen(workload, seq, layer, L, rows, Hq=32, Hkv=8):
+    return prefill_layer(workload, seq, layer, seq_len=L, n_q_heads=Hq, n_kv_heads=Hkv, window=rows)
+
+
+def test_full_span_single_layer_1k():
+    L = 1024
+    run_route([OP.H2O_FULL], [200], [[gen(30, 0, 0, L, L)]], window=32, L=L)
+
+
+def test_mixed_route_with_full_span_ragged():
+    """StreamingLLM, SnapKV, H2O (window) and H2O_FULL layers in one call, L = 777."""
+    L, w = 777, 32
+    rules = [OP.STREAMING, OP.SNAPKV, OP.H2O, OP.H2O_FULL, OP.H2O_FULL]
+    budgets = [64, 100, 100, 100, 300]
+    layers = [[gen(31, 0, l, L, L if rules[l] == OP.H2O_FULL else w)] for l in range(len(rules))]
+    run_route(rules, budgets, layers, window=w, L=L)
+
+
+@pytest.mark.parametrize("Hq,Hkv,L,B", [(16, 8, 300, 2), (32, 4, 513, 1), (8, 8, 200, 1)])
+def test_full_span_groups(Hq, Hkv, L, B):
+    """G = 2, 8, 1 (query tiles of 64, 16, 128 positions), ragged prompts, a batch of two."""
+    layers = [[gen(32, s, 0, L, L, Hq, Hkv) for s in range(B)]]
+    run_route([OP.H2O_FULL], [L // 3], layers, window=16, L=L)
+
+
+def test_full_span_totals_at_8k():
+    """At L = 8192 (keeping everything, so every score is reported): each head's full-span
+    scores total L, one unit of attention per query."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    L = 8192
+    g = torch.Generator(device="cuda").manual_seed(5)
+    q = torch.randn((1, 32, L, 128), generator=g, device="cuda", dtype=torch.bfloat16)
+    k = torch.randn((1, 8, L, 128), generator=g, device="cuda", dtype=torch.bfloat16)
+    v = torch.randn((1, 8, L, 128), generator=g, device="cuda", dtype=torch.bfloat16)
+    plan = rkv.Plan([OP.H2O_FULL], [L], window=32)
+    out = rkv.evict_prefill(plan, [q], [k], [v], score_out=True)
+    torch.cuda.synchronize()
+    assert rkv.prefill_check(out["workspace"]) == 0
+    tot = out["scores"][0].double().sum(-1).cpu().numpy()
+    np.testing.assert_allclose(tot, L, rtol=1e-4)
