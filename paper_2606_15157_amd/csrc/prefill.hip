@@ -453,6 +453,11 @@ __device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base)
                : "memory", "m0");
 }
+// The same with a wave-uniform base address in SGPRs and a 32-bit per-lane byte offset.
+__device__ __forceinline__ void dma16s(const void* base, uint32_t off, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds_base)
+               : "memory", "m0");
+}
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
@@ -905,25 +910,34 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     const int key0 = j.slice * kSlice;
     const uint32_t q_lds = lds_addr(&sQ[b][4 * (wv & 3) * kHeadDim]);
     const uint32_t k_lds = lds_addr(&sK[b][4 * (wv & 3) * kHeadDim]);
+    // common case: a uniform base per instruction (scalar arithmetic) and the lane's fixed offset
+    if (__builtin_expect(!padded_rows, 1)) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int g = u / (2 * NTH), ii0 = 16 * (u % (2 * NTH));
-      uint32_t off = (uint32_t)(g * w + ii0) * 256u + lane_off;
-      if (__builtin_expect(padded_rows, 0)) {
-        const bool ok = g < G && ii0 + lrow < w;
-        off = ok ? off : (uint32_t)((lane & 15) ^ lrow) * 16u;   // padding rows repeat row 0
+      for (int u = 0; u < 8; ++u) {
+        const int g = u / (2 * NTH), ii0 = 16 * (u % (2 * NTH));
+        dma16s(qjob + (size_t)(g * w + ii0) * 256u, lane_off, q_lds + 16u * kHeadDim * 2u * u);
       }
-      dma16(qjob + off, q_lds + 16u * kHeadDim * 2u * u);
+    } else {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int g = u / (2 * NTH), ii0 = 16 * (u % (2 * NTH));
+        const bool ok = g < G && ii0 + lrow < w;
+        const uint32_t off = ok ? (uint32_t)(g * w + ii0) * 256u + lane_off
+                                : (uint32_t)((lane & 15) ^ lrow) * 16u;   // padding rows repeat row 0
+        dma16(qjob + off, q_lds + 16u * kHeadDim * 2u * u);
+      }
     }
     const bool tail = key0 + kSlice > L;
+    if (__builtin_expect(!tail, 1)) {
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      size_t off = (size_t)(key0 + 16 * u) * 256u + lane_off;
-      if (__builtin_expect(tail, 0)) {
+      for (int u = 0; u < 8; ++u)
+        dma16s(khead + (size_t)(key0 + 16 * u) * 256u, lane_off, k_lds + 16u * kHeadDim * 2u * u);
+    } else {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
         const int key = min(key0 + 16 * u + lrow, L - 1);
-        off = (size_t)key * 256u + (uint32_t)((lane & 15) ^ lrow) * 16u;
+        dma16(khead + (size_t)key * 256u + (uint32_t)((lane & 15) ^ lrow) * 16u, k_lds + 16u * kHeadDim * 2u * u);
       }
-      dma16(khead + off, k_lds + 16u * kHeadDim * 2u * u);
     }
     if (wv == 4) {
       // the job's 128 reference logits: lanes 0-31 move 16 bytes each (the DMA writes only the
