@@ -7,7 +7,8 @@
 // evicted and the new token takes its slot.  TOVA: the same probabilities; an entry's score is
 // their group mean at this step alone, every entry (the new one included) is a candidate, and
 // the smallest score is evicted (ties: smallest position).  StreamingLLM: the oldest non-sink
-// slot is replaced.  Keys are read with four lanes per 256-byte row (64 B per lane).
+// slot is replaced.  Keys are read with four lanes per 256-byte row, 64 contiguous bytes per
+// load instruction and row.
 #include <hip/hip_runtime.h>
 
 #include "rkv_internal.h"
@@ -65,10 +66,50 @@ __device__ __forceinline__ uint64_t block_reduce_min_u64(uint64_t v, uint64_t* s
   return r;
 }
 
+// Block-wide max / sum of G values at once (per-value order as in the scalar versions).
+template <int G>
+__device__ __forceinline__ void block_reduce_max_v(float (&v)[G], float* sh) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v[g] = fmaxf(v[g], __shfl_xor(v[g], o));
+    if (lane == 0) sh[wv * G + g] = v[g];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    float r = sh[g];
+#pragma unroll
+    for (int i = 1; i < kDecWaves; ++i) r = fmaxf(r, sh[i * G + g]);
+    v[g] = r;
+  }
+  __syncthreads();
+}
+template <int G>
+__device__ __forceinline__ void block_reduce_sum_v(float (&v)[G], float* sh) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v[g] += __shfl_xor(v[g], o);
+    if (lane == 0) sh[wv * G + g] = v[g];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    float r = 0.f;
+#pragma unroll
+    for (int i = 0; i < kDecWaves; ++i) r += sh[i * G + g];
+    v[g] = r;
+  }
+  __syncthreads();
+}
+
 template <int G>
 __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch D) {
   extern __shared__ float sDyn[];
-  __shared__ float shf[kDecWaves];
+  __shared__ float shf[kDecWaves * 8];
   __shared__ uint64_t shu[kDecWaves];
   const int tid = threadIdx.x;
   const int Hkv = D.n_kv_heads, B = D.batch;
@@ -100,28 +141,43 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
   } else {
     float* sZ = sDyn;                      // [G][C+1] logits, then probabilities
     float* sAcc = sDyn + (size_t)G * (C + 1);  // [C+1] updated accumulated scores
-    // query pairs for this lane's quarter of the head dimension
+    // lane qq of an entry takes the 16-byte chunks 4 i + qq (i = 0..3) of the head dimension, so
+    // that the four lanes of a row read 64 contiguous bytes per load; the queries likewise
     const int qq = tid & 3;
     uint32_t qr[G][16];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      const uint32_t* qp = reinterpret_cast<const uint32_t*>(ly.q + ((size_t)s * D.n_q_heads + h * G + g) * kHeadDim + 32 * qq);
+      const uint16_t* qp = ly.q + ((size_t)s * D.n_q_heads + h * G + g) * kHeadDim;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(qp + 4 * i);
+        const u32x4 v = *reinterpret_cast<const u32x4*>(qp + 8 * (4 * i + qq));
         qr[g][4 * i] = v[0]; qr[g][4 * i + 1] = v[1]; qr[g][4 * i + 2] = v[2]; qr[g][4 * i + 3] = v[3];
       }
     }
+    // key rows stream through registers one block of 64 entries ahead of the dot products
+    auto load_rows = [&](int base, u32x4 (&kv)[4]) {
+      const int e = base + (tid >> 2);
+      if (e <= C) {
+        const uint16_t* kr = e < C ? kc + (size_t)e * kHeadDim : knew;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) kv[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kr + 8 * (4 * i + qq)));
+      }
+    };
+    u32x4 kn[4];
+    load_rows(0, kn);
+    float mx[G];   // running maximum logit per query head (lanes holding a finished dot product)
+#pragma unroll
+    for (int g = 0; g < G; ++g) mx[g] = -__builtin_inff();
     for (int base = 0; base <= C; base += kDecThreads / 4) {
       const int e = base + (tid >> 2);
+      u32x4 kv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) kv[i] = kn[i];
+      if (base + kDecThreads / 4 <= C) load_rows(base + kDecThreads / 4, kn);
       float dot[G];
 #pragma unroll
       for (int g = 0; g < G; ++g) dot[g] = 0.f;
       if (e <= C) {
-        const uint16_t* kr = (e < C ? kc + (size_t)e * kHeadDim : knew) + 32 * qq;
-        u32x4 kv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) kv[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kr + 8 * i));
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           float d = 0.f;
@@ -139,26 +195,33 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
       }
       if (e <= C && qq == 0) {
 #pragma unroll
-        for (int g = 0; g < G; ++g) sZ[g * (C + 1) + e] = dot[g];
+        for (int g = 0; g < G; ++g) {
+          sZ[g * (C + 1) + e] = dot[g];
+          mx[g] = fmaxf(mx[g], dot[g]);
+        }
       }
     }
-    __syncthreads();
+    // every head's maximum and row sum in one pass over the logits, two block reductions
     const float sl2 = D.scale_log2;
+    block_reduce_max_v<G>(mx, shf);   // its first barrier also publishes the logits in LDS
+    float sm[G];
+#pragma unroll
     for (int g = 0; g < G; ++g) {
-      float m = -__builtin_inff();
-      for (int e = tid; e <= C; e += kDecThreads) m = fmaxf(m, sZ[g * (C + 1) + e]);
-      m = block_reduce_max(m, shf) * sl2;
-      float sm = 0.f;
-      for (int e = tid; e <= C; e += kDecThreads) {
-        const float x = __builtin_amdgcn_exp2f(fmaf(sZ[g * (C + 1) + e], sl2, -m));
-        sZ[g * (C + 1) + e] = x;
-        sm += x;
-      }
-      sm = block_reduce_sum(sm, shf);
-      const float inv = 1.0f / sm;
-      for (int e = tid; e <= C; e += kDecThreads) sZ[g * (C + 1) + e] *= inv;
+      mx[g] *= sl2;
+      sm[g] = 0.f;
     }
-    __syncthreads();
+    for (int e = tid; e <= C; e += kDecThreads) {
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const float x = __builtin_amdgcn_exp2f(fmaf(sZ[g * (C + 1) + e], sl2, -mx[g]));
+        sZ[g * (C + 1) + e] = x;
+        sm[g] += x;
+      }
+    }
+    block_reduce_sum_v<G>(sm, shf);
+    float inv[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) inv[g] = 1.0f / sm[g];
     // H2O: candidates have position <= p - r and the score accumulates; TOVA: every entry is a
     // candidate and the score is this step's alone
     const bool tova = ly.rule == RKV_TOVA;
@@ -166,7 +229,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
     for (int e = tid; e <= C; e += kDecThreads) {
       float pm = 0.f;
 #pragma unroll
-      for (int g = 0; g < G; ++g) pm += sZ[g * (C + 1) + e];
+      for (int g = 0; g < G; ++g) pm += sZ[g * (C + 1) + e] * inv[g];
       pm = pm / (float)G;
       const float a = (e < C && !tova ? acc[e] : 0.f) + pm;
       sAcc[e] = a;
