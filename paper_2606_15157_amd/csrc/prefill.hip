@@ -810,7 +810,7 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 // Minus the reference logit of every row of every scored job, and the per-pass resets: the
 // status word and the job's slices' row sums ("not stored": NaN).
-// One workgroup per job; thread = (row, half of the head dimension).
+// One workgroup per job.
 template <int NTH>
 __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
   constexpr int R = 128;
@@ -825,32 +825,47 @@ __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
     const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
     for (int i = tid; i < P.n_slices * R / 4; i += 256) st[i] = nan4;
   }
-  const int r = tid >> 1, hv = tid & 1;
-  const int g = r / (NTH * 32), ii = r - g * (NTH * 32);
-  const bool valid = g < G && ii < w;
-  float zd = 0.f, zs = 0.f;
-  if (valid) {
-    const uint16_t* q = ly.q + ((size_t)(s * Hq + h * G + g) * w + ii) * kHeadDim + hv * 64;
-    const uint16_t* kh = ly.k + (size_t)(s * Hkv + h) * L * kHeadDim + hv * 64;
-    const uint16_t* kd = kh + (size_t)(L - w + ii) * kHeadDim;
+  // 16 lanes per row, lane c taking 16-byte chunk c of the query, the row's own key and key 0
+  // (each load instruction reads whole 256-byte rows); 16 rows per pass, 8 passes
+  const int c = tid & 15;
+  const u32x4* ks = reinterpret_cast<const u32x4*>(ly.k + (size_t)(s * Hkv + h) * L * kHeadDim) + c;
+  u32x4 qa[8], da[8], sa[8];
+  bool valid[8];
 #pragma unroll
-    for (int c = 0; c < 8; ++c) {
-      const u32x4 qa = *reinterpret_cast<const u32x4*>(q + 8 * c);
-      const u32x4 da = *reinterpret_cast<const u32x4*>(kd + 8 * c);
-      const u32x4 sa = *reinterpret_cast<const u32x4*>(kh + 8 * c);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float q0 = __uint_as_float(qa[u] << 16), q1 = __uint_as_float(qa[u] & 0xffff0000u);
-        zd = fmaf(q0, __uint_as_float(da[u] << 16), zd);
-        zd = fmaf(q1, __uint_as_float(da[u] & 0xffff0000u), zd);
-        zs = fmaf(q0, __uint_as_float(sa[u] << 16), zs);
-        zs = fmaf(q1, __uint_as_float(sa[u] & 0xffff0000u), zs);
-      }
+  for (int p = 0; p < 8; ++p) {
+    const int r = 16 * p + (tid >> 4);
+    const int g = r / (NTH * 32), ii = r - g * (NTH * 32);
+    valid[p] = g < G && ii < w;
+    if (valid[p]) {
+      qa[p] = reinterpret_cast<const u32x4*>(ly.q + ((size_t)(s * Hq + h * G + g) * w + ii) * kHeadDim)[c];
+      da[p] = ks[(size_t)(L - w + ii) * 16];
+      sa[p] = ks[0];
     }
   }
-  zd += __shfl_xor(zd, 1);
-  zs += __shfl_xor(zs, 1);
-  if (hv == 0) P.ncl[(size_t)job * R + r] = valid ? -fmaxf(zd, zs) : 0.f;
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    float zd = 0.f, zs = 0.f;
+    if (valid[p]) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float q0 = __uint_as_float(qa[p][u] << 16), q1 = __uint_as_float(qa[p][u] & 0xffff0000u);
+        zd = fmaf(q0, __uint_as_float(da[p][u] << 16), zd);
+        zd = fmaf(q1, __uint_as_float(da[p][u] & 0xffff0000u), zd);
+        zs = fmaf(q0, __uint_as_float(sa[p][u] << 16), zs);
+        zs = fmaf(q1, __uint_as_float(sa[p][u] & 0xffff0000u), zs);
+      }
+    }
+    // sums over the 16 lanes of the row: rotations by 8, 4, 2, 1 inside each 16-lane DPP row
+    zd += dppf<0x128>(zd);
+    zs += dppf<0x128>(zs);
+    zd += dppf<0x124>(zd);
+    zs += dppf<0x124>(zs);
+    zd += dppf<0x122>(zd);
+    zs += dppf<0x122>(zs);
+    zd += dppf<0x121>(zd);
+    zs += dppf<0x121>(zs);
+    if (c == 0) P.ncl[(size_t)job * R + 16 * p + (tid >> 4)] = valid[p] ? -fmaxf(zd, zs) : 0.f;
+  }
 }
 
 // Reduce-scatter of 16 values over the 16 lanes of each row: afterwards lane l holds the sum of
