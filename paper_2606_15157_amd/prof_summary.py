@@ -24,6 +24,8 @@ def kernel_stats(run_dir: str):
 def short_name(name: str) -> str:
     """Kernel name without return type, namespaces and parameter list."""
     name = re.sub(r"^void ", "", name)
+    if name.startswith("at::"):   # torch's own kernels (input generation in the benchmark)
+        return "torch " + re.split(r"[<(]", name)[0]
     name = name.replace("rkv::(anonymous namespace)::", "")
     depth, cut = 0, len(name)
     for i, ch in enumerate(name):      # drop the parameter list: the first '(' outside <...>
