@@ -458,6 +458,17 @@ __device__ __forceinline__ void dma16s(const void* base, uint32_t off, uint32_t 
   asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds_base)
                : "memory", "m0");
 }
+// Two of those 4 KiB apart: [base + off] -> lds_base and [base + 4096 + off] -> lds_base + 4096
+// (+ 16 lane).  The instruction offset applies to the global and to the LDS address alike, so
+// one base and one M0 value serve both.
+__device__ __forceinline__ void dma16s_pair(const char* base, uint32_t off, uint32_t lds_base) {
+  asm volatile(
+      "s_mov_b32 m0, %2\n\ts_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1 offset:-4096\n\t"
+      "global_load_lds_dwordx4 %0, %1" ::"v"(off),
+      "s"(base + 4096), "s"(lds_base + 4096u)
+      : "memory", "m0");
+}
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p);
@@ -927,11 +938,9 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     const uint32_t k_lds = lds_addr(&sK[b][4 * (wv & 3) * kHeadDim]);
     // common case: a uniform base per instruction (scalar arithmetic) and the lane's fixed offset
     if (__builtin_expect(!padded_rows, 1)) {
+      // w = 32 NTH rows per head and G NTH = 4: instruction u reads rows 16 u + lrow, 4 KiB apart
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int g = u / (2 * NTH), ii0 = 16 * (u % (2 * NTH));
-        dma16s(qjob + (size_t)(g * w + ii0) * 256u, lane_off, q_lds + 16u * kHeadDim * 2u * u);
-      }
+      for (int u = 0; u < 8; u += 2) dma16s_pair(qjob + 4096u * u, lane_off, q_lds + 4096u * u);
     } else {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -944,9 +953,9 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     }
     const bool tail = key0 + kSlice > L;
     if (__builtin_expect(!tail, 1)) {
+      const char* kslice = khead + (size_t)key0 * 256u;
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        dma16s(khead + (size_t)(key0 + 16 * u) * 256u, lane_off, k_lds + 16u * kHeadDim * 2u * u);
+      for (int u = 0; u < 8; u += 2) dma16s_pair(kslice + 4096u * u, lane_off, k_lds + 4096u * u);
     } else {
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
@@ -1085,22 +1094,26 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       const int kl = tid >> 1, h = tid & 1, kk = cbase + kl;
       const float* c0 = sColP[h][0];
       const float* c1 = sColP[h][1];
-      float su = 0.f, sc = 0.f;
-      if (kk < L) {
-        const int lo = max(kk - 3, cbase) - cbase, hi = min(min(kk + 3, cbase + kSlice - 1), npre - 1) - cbase;
-        float m0 = NEG_INF, m1 = NEG_INF;
+      // pool window [lo, hi] inside the slice and the prefix; it holds kl whenever the pooled
+      // score is used (kk < L - w).  Clamping a neighbour into the window repeats a member, which
+      // leaves the maximum unchanged, so all fourteen reads are unconditional (no branches, one
+      // wait); for window keys (hi < kl) the range degenerates to [lo, lo] and the result is unused
+      const int lo = max(kk - 3, cbase) - cbase;
+      const int hi = max(min(min(kk + 3, cbase + kSlice - 1), npre - 1) - cbase, lo);
+      float a[7], b[7];
 #pragma unroll
-        for (int u = -3; u <= 3; ++u) {
-          const int q = kl + u;
-          const bool in = q >= lo && q <= hi;
-          const int qc = in ? q : kl;
-          const float a = c0[qc], b = c1[qc];
-          m0 = in ? fmaxf(m0, a) : m0;
-          m1 = in ? fmaxf(m1, b) : m1;
-        }
-        su = c0[kl] + c1[kl];
-        sc = (m0 > NEG_INF ? m0 : 0.f) + (m1 > NEG_INF ? m1 : 0.f);
+      for (int u = 0; u < 7; ++u) {
+        const int qc = min(max(kl + u - 3, lo), hi);
+        a[u] = c0[qc];
+        b[u] = c1[qc];
       }
+      float m0 = a[0], m1 = b[0];
+#pragma unroll
+      for (int u = 1; u < 7; ++u) {
+        m0 = fmaxf(m0, a[u]);
+        m1 = fmaxf(m1, b[u]);
+      }
+      float su = c0[kl] + c1[kl], sc = m0 + m1;
       su += __shfl_xor(su, 1);
       sc += __shfl_xor(sc, 1);
       if (h == 0 && kk < L) {
