@@ -981,19 +981,31 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       e[rs][0] = c4;
       e[rs][1] = c4;
     }
+    // software pipeline over the four k-steps: the six fragments of k-step st + 1 are read
+    // from LDS while the eight MFMAs of k-step st run (two fragment sets live)
+    bf16x8 kf[2][2], qf[2][4];
+    auto load_step = [&](int st, int b2) {
+      kf[b2][0] = frag16(k, kt * 32 + l16, 4 * st + lg);
+      kf[b2][1] = frag16(k, kt * 32 + 16 + l16, 4 * st + lg);
+#pragma unroll
+      for (int rs = 0; rs < 4; ++rs) qf[b2][rs] = frag16(q, rh * 64 + rs * 16 + l16, 4 * st + lg);
+    };
+    load_step(0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 10, 0);   // DS reads: the references and k-step 0
 #pragma unroll
     for (int st = 0; st < 4; ++st) {
-      const bf16x8 k0 = frag16(k, kt * 32 + l16, 4 * st + lg);
-      const bf16x8 k1 = frag16(k, kt * 32 + 16 + l16, 4 * st + lg);
+      if (st < 3) {
+        load_step(st + 1, (st + 1) & 1);
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+      }
 #pragma unroll
       for (int rs = 0; rs < 4; ++rs) {
-        const bf16x8 qa = frag16(q, rh * 64 + rs * 16 + l16, 4 * st + lg);
-        e[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, k0, e[rs][0], 0, 0, 0);
-        e[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, k1, e[rs][1], 0, 0, 0);
+        e[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st & 1][rs], kf[st & 1][0], e[rs][0], 0, 0, 0);
+        e[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st & 1][rs], kf[st & 1][1], e[rs][1], 0, 0, 0);
       }
-      // one k-step's fragments live at a time (the other wave of the SIMD covers the LDS latency)
-      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);   // MFMA
     }
+    __builtin_amdgcn_sched_barrier(0);
     const int key_w0 = j.slice * kSlice + kt * 32;
     if (__builtin_expect(padded_rows || key_w0 + 31 > L - w, 0)) {
       // rare tiles (reaching into the window or past the prompt, or padding rows): logits of
@@ -1214,7 +1226,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
 
   f32x4v e0[4][2], e1[4][2], e2[4][2], e3[4][2];
   PipeRef ja = pipe_item(first, nsl, B, Hkv);   // item t
-  PipeRef j1 = ja, j2 = ja, j3 = ja;              // items t - 1, t - 2, t - 3
+  PipeRef j1 = ja, j2 = ja;                       // items t - 1, t - 2
   if (wv >= 4) {
     issue_dma(ja, 0);
     if (T > 1) {
@@ -1225,7 +1237,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   }
 
   auto iteration = [&](int t, f32x4v (&ea)[4][2], f32x4v (&eb)[4][2]) {
-    const bool doA = t < T, doB = t >= 3 && t - 3 < T;
+    const bool doA = t < T, doB = t >= 2 && t - 2 < T;
     // B1 (the DMA of item t was complete at MID of iteration t - 1; the first iteration waits
     // for the two DMAs issued before the loop)
     if (t == 0) wait_vmcnt<0>();
@@ -1234,16 +1246,14 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     // results unused), so each register set is redefined unconditionally
     phase_a(ja, t & 1, ea);
     // MID: everything this wave issued in earlier iterations has completed (the row sums of item
-    // t - 3's job and the DMA of item t + 1); the row sums become item t - 3's normalisers.  The
-    // row sums of item t - 2's job (consumed at the next MID) are loaded at once, in every
-    // iteration so that the registers have one definition (the job is clamped where the item
-    // lies outside the pipeline)
+    // t - 2's job and the DMA of item t + 1); the row sums become item t - 2's normalisers.  The
+    // row sums of item t - 1's job (stored by its workgroups after their phase A, consumed at
+    // the next MID) are loaded at once, in every iteration so that the registers have one
+    // definition (the job is clamped where the item lies outside the pipeline)
     wait_vmcnt<0>();
-    if (doB) take_stats(j3);
-    load_stats(min(j2.job, n_jobs - 1));
-    lds_barrier();   // B1.5
-    phase_b(j3, eb);
-    lds_barrier();   // B2: every wave is done with buffer t % 2 and with sColP
+    if (doB) take_stats(j2);
+    load_stats(min(j1.job, n_jobs - 1));
+    lds_barrier();   // B1.5: every wave's phase A is done (sStat complete, buffer t % 2 free)
     // wave 0: item t's row sums (the consumers check for sums not stored yet)
     if (wv == 0 && doA) {
       float2 o;
@@ -1251,29 +1261,31 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       o.y = sStat[0][2 * lane + 1] + sStat[1][2 * lane + 1] + sStat[2][2 * lane + 1] + sStat[3][2 * lane + 1];
       store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + 2 * lane, o.x, o.y);
     }
+    phase_b(j2, eb);
+    lds_barrier();   // B2: sColP complete
     if (wv < 4) {
-      if (doB) store(j3);
+      if (doB) store(j2);
     } else if (t + 2 < T) {
       PipeRef jn = ja;
       pipe_advance(jn, dj, ds, nsl, B, Hkv);
       pipe_advance(jn, dj, ds, nsl, B, Hkv);
       issue_dma(jn, t & 1);
     }
-    j3 = j2;
     j2 = j1;
     j1 = ja;
     pipe_advance(ja, dj, ds, nsl, B, Hkv);
   };
 
-  // T + 3 iterations drain the pipeline; the count is padded to a multiple of four (the padding
-  // iterations store nothing) so that the unrolled body has a single exit at its end
-  const int n_iter = (T + 3 + 3) & ~3;
+  // T + 2 iterations drain the pipeline; the count is padded to a multiple of four (the padding
+  // iterations store nothing) so that the unrolled body has a single exit at its end.  Item t's
+  // exponentials live in set t % 4 from iteration t to t + 2, so three sets are live at a time.
+  const int n_iter = (T + 2 + 3) & ~3;
 #pragma unroll 1
   for (int t = 0; t < n_iter; t += 4) {
-    iteration(t, e0, e1);
-    iteration(t + 1, e1, e2);
-    iteration(t + 2, e2, e3);
-    iteration(t + 3, e3, e0);
+    iteration(t, e0, e2);
+    iteration(t + 1, e1, e3);
+    iteration(t + 2, e2, e0);
+    iteration(t + 3, e3, e1);
   }
 }
 
