@@ -774,7 +774,7 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
 
 // ---------------------------------------------------------------------------------------------
 // Pipelined scoring against a per-row reference (four row tiles, one eight-wave workgroup per
-// CU, four items in flight).
+// CU, three items in flight).
 //
 // Reference.  The softmax of a window row is shift-invariant, so the exponentials may be taken
 // against any per-row constant c_i that keeps them in range.  c_i is the larger of the row's
@@ -796,25 +796,27 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel
 // job loads all of the job's row sums (at most 64 slices) and sums them itself, so the only
 // cross-workgroup dependency is store -> load, with no counter and no designated folder.
 //
-// Schedule of iteration t (item t enters phase A, item t - 3 phase B, each in its own register
+// Schedule of iteration t (item t enters phase A, item t - 2 phase B, each in its own register
 // set; no wait is for an operation issued in the same iteration):
 //   B1
-//   A     logits, exponentials, per-row partial sums per key tile into sStat
+//   A     logits (k-step fragments read one step ahead), exponentials, per-row partial sums per
+//         key tile into sStat
 //   MID   every wave: all its earlier memory operations have completed; the row sums of item
-//         t - 3's job (loaded at MID of iteration t - 1; re-read while any is still NaN)
-//         -> reciprocal normalisers in sAlpha; then the loads of item t - 2's row sums
+//         t - 2's job (loaded at MID of iteration t - 1; re-read while any is still NaN)
+//         -> reciprocal normalisers in sAlpha; then the loads of item t - 1's row sums
 //   B1.5
-//   B     item t - 3: probabilities, sums over the window rows per query head (or group) into sColP
+//   wave 0: store item t's row sums
+//   B     item t - 2: probabilities, sums over the window rows per query head (or group) into sColP
 //   B2
-//   wave 0: store item t's row sums; waves 0-3: scores of item t - 3; waves 4-7: LDS DMA of
-//         item t + 2 into the buffer item t has just left
+//   waves 0-3: scores of item t - 2; waves 4-7: LDS DMA of item t + 2 into the buffer item t has
+//         just left
 // Progress: the loads of iteration t - 1 are for sums that other workgroups store in iterations
-// <= t - 2 (a job's slices sit in at most two consecutive iterations because a job has no more
-// slices than there are workgroups), so with every workgroup resident no wait is on a later one.
+// <= t - 1, before their own waits of iteration t (a job's slices sit in at most two consecutive
+// iterations because a job has no more slices than there are workgroups), so with every
+// workgroup resident no wait is on a later one.
 // ---------------------------------------------------------------------------------------------
 constexpr int kPipeWaves = 8;
 constexpr int kPipeThreads = kPipeWaves * 64;
-constexpr int kPipeDepth = 4;
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
