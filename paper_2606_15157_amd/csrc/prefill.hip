@@ -1697,14 +1697,16 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
 
 // Selection with every candidate score held in registers (kSelRegs per thread, 1024 threads):
 // wave wv owns the contiguous key range [w0, w1); its lane l holds keys w0 + 64 i + l.  Dynamic
-// LDS holds the job's slice-edge column sums and the repaired scores next to slice borders.
+// LDS holds the job's slice-edge column sums and the repaired scores next to slice borders
+// (with their per-head pool maxima).
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kSelRegs = 16;
 constexpr int kSelRegsMaxKeys = kSelRegs * kSelThreads;
 
 __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillLaunch P) {
-  extern __shared__ __attribute__((aligned(16))) float sDyn[];   // [n_edge] edges, then [n_fix] repaired scores
+  // dynamic LDS: [n_edge] edges, [n_fix] repaired scores, [n_fix G] per-head pool maxima
+  extern __shared__ __attribute__((aligned(16))) float sDyn[];
   __shared__ int sHist[kHistBins];
   __shared__ int sScan[2 * kSelWaves];
   __shared__ int sSel[2];
@@ -1750,23 +1752,28 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
     lds_barrier();
     // SnapKV: redo the pooled score of positions within pool_half of an interior slice border;
     // slice cb-1 holds keys [bnd-2P, bnd) at edge offsets [2P, 4P), slice cb keys [bnd, bnd+2P) at [0, 2P)
+    // first the pool maximum of every (position, head) over all threads, then the head sum of
+    // every position in head order
     const int npre = L - w;
-    for (int e = tid; e < n_fix; e += kSelThreads) {
+    float* sPart = sFix + n_fix;
+    for (int task = tid; task < n_fix * G; task += kSelThreads) {
+      const int e = task / G, g = task - e * G;
       const int cb = 1 + e / twoP, o = e - (cb - 1) * twoP;
       const int bnd = cb * kSlice, j = bnd - ph + o;
-      float sc = 0.f;
+      float m = NEG_INF;
       if (j >= 0 && j < npre && j < n) {
-        const int left = (cb - 1) * G * E, right = cb * G * E;
+        const int left = (cb - 1) * G * E + g * E + twoP - (bnd - twoP), right = cb * G * E + g * E - bnd;
         const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
-        for (int g = 0; g < G; ++g) {
-          float m = NEG_INF;
-          for (int t = lo; t <= hi; ++t) {
-            const int ei = (t < bnd) ? left + g * E + twoP + (t - (bnd - twoP)) : right + g * E + (t - bnd);
-            m = fmaxf(m, sEdge[ei]);
-          }
-          sc += m;
-        }
+        for (int t = lo; t <= hi; ++t) m = fmaxf(m, sEdge[t < bnd ? left + t : right + t]);
       }
+      sPart[task] = m;
+    }
+    lds_barrier();
+    for (int e = tid; e < n_fix; e += kSelThreads) {
+      const int cb = 1 + e / twoP, j = cb * kSlice - ph + (e - (cb - 1) * twoP);
+      float sc = 0.f;
+      if (j >= 0 && j < npre && j < n)
+        for (int g = 0; g < G; ++g) sc += sPart[e * G + g];
       sFix[e] = sc * inv_g;
     }
     lds_barrier();
@@ -2063,7 +2070,8 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
     }
     // registers hold every candidate score when the prompt is short enough and the edge sums fit
     const size_t dyn = sizeof(float) * ((size_t)P.n_slices * P.group * 4 * P.pool_half +
-                                        (size_t)(P.n_slices > 0 ? P.n_slices - 1 : 0) * 2 * P.pool_half);
+                                        (size_t)(P.n_slices > 0 ? P.n_slices - 1 : 0) * 2 * P.pool_half *
+                                            (1 + P.group));
     profile_mark(kStageSelect, false, stream);
     if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - kHistBins * 4 - 256)
       select_regs_kernel<<<n_sel, kSelThreads, dyn, st>>>(P);
