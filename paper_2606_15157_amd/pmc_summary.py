@@ -5,6 +5,12 @@
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir_write> -o run -- (same command)
     python -m paper_2606_15157_amd.pmc_summary <dir_fetch> <dir_write> <out.json> <out.md>
 
+    python -m paper_2606_15157_amd.pmc_summary --sq <out.md> <dir> [<dir> ...]
+
+The second form tabulates SQ counters of the scoring kernel from one or more rocprofv3 --pmc
+runs (median over the kernel's dispatches in each run): shares of SQ_WAVE_CYCLES and instruction
+counts per wave and per pipeline iteration.
+
 FETCH_SIZE / WRITE_SIZE (KiB per dispatch) are scaled by what the same counter reads for the
 plain 1 GiB device copy that --copy-calibration runs (bytes known exactly), and the result is
 stored with the hash of the kernel source it was measured on.
@@ -94,5 +100,46 @@ def main(argv):
     print(json.dumps(rec))
 
 
+SQ_SHARES = ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU",
+             "SQ_ACTIVE_INST_SCA", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_ACTIVE_INST_LDS", "SQ_WAIT_INST_LDS",
+             "SQ_ACTIVE_INST_MISC", "SQ_ACTIVE_INST_VMEM", "SQ_LDS_IDX_ACTIVE", "SQ_LDS_BANK_CONFLICT",
+             "SQ_LDS_ADDR_CONFLICT", "SQ_BUSY_CYCLES")
+SQ_COUNTS = ("SQ_INSTS_VALU", "SQ_INSTS_SALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS", "SQ_INSTS_VMEM")
+
+
+def sq_main(out_md, dirs, iterations=64):
+    vals = {}
+    for d in dirs:
+        path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+        counters = {row["Counter_Name"] for row in csv.DictReader(open(path[0]))}
+        for c in counters:
+            _, v = pick(per_dispatch(d, c), SCORE_NAME)
+            vals[c] = statistics.median(v)
+    wc, waves = vals["SQ_WAVE_CYCLES"], vals["SQ_WAVES"]
+    with open(out_md, "w") as f:
+        f.write(f"# SQ counters of {SCORE_NAME} (32-layer mixed route, L=8192)\n\n")
+        f.write("Commands (one run per counter set, from /tmp with TMPDIR=/tmp; median over the dispatches "
+                "of each run):\n\n")
+        for d in dirs:
+            path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+            cs = sorted({row["Counter_Name"] for row in csv.DictReader(open(path[0]))})
+            f.write(f"    rocprofv3 --pmc {' '.join(cs)} --output-format csv -d <dir> -o run -- python3 bench.py "
+                    "--steps 3 --warmup 1 --no-cpu-baseline --no-decode --no-entropy --no-fullspan\n")
+        f.write(f"    python -m paper_2606_15157_amd.pmc_summary --sq <out.md> <dir> ...\n\n")
+        f.write(f"{waves:.0f} waves; each runs {iterations} pipeline iterations.\n\n")
+        f.write("| counter | value | share of SQ_WAVE_CYCLES |\n|---|---|---|\n")
+        for c in SQ_SHARES:
+            if c in vals:
+                f.write(f"| {c} | {vals[c]:.4g} | {vals[c] / wc:.3f} |\n")
+        f.write("\n| instructions | per wave | per wave and iteration |\n|---|---|---|\n")
+        for c in SQ_COUNTS:
+            if c in vals:
+                f.write(f"| {c} | {vals[c] / waves:.0f} | {vals[c] / waves / iterations:.0f} |\n")
+    print(open(out_md).read())
+
+
 if __name__ == "__main__":
-    main(sys.argv)
+    if len(sys.argv) > 1 and sys.argv[1] == "--sq":
+        sq_main(sys.argv[2], sys.argv[3:])
+    else:
+        main(sys.argv)

@@ -2,7 +2,12 @@
 
     rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o run -- python3 bench.py \
         --steps 50 --warmup 5 --no-cpu-baseline
-    python -m paper_2606_15157_amd.prof_summary <dir> <out.md> "<title>" "<command>"
+    python -m paper_2606_15157_amd.prof_summary <dir> <out.md> "<title>" "<command>" \
+        [<kernel> <n>]
+
+With <kernel> and <n>, the first n dispatches of that kernel (by start time; in the default
+benchmark run these are the warm-up and timed passes of the headline route, before any other
+measurement launches it) are also averaged on their own from the kernel trace.
 """
 from __future__ import annotations
 
@@ -36,6 +41,16 @@ def short_name(name: str) -> str:
     return name[:cut]
 
 
+def first_dispatches(run_dir: str, kernel: str, n: int):
+    """Durations (ns) of the first n dispatches of the kernel whose short name is `kernel`."""
+    path = glob.glob(os.path.join(run_dir, "**", "*kernel_trace.csv"), recursive=True)
+    if not path:
+        raise FileNotFoundError(f"no kernel_trace.csv under {run_dir}")
+    rows = [r for r in csv.DictReader(open(path[0])) if short_name(r["Kernel_Name"]) == kernel]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    return [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows[:n]]
+
+
 def main(argv):
     run_dir, out_md, title, command = argv[1:5]
     rows = kernel_stats(run_dir)
@@ -46,6 +61,12 @@ def main(argv):
             f.write(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
                     f"{float(r['Percentage']):.1f}% |\n")
+        if len(argv) > 6:
+            kernel, n = argv[5], int(argv[6])
+            d = first_dispatches(run_dir, kernel, n)
+            f.write(f"\nFirst {len(d)} dispatches of {kernel} (the headline route's warm-up and timed "
+                    f"passes): average {sum(d) / len(d) / 1e3:.1f} us, min {min(d) / 1e3:.1f} us, "
+                    f"max {max(d) / 1e3:.1f} us.\n")
     print(open(out_md).read())
 
 
