@@ -201,6 +201,22 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
         }
       }
     }
+    // H2O: candidates have position <= p - r and the score accumulates; TOVA: every entry is a
+    // candidate and the score is this step's alone
+    const bool tova = ly.rule == RKV_TOVA;
+    const int limit = tova ? p : p - ly.recent;
+    // positions and accumulated scores of entries tid + 256 k (k < kDecPre), requested now so
+    // that they arrive during the reductions and the exponential pass (the key registers are
+    // free here); entries past those are read when visited
+    constexpr int kDecPre = 4;
+    int pre_pos[kDecPre];
+    float pre_acc[kDecPre];
+#pragma unroll
+    for (int k = 0; k < kDecPre; ++k) {
+      const int e = tid + kDecThreads * k;
+      pre_pos[k] = e < C ? pos[e] : p;
+      pre_acc[k] = e < C && !tova ? acc[e] : 0.f;
+    }
     // every head's maximum and row sum in one pass over the logits, two block reductions
     const float sl2 = D.scale_log2;
     block_reduce_max_v<G>(mx, shf);   // its first barrier also publishes the logits in LDS
@@ -222,23 +238,23 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
     float inv[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) inv[g] = 1.0f / sm[g];
-    // H2O: candidates have position <= p - r and the score accumulates; TOVA: every entry is a
-    // candidate and the score is this step's alone
-    const bool tova = ly.rule == RKV_TOVA;
-    const int limit = tova ? p : p - ly.recent;
-    for (int e = tid; e <= C; e += kDecThreads) {
+    auto visit = [&](int e, float acc_e, int ps) {
       float pm = 0.f;
 #pragma unroll
       for (int g = 0; g < G; ++g) pm += sZ[g * (C + 1) + e] * inv[g];
       pm = pm / (float)G;
-      const float a = (e < C && !tova ? acc[e] : 0.f) + pm;
+      const float a = acc_e + pm;
       sAcc[e] = a;
-      const int ps = e < C ? pos[e] : p;
       if (ps <= limit) {
         const uint64_t key = ((uint64_t)__float_as_uint(a) << 32) | (uint32_t)ps;
         best = key < best ? key : best;
       }
-    }
+    };
+#pragma unroll
+    for (int k = 0; k < kDecPre; ++k)
+      if (tid + kDecThreads * k <= C) visit(tid + kDecThreads * k, pre_acc[k], pre_pos[k]);
+    for (int e = tid + kDecThreads * kDecPre; e <= C; e += kDecThreads)
+      visit(e, e < C && !tova ? acc[e] : 0.f, e < C ? pos[e] : p);
     best = block_reduce_min_u64(best, shu);
     const int vpos = (int)(uint32_t)(best & 0xffffffffu);
     // slot holding the winning position (positions are distinct); C = the new token
@@ -246,7 +262,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
     if (tid == 0) sVictim = -1;
     __syncthreads();
     if (best != ~0ull) {
-      for (int e = tid; e <= C; e += kDecThreads) {
+#pragma unroll
+      for (int k = 0; k < kDecPre; ++k)
+        if (tid + kDecThreads * k <= C && pre_pos[k] == vpos) sVictim = tid + kDecThreads * k;
+      for (int e = tid + kDecThreads * kDecPre; e <= C; e += kDecThreads) {
         const int ps = e < C ? pos[e] : p;
         if (ps == vpos) sVictim = e;
       }
