@@ -44,7 +44,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
   constexpr int NW = G > 4 ? G : 4;   // at least four waves share the K tile loads
   constexpr int NT = 64 * NW;
   constexpr int PER = kSlice * kHeadDim / 8 / NT;   // 16-byte K chunks per thread per tile
-  __shared__ __attribute__((aligned(16))) uint16_t sK[kSlice * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kSlice * kHeadDim];   // double-buffered K tile
   __shared__ float sC[NW][kEntRows];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, lg = lane >> 4, l16 = lane & 15;
   const int L = E.seq_len, n_q = E.n_q, Hq = E.n_q_heads, Hkv = E.n_kv_heads;
@@ -100,9 +100,12 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
       qa[rs][st] = as_bf16x8(v);
     }
   }
-  // ---- K tiles: keys [0, t_last] where t_last is the block's last valid position
+  // ---- K tiles: keys [0, t_last] where t_last is the block's last valid position.  Tiles
+  // whose keys every row of the block sees (k0 + 127 <= t0) are "bulk" tiles; the rest (at most
+  // two) need the causal mask.
   const int t_last = L - n_q + min(i0 + kEntRows, n_q) - 1;
   const int n_tiles = t_last / kSlice + 1;
+  const int n_bulk = min((t0 + 1) / kSlice, n_tiles);
   u32x4 pre[PER];
   auto fetch = [&](int kt) {
 #pragma unroll
@@ -112,14 +115,21 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
       pre[u] = *reinterpret_cast<const u32x4*>(khead + (size_t)kk * kHeadDim + 8 * ch);
     }
   };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
+      *reinterpret_cast<u32x4*>(&sK[buf][(key * 16 + (ch ^ (key & 15))) * 8]) = pre[u];
+    }
+  };
   fetch(0);
   __syncthreads();   // sC written
-  float cref[2][4];
+  const float sl2 = E.scale_log2;
+  float ncs[2][4];   // -c sl2 per row
 #pragma unroll
   for (int rs = 0; rs < 2; ++rs)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) cref[rs][i] = sC[wv][16 * rs + 4 * lg + i];
-  const float sl2 = E.scale_log2;
+    for (int i = 0; i < 4; ++i) ncs[rs][i] = -sC[wv][16 * rs + 4 * lg + i] * sl2;
   float Z[2][4], T[2][4];
 #pragma unroll
   for (int rs = 0; rs < 2; ++rs)
@@ -128,56 +138,103 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
       Z[rs][i] = 0.f;
       T[rs][i] = 0.f;
     }
-
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    __syncthreads();   // every wave is done with the previous tile
+  // logits of key sub-tiles ks0 .. ks0 + 3 of the tile in buffer buf (x = q.k, the reference is
+  // applied with the scale afterwards)
+  auto mfma_half = [&](int buf, int ks0, f32x4 (&a)[2][4]) {
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
-      *reinterpret_cast<u32x4*>(&sK[(key * 16 + (ch ^ (key & 15))) * 8]) = pre[u];
-    }
-    __syncthreads();
-    if (kt + 1 < n_tiles) fetch(kt + 1);
-    if (!compute) continue;
-    const int k0 = kt * kSlice;
-    f32x4 acc[2][8];
+    for (int st = 0; st < 4; ++st)
 #pragma unroll
-    for (int rs = 0; rs < 2; ++rs)
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[rs][ks][i] = -cref[rs][i];
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const int key = 16 * ks + l16, ch = 4 * st + lg;
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[(key * 16 + (ch ^ (key & 15))) * 8]);
-        acc[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], kf, acc[0][ks], 0, 0, 0);
-        acc[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], kf, acc[1][ks], 0, 0, 0);
+      for (int ks = 0; ks < 4; ++ks) {
+        const int key = 16 * (ks0 + ks) + l16, ch = 4 * st + lg;
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[buf][(key * 16 + (ch ^ (key & 15))) * 8]);
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        a[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], kf, st == 0 ? z : a[0][ks], 0, 0, 0);
+        a[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], kf, st == 0 ? z : a[1][ks], 0, 0, 0);
       }
-      // one k-step's fragments live at a time
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    // keys past a row's position (and past the prompt) take no part; only the last tiles need it
-    const bool edge = k0 + kSlice - 1 > t0;
+  };
+  // exponentials and the row sums Z (of e) and T (of e x) for four key sub-tiles
+  auto valu_half = [&](const f32x4 (&a)[2][4]) {
 #pragma unroll
     for (int rs = 0; rs < 2; ++rs)
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
+      for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float x = acc[rs][ks][i] * sl2;
-          if (edge) {
-            const int key = k0 + 16 * ks + l16;
-            const int ir = i0 + 16 * rs + 4 * lg + i;
-            const int t = L - n_q + ir;
-            if (key > t || ir >= n_q) x = kMasked;
-          }
+          const float x = fmaf(a[rs][ks][i], sl2, ncs[rs][i]);
           const float e = __builtin_amdgcn_exp2f(x);
           Z[rs][i] += e;
           T[rs][i] = fmaf(e, x, T[rs][i]);
         }
+  };
+  // one MFMA half interleaved with one exponential half: per group, one K fragment read, two
+  // MFMAs and eight VALU instructions
+  auto interleave = [&]() {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+      if (j < 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+  };
+  f32x4 accA[2][4], accB[2][4];
+  // bulk tiles, software-pipelined: MFMA half B of tile kt with the exponentials of half A, then
+  // (after the barrier that publishes tile kt + 1) MFMA half A of tile kt + 1 with the
+  // exponentials of half B of tile kt.  The order of the sums is that of the plain loop.
+  put(0);
+  if (n_tiles > 1) fetch(1);
+  __syncthreads();
+  if (compute && n_bulk > 0) mfma_half(0, 0, accA);
+  for (int kt = 0; kt < n_bulk; ++kt) {
+    if (compute) {
+      mfma_half(kt & 1, 4, accB);
+      valu_half(accA);
+      interleave();
+    }
+    if (kt + 1 < n_tiles) {
+      put((kt + 1) & 1);
+      if (kt + 2 < n_tiles) fetch(kt + 2);
+    }
+    __syncthreads();   // tile kt + 1 published; every wave is done with tile kt's buffer
+    if (compute) {
+      if (kt + 1 < n_bulk) {
+        mfma_half((kt + 1) & 1, 0, accA);
+        valu_half(accB);
+        interleave();
+      } else {
+        valu_half(accB);
+      }
+    }
+  }
+  // edge tiles: keys past a row's position (and past the prompt) take no part
+  for (int kt = n_bulk; kt < n_tiles; ++kt) {
+    if (compute) {
+      const int k0 = kt * kSlice;
+      mfma_half(kt & 1, 0, accA);
+      mfma_half(kt & 1, 4, accB);
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float av = hf == 0 ? accA[rs][ks][i] : accB[rs][ks][i];
+              float x = fmaf(av, sl2, ncs[rs][i]);
+              const int key = k0 + 16 * (4 * hf + ks) + l16;
+              const int ir = i0 + 16 * rs + 4 * lg + i;
+              if (key > L - n_q + ir || ir >= n_q) x = kMasked;
+              const float e = __builtin_amdgcn_exp2f(x);
+              Z[rs][i] += e;
+              T[rs][i] = fmaf(e, x, T[rs][i]);
+            }
+    }
+    if (kt + 1 < n_tiles) {
+      put((kt + 1) & 1);
+      if (kt + 2 < n_tiles) fetch(kt + 2);
+    }
+    __syncthreads();
   }
   // ---- the 16 lanes of each row (one DPP row) add up; lane l16 == 0 writes the entropy and
   // adds it to the workgroup's partial sum (fixed order: lanes, then waves)
