@@ -119,6 +119,14 @@ __global__ void reset_counters(uint32_t* counters, int n, uint32_t* lam, int n_l
 // ---------------------------------------------------------------------------------------------
 // Cross-lane sums over the 32 window rows held by the lanes of each half-wave.
 // ---------------------------------------------------------------------------------------------
+// Sum of an integer over the 16 lanes of each DPP row (every lane of the row gets it).
+__device__ __forceinline__ int row16_sum(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x128, 0xf, 0xf, false);   // row_ror:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x124, 0xf, 0xf, false);   // row_ror:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x122, 0xf, 0xf, false);   // row_ror:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x121, 0xf, 0xf, false);   // row_ror:1
+  return x;
+}
 template <int CTRL>
 __device__ __forceinline__ float dppf(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
@@ -1701,6 +1709,7 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
 // (with their per-head pool maxima).
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
+static_assert(kSelWaves <= 16, "wave prefixes are summed over one 16-lane DPP row");
 constexpr int kSelRegs = 16;
 constexpr int kSelRegsMaxKeys = kSelRegs * kSelThreads;
 
@@ -1710,7 +1719,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   __shared__ int sHist[kHistBins];
   __shared__ int sScan[2 * kSelWaves];
   __shared__ int sSel[2];
-  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id();
+  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), l16 = lane & 15;
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_slices;
   const int job = blockIdx.x;
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
@@ -1827,8 +1836,8 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
         }
         if (lane == 63) sScan[wv] = inc;
         lds_barrier();
-        int above = inc - cnt;
-        for (int q = 0; q < wv; ++q) above += sScan[q];
+        // plus the counts of the waves before this one: one read per lane, a 16-lane sum
+        int above = inc - cnt + row16_sum(l16 < wv ? sScan[l16] : 0);
         if (kk > above && kk <= above + cnt) {
           for (int q = 0; q < per; ++q) {
             const int b = nb - 1 - (tid * per + q);
@@ -1865,11 +1874,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
         sScan[2 * wv + 1] = ce;
       }
       lds_barrier();
-      int bg = 0, be = 0;
-      for (int q = 0; q < wv; ++q) {
-        bg += sScan[2 * q];
-        be += sScan[2 * q + 1];
-      }
+      int bg = row16_sum(l16 < wv ? sScan[2 * l16] : 0), be = row16_sum(l16 < wv ? sScan[2 * l16 + 1] : 0);
 #pragma unroll
       for (int i = 0; i < kSelRegs; ++i) {
         const int j = w0 + 64 * i + lane;
