@@ -1716,9 +1716,9 @@ constexpr int kSelRegsMaxKeys = kSelRegs * kSelThreads;
 __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillLaunch P) {
   // dynamic LDS: [n_edge] edges, [n_fix] repaired scores, [n_fix G] per-head pool maxima
   extern __shared__ __attribute__((aligned(16))) float sDyn[];
-  __shared__ int sHist[kHistBins];
+  __shared__ int sHist[2][kHistBins];   // pass p uses buffer p % 2
   __shared__ int sScan[2 * kSelWaves];
-  __shared__ int sSel[2];
+  __shared__ int sSel[2][2];            // likewise
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), l16 = lane & 15;
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_slices;
   const int job = blockIdx.x;
@@ -1811,23 +1811,29 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
       // >= 0, so the unsigned order of their bit patterns is the numeric order)
       uint32_t prefix = 0u, pmask = 0u;
       int kk = k;
+      // both histogram buffers start cleared; buffer 0 is cleared again during pass 1 (pass 0's
+      // last read of it precedes pass 0's last barrier), so a pass needs three barriers
+      for (int b = tid; b < 2 * kHistBins; b += kSelThreads) (&sHist[0][0])[b] = 0;
+      lds_barrier();
 #pragma unroll 1
       for (int pass = 0; pass < 3; ++pass) {
         const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
         const int nb = pass == 0 ? 2048 : 1024;
-        for (int b = tid; b < nb; b += kSelThreads) sHist[b] = 0;
-        lds_barrier();
+        int* hist = sHist[pass & 1];
+        int* sel = sSel[pass & 1];
 #pragma unroll
         for (int i = 0; i < kSelRegs; ++i) {
           const int j = w0 + 64 * i + lane;
           const uint32_t u = rank_bits(x[i]);
-          if (j < w1 && (u & pmask) == prefix) atomicAdd(&sHist[(u >> shift) & (nb - 1)], 1);
+          if (j < w1 && (u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & (nb - 1)], 1);
         }
+        if (pass == 1)
+          for (int b = tid; b < 1024; b += kSelThreads) sHist[0][b] = 0;   // for pass 2
         lds_barrier();
         // bins in descending order: thread tid owns bins nb-1-tid*per .. (per = 2 or 1)
         const int per = nb / kSelThreads;
         int cnt = 0;
-        for (int q = 0; q < per; ++q) cnt += sHist[nb - 1 - (tid * per + q)];
+        for (int q = 0; q < per; ++q) cnt += hist[nb - 1 - (tid * per + q)];
         int inc = cnt;  // inclusive scan of cnt over the workgroup
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
@@ -1841,20 +1847,19 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
         if (kk > above && kk <= above + cnt) {
           for (int q = 0; q < per; ++q) {
             const int b = nb - 1 - (tid * per + q);
-            const int hb = sHist[b];
+            const int hb = hist[b];
             if (kk <= above + hb) {
-              sSel[0] = b;
-              sSel[1] = kk - above;
+              sel[0] = b;
+              sel[1] = kk - above;
               break;
             }
             above += hb;
           }
         }
         lds_barrier();
-        prefix |= (uint32_t)sSel[0] << shift;
+        prefix |= (uint32_t)sel[0] << shift;
         pmask |= (uint32_t)(nb - 1) << shift;
-        kk = sSel[1];
-        lds_barrier();
+        kk = sel[1];
       }
       const uint32_t tau = prefix;
       const int need = kk;  // ties at tau taken in position order
@@ -2078,7 +2083,7 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
                                         (size_t)(P.n_slices > 0 ? P.n_slices - 1 : 0) * 2 * P.pool_half *
                                             (1 + P.group));
     profile_mark(kStageSelect, false, stream);
-    if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - kHistBins * 4 - 256)
+    if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - 2 * kHistBins * 4 - 256)
       select_regs_kernel<<<n_sel, kSelThreads, dyn, st>>>(P);
     else
       select_kernel<<<n_sel, kThreads, kSelectLds, st>>>(P);
