@@ -46,7 +46,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void fullspan_rows_kernel(
   constexpr int NW = G > 4 ? G : 4;
   constexpr int NT = 64 * NW;
   constexpr int PER = kSlice * kHeadDim / 8 / NT;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[kSlice * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][kSlice * kHeadDim];   // double-buffered K tile
   __shared__ float sC[NW][kFsRows];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, lg = lane >> 4, l16 = lane & 15;
   const int L = P.seq_len, Hq = P.n_q_heads, Hkv = P.n_kv_heads, B = P.batch;
@@ -97,6 +97,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void fullspan_rows_kernel(
   }
   const int t_last = min(t0 + kFsRows, L) - 1;
   const int n_tiles = t_last / kSlice + 1;
+  const int n_bulk = min((t0 + 1) / kSlice, n_tiles);   // tiles every row of the block sees whole
   u32x4 pre[PER];
   auto fetch = [&](int kt) {
 #pragma unroll
@@ -106,59 +107,111 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void fullspan_rows_kernel(
       pre[u] = *reinterpret_cast<const u32x4*>(khead + (size_t)kk * kHeadDim + 8 * ch);
     }
   };
+  auto put = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
+      *reinterpret_cast<u32x4*>(&sK[buf][swz(key, ch)]) = pre[u];
+    }
+  };
   fetch(0);
   __syncthreads();
-  float cref[2][4], Z[2][4];
+  const float sl2 = P.scale_log2;
+  float cref[2][4], ncs[2][4], Z[2][4];
 #pragma unroll
   for (int rs = 0; rs < 2; ++rs)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       cref[rs][i] = sC[wv][16 * rs + 4 * lg + i];
+      ncs[rs][i] = -cref[rs][i] * sl2;
       Z[rs][i] = 0.f;
     }
-  const float sl2 = P.scale_log2;
-  for (int kt = 0; kt < n_tiles; ++kt) {
-    __syncthreads();
+  // logits (q.k) of key sub-tiles ks0 .. ks0 + 3 of the tile in buffer buf
+  auto mfma_half = [&](int buf, int ks0, f32x4 (&a)[2][4]) {
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
-      *reinterpret_cast<u32x4*>(&sK[swz(key, ch)]) = pre[u];
-    }
-    __syncthreads();
-    if (kt + 1 < n_tiles) fetch(kt + 1);
-    if (!compute) continue;
-    const int k0 = kt * kSlice;
-    f32x4 acc[2][8];
+    for (int st = 0; st < 4; ++st)
 #pragma unroll
-    for (int rs = 0; rs < 2; ++rs)
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc[rs][ks][i] = -cref[rs][i];
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[swz(16 * ks + l16, 4 * st + lg)]);
-        acc[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], kf, acc[0][ks], 0, 0, 0);
-        acc[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], kf, acc[1][ks], 0, 0, 0);
+      for (int ks = 0; ks < 4; ++ks) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(&sK[buf][swz(16 * (ks0 + ks) + l16, 4 * st + lg)]);
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        a[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], kf, st == 0 ? z : a[0][ks], 0, 0, 0);
+        a[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], kf, st == 0 ? z : a[1][ks], 0, 0, 0);
       }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    const bool edge = k0 + kSlice - 1 > t0;
+  };
+  auto valu_half = [&](const f32x4 (&a)[2][4]) {
 #pragma unroll
     for (int rs = 0; rs < 2; ++rs)
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
+      for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float x = acc[rs][ks][i] * sl2;
-          if (edge) {
-            const int key = k0 + 16 * ks + l16, t = t0 + 16 * rs + 4 * lg + i;
-            if (key > t || t >= L) x = kMasked;
-          }
-          Z[rs][i] += __builtin_amdgcn_exp2f(x);
-        }
+        for (int i = 0; i < 4; ++i) Z[rs][i] += __builtin_amdgcn_exp2f(fmaf(a[rs][ks][i], sl2, ncs[rs][i]));
+  };
+  // one MFMA half interleaved with one exponential half: per group, one K fragment read, two
+  // MFMAs and six VALU instructions
+  auto interleave = [&]() {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      if (j < 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+  };
+  f32x4 accA[2][4], accB[2][4];
+  // bulk tiles, software-pipelined: MFMA half B of tile kt with the exponentials of half A, then
+  // (after the barrier that publishes tile kt + 1) MFMA half A of tile kt + 1 with the
+  // exponentials of half B of tile kt; the sums keep the order of the plain loop
+  put(0);
+  if (n_tiles > 1) fetch(1);
+  __syncthreads();
+  if (compute && n_bulk > 0) mfma_half(0, 0, accA);
+  for (int kt = 0; kt < n_bulk; ++kt) {
+    if (compute) {
+      mfma_half(kt & 1, 4, accB);
+      valu_half(accA);
+      interleave();
+    }
+    if (kt + 1 < n_tiles) {
+      put((kt + 1) & 1);
+      if (kt + 2 < n_tiles) fetch(kt + 2);
+    }
+    __syncthreads();   // tile kt + 1 published; every wave is done with tile kt's buffer
+    if (compute) {
+      if (kt + 1 < n_bulk) {
+        mfma_half((kt + 1) & 1, 0, accA);
+        valu_half(accB);
+        interleave();
+      } else {
+        valu_half(accB);
+      }
+    }
+  }
+  // edge tiles: keys past a row's position (and rows past the prompt) take no part
+  for (int kt = n_bulk; kt < n_tiles; ++kt) {
+    if (compute) {
+      const int k0 = kt * kSlice;
+      mfma_half(kt & 1, 0, accA);
+      mfma_half(kt & 1, 4, accB);
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int rs = 0; rs < 2; ++rs)
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float av = hf == 0 ? accA[rs][ks][i] : accB[rs][ks][i];
+              float x = fmaf(av, sl2, ncs[rs][i]);
+              const int key = k0 + 16 * (4 * hf + ks) + l16, t = t0 + 16 * rs + 4 * lg + i;
+              if (key > t || t >= L) x = kMasked;
+              Z[rs][i] += __builtin_amdgcn_exp2f(x);
+            }
+    }
+    if (kt + 1 < n_tiles) {
+      put((kt + 1) & 1);
+      if (kt + 2 < n_tiles) fetch(kt + 2);
+    }
+    __syncthreads();
   }
   if (!compute) return;
 #pragma unroll
