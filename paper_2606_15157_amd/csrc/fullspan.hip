@@ -237,8 +237,11 @@ __global__ __launch_bounds__(256, 2) void fullspan_cols_kernel(const PrefillLaun
   constexpr int NT = 256;
   constexpr int PT = 128 / G;                      // query positions per 128-row tile
   constexpr int PER = 128 * kHeadDim / 8 / NT;     // 16-byte chunks of the query tile per thread
-  __shared__ __attribute__((aligned(16))) uint16_t sQ[128 * kHeadDim];
-  __shared__ float sLam[128];
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[2][128 * kHeadDim];   // double-buffered tiles
+  // the row normalisers of tile it sit in sLam[it % 3]: the exponentials of a tile's second half
+  // run after the barrier that publishes the next tile, while faster waves may already write the
+  // tile after that
+  __shared__ float sLam[3][128];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, lg = lane >> 4, l16 = lane & 15;
   const int L = P.seq_len, Hq = P.n_q_heads, Hkv = P.n_kv_heads, B = P.batch;
   const int nkb = (L + kSlice - 1) / kSlice;
@@ -278,55 +281,112 @@ __global__ __launch_bounds__(256, 2) void fullspan_cols_kernel(const PrefillLaun
       lpre = t < L ? lamj[(size_t)gg * L + t] : 0.f;
     }
   };
-  fetch(0);
-  const float sl2 = P.scale_log2;
-  float col[2] = {0.f, 0.f};
-  for (int it = 0; it < n_tiles; ++it) {
-    __syncthreads();
+  auto put = [&](int it) {   // tile it (in registers) into sQ[it % 2], sLam[it % 3]
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int c = tid + NT * u, row = c >> 4, ch = c & 15;
-      *reinterpret_cast<u32x4*>(&sQ[swz(row, ch)]) = pre[u];
+      *reinterpret_cast<u32x4*>(&sQ[it & 1][swz(row, ch)]) = pre[u];
     }
-    if (tid < 128) sLam[tid] = lpre;
-    __syncthreads();
-    if (it + 1 < n_tiles) fetch(it + 1);
-    const int t0 = tfirst + it * PT;
-    f32x4 acc[8][2];
+    if (tid < 128) sLam[it % 3][tid] = lpre;
+  };
+  const float sl2 = P.scale_log2;
+  float col[2] = {0.f, 0.f};
+  // logits of row sub-tiles rs0 .. rs0 + 3 of the tile in buffer buf against this wave's keys
+  auto mfma_half = [&](int buf, int rs0, f32x4 (&a)[4][2]) {
 #pragma unroll
-    for (int rs = 0; rs < 8; ++rs)
+    for (int st = 0; st < 4; ++st)
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) acc[rs][ks] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-#pragma unroll
-      for (int rs = 0; rs < 8; ++rs) {
-        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(&sQ[swz(16 * rs + l16, 4 * st + lg)]);
-        acc[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[0][st], acc[rs][0], 0, 0, 0);
-        acc[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[1][st], acc[rs][1], 0, 0, 0);
+      for (int rs = 0; rs < 4; ++rs) {
+        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(&sQ[buf][swz(16 * (rs0 + rs) + l16, 4 * st + lg)]);
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        a[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[0][st], st == 0 ? z : a[rs][0], 0, 0, 0);
+        a[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa, kf[1][st], st == 0 ? z : a[rs][1], 0, 0, 0);
       }
-      __builtin_amdgcn_sched_barrier(0);
+  };
+  // probabilities of those rows summed per key (no mask: a bulk tile)
+  auto valu_half = [&](int it, int rs0, const f32x4 (&a)[4][2]) {
+#pragma unroll
+    for (int rs = 0; rs < 4; ++rs) {
+      const f32x4 lm = *reinterpret_cast<const f32x4*>(&sLam[it % 3][16 * (rs0 + rs) + 4 * lg]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) col[ks] += __builtin_amdgcn_exp2f(fmaf(a[rs][ks][i], sl2, -lm[i]));
     }
-    // rows 16 rs + 4 lg + i: head (row / PT), position t0 + row % PT; hidden keys and rows past
-    // the prompt contribute 0
-    const bool edge = t0 < j0 + kSlice - 1 || t0 + PT > L;
+  };
+  auto interleave = [&]() {
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-    for (int rs = 0; rs < 8; ++rs) {
-      const f32x4 lm = *reinterpret_cast<const f32x4*>(&sLam[16 * rs + 4 * lg]);
+    for (int j = 0; j < 16; ++j) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+      if (j < 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+  };
+  f32x4 accA[4][2], accB[4][2];
+  // a tile with masks (near the diagonal, or past the prompt): rows 16 rs + 4 lg + i are head
+  // (row / PT) at position t0 + row % PT; hidden keys and rows past the prompt contribute 0
+  auto edge_tile = [&](int it) {
+    const int t0 = tfirst + it * PT;
+    mfma_half(it & 1, 0, accA);
+    mfma_half(it & 1, 4, accB);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
+    for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-          float x = fmaf(acc[rs][ks][i], sl2, -lm[i]);
-          if (edge) {
-            const int row = 16 * rs + 4 * lg + i, t = t0 + row % PT;
+      for (int rs = 0; rs < 4; ++rs) {
+        const f32x4 lm = *reinterpret_cast<const f32x4*>(&sLam[it % 3][16 * (4 * hf + rs) + 4 * lg]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int ks = 0; ks < 2; ++ks) {
+            float x = fmaf(hf == 0 ? accA[rs][ks][i] : accB[rs][ks][i], sl2, -lm[i]);
+            const int row = 16 * (4 * hf + rs) + 4 * lg + i, t = t0 + row % PT;
             const int key = j0 + 32 * wv + 16 * ks + l16;
             if (key > t || t >= L) x = kMasked;
+            col[ks] += __builtin_amdgcn_exp2f(x);
           }
-          col[ks] += __builtin_amdgcn_exp2f(x);
-        }
+      }
+  };
+  // publish tile it + 1 (already in registers) and request tile it + 2
+  auto advance = [&](int it) {
+    if (it + 1 < n_tiles) {
+      put(it + 1);
+      if (it + 2 < n_tiles) fetch(it + 2);
+    }
+    __syncthreads();
+  };
+  fetch(0);
+  put(0);
+  if (n_tiles > 1) fetch(1);
+  __syncthreads();
+  // tiles [it_lo, it_end) need no mask (every key at or before every row, every row inside the
+  // prompt); they run software-pipelined as in the row pass, the others plainly, in tile order
+  const int it_end = min(n_tiles, (L - tfirst) / PT);
+  const int it_lo = min(it_end, (j0 + kSlice - 1 - tfirst + PT - 1) / PT);
+  int it = 0;
+  for (; it < it_lo; ++it) {
+    edge_tile(it);
+    advance(it);
+  }
+  if (it < it_end) {
+    mfma_half(it & 1, 0, accA);
+    for (; it < it_end; ++it) {
+      mfma_half(it & 1, 4, accB);
+      valu_half(it, 0, accA);
+      interleave();
+      advance(it);
+      if (it + 1 < it_end) {
+        mfma_half((it + 1) & 1, 0, accA);
+        valu_half(it, 4, accB);
+        interleave();
+      } else {
+        valu_half(it, 4, accB);
       }
     }
+  }
+  for (; it < n_tiles; ++it) {
+    edge_tile(it);
+    advance(it);
   }
   // sum over the four lane groups (rows 4 lg + i): lanes l, l ^ 32, then l ^ 16
 #pragma unroll
