@@ -6,11 +6,12 @@
 //
 // entropy_rows_kernel: one workgroup per (layer, sequence, KV head, block of 32 query
 // positions), one wave per query head of the group.  The wave's query fragments stay in
-// registers; the K tiles of 128 keys stream through LDS (prefetched into registers one tile
-// ahead) and the logits come from 16x16x32 bf16 MFMA, accumulator started at minus a per-row
+// registers; the K tiles of 128 keys stream through two LDS buffers (prefetched into registers
+// one tile ahead) and the logits z come from 16x16x32 bf16 MFMA, taken against a per-row
 // reference c_t = max(logit with key t, logit with key 0) (both true logits of the row), so
 // e = exp2(x) with x = (z - c) log2(e) / sqrt(d) stays finite unless a key beats the reference
-// by more than ~88 natural-log units.  Per row the lane keeps Z = sum e and T = sum e x over its
+// by more than ~88 natural-log units.  On tiles without masks the MFMAs of one half-tile run
+// interleaved with the exponentials of the other half.  Per row the lane keeps Z = sum e and T = sum e x over its
 // keys; the 16 lanes of a row meet once at the end, and
 //   H = -sum p ln p = ln 2 (log2 Z - T / Z).
 // A non-finite row is written as it is and reported by the averaging kernel.

@@ -4,8 +4,8 @@
 // Two passes over the causal logits, no atomics, fixed summation order:
 //
 // fullspan_rows_kernel: one workgroup per (job, 32 query positions), one wave per query head of
-//   the group.  The wave's query fragments stay in registers, 128-key tiles stream through LDS,
-//   bf16 MFMA logits are taken against a fixed per-row reference c_t = max(logit with key t,
+//   the group.  The wave's query fragments stay in registers, 128-key tiles stream through two
+//   LDS buffers, bf16 MFMA logits are taken against a fixed per-row reference c_t = max(logit with key t,
 //   logit with key 0); the row's log2 normaliser Lambda_t = c_t log2(e)/sqrt(d) + log2(sum_j
 //   exp2(x_tj - c_t log2(e)/sqrt(d))) goes to the workspace.  A non-finite normaliser (a key
 //   beyond ~88 natural-log units above the reference) sets status bit 1.
@@ -13,6 +13,8 @@
 //   wave's key fragments stay in registers, 128-row query tiles (G heads x 128/G positions) at or
 //   after the block stream through LDS with their normalisers, and each lane sums
 //   p = exp2(x - Lambda_t) over its rows; the four lane groups meet once at the end.
+// In both, tiles without masks run software-pipelined: the MFMAs of one half-tile interleave
+// with the exponentials of the other half, in the summation order of the plain loop.
 // Jobs here are the full-span ones: job = (slot * B + b) * Hkv + h with slot >= n_window.
 #include <hip/hip_runtime.h>
 
