@@ -141,63 +141,59 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
   } else {
     float* sZ = sDyn;                      // [G][C+1] logits, then probabilities
     float* sAcc = sDyn + (size_t)G * (C + 1);  // [C+1] updated accumulated scores
-    // lane qq of an entry takes the 16-byte chunks 4 i + qq (i = 0..3) of the head dimension, so
-    // that the four lanes of a row read 64 contiguous bytes per load; the queries likewise
-    const int qq = tid & 3;
-    uint32_t qr[G][16];
+    // 16 lanes per entry: lane c (= tid % 16) takes the 16-byte chunk c of the head dimension, so
+    // a wave's load instruction reads four whole 256-byte rows; lanes hold chunk c of every
+    // query head.  An iteration covers 64 entries, entry base + tid / 16 + 16 j for j = 0..3.
+    const int c16 = tid & 15, rsub = tid >> 4;
+    u32x4 qr[G];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const uint16_t* qp = ly.q + ((size_t)s * D.n_q_heads + h * G + g) * kHeadDim;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const u32x4 v = *reinterpret_cast<const u32x4*>(qp + 8 * (4 * i + qq));
-        qr[g][4 * i] = v[0]; qr[g][4 * i + 1] = v[1]; qr[g][4 * i + 2] = v[2]; qr[g][4 * i + 3] = v[3];
-      }
-    }
-    // key rows stream through registers one block of 64 entries ahead of the dot products
+    for (int g = 0; g < G; ++g)
+      qr[g] = reinterpret_cast<const u32x4*>(ly.q + ((size_t)s * D.n_q_heads + h * G + g) * kHeadDim)[c16];
+    constexpr int kBlk = kDecThreads / 4;   // 64 entries per iteration
     auto load_rows = [&](int base, u32x4 (&kv)[4]) {
-      const int e = base + (tid >> 2);
-      if (e <= C) {
-        const uint16_t* kr = e < C ? kc + (size_t)e * kHeadDim : knew;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) kv[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kr + 8 * (4 * i + qq)));
+      for (int j = 0; j < 4; ++j) {
+        const int e = base + rsub + 16 * j;
+        if (e <= C) {
+          const uint16_t* kr = e < C ? kc + (size_t)e * kHeadDim : knew;
+          kv[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kr) + c16);
+        }
       }
     };
     u32x4 kn[4];
     load_rows(0, kn);
-    float mx[G];   // running maximum logit per query head (lanes holding a finished dot product)
+    float mx[G];   // running maximum logit per query head
 #pragma unroll
     for (int g = 0; g < G; ++g) mx[g] = -__builtin_inff();
-    for (int base = 0; base <= C; base += kDecThreads / 4) {
-      const int e = base + (tid >> 2);
+    for (int base = 0; base <= C; base += kBlk) {
       u32x4 kv[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) kv[i] = kn[i];
-      if (base + kDecThreads / 4 <= C) load_rows(base + kDecThreads / 4, kn);
-      float dot[G];
+      for (int j = 0; j < 4; ++j) kv[j] = kn[j];
+      if (base + kBlk <= C) load_rows(base + kBlk, kn);
+      float dot[4][G];
 #pragma unroll
-      for (int g = 0; g < G; ++g) dot[g] = 0.f;
-      if (e <= C) {
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           float d = 0.f;
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) d = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(kv[i][j]), as_bf16x2(qr[g][4 * i + j]), d, false);
-          dot[g] = d;
+          for (int u = 0; u < 4; ++u) d = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(kv[j][u]), as_bf16x2(qr[g][u]), d, false);
+          // sum over the 16 lanes of the entry (one DPP row): every lane gets it
+          d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x128, 0xf, 0xf, false));
+          d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x124, 0xf, 0xf, false));
+          d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x122, 0xf, 0xf, false));
+          d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x121, 0xf, 0xf, false));
+          dot[j][g] = d;
         }
-      }
 #pragma unroll
-      for (int g = 0; g < G; ++g) {
-        dot[g] += __shfl_xor(dot[g], 1);
-        dot[g] += __shfl_xor(dot[g], 2);
-      }
-      if (e <= C && qq == 0) {
+      for (int j = 0; j < 4; ++j) {
+        const int e = base + rsub + 16 * j;
+        if (e <= C) {
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          sZ[g * (C + 1) + e] = dot[g];
-          mx[g] = fmaxf(mx[g], dot[g]);
+          for (int g = 0; g < G; ++g) {
+            mx[g] = fmaxf(mx[g], dot[j][g]);
+            if (c16 == ((j * G + g) & 15)) sZ[g * (C + 1) + e] = dot[j][g];   // one lane writes each
+          }
         }
       }
     }
