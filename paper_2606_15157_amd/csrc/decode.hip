@@ -149,27 +149,25 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
 #pragma unroll
     for (int g = 0; g < G; ++g)
       qr[g] = reinterpret_cast<const u32x4*>(ly.q + ((size_t)s * D.n_q_heads + h * G + g) * kHeadDim)[c16];
-    constexpr int kBlk = kDecThreads / 4;   // 64 entries per iteration
+    constexpr int kBlk = kDecThreads / 4;   // 64 entries per block
+    // two blocks of key rows in flight: block b + 1's loads are outstanding while block b's dot
+    // products run, and block b + 2's are issued right after them (two register sets,
+    // alternating).  Every load is unconditional (entries past the end read the new token's row,
+    // which the cache serves), so the compiler's waits leave the other block in flight.
     auto load_rows = [&](int base, u32x4 (&kv)[4]) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int e = base + rsub + 16 * j;
-        if (e <= C) {
-          const uint16_t* kr = e < C ? kc + (size_t)e * kHeadDim : knew;
-          kv[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kr) + c16);
-        }
+        const uint16_t* kr = e < C ? kc + (size_t)e * kHeadDim : knew;
+        kv[j] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kr) + c16);
       }
     };
-    u32x4 kn[4];
-    load_rows(0, kn);
-    float mx[G];   // running maximum logit per query head
+    float mx[G];
 #pragma unroll
     for (int g = 0; g < G; ++g) mx[g] = -__builtin_inff();
-    for (int base = 0; base <= C; base += kBlk) {
-      u32x4 kv[4];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kv[j] = kn[j];
-      if (base + kBlk <= C) load_rows(base + kBlk, kn);
+    // dot products of the block at base (rows in kv), summed over the 16 lanes of each entry
+    // (one DPP row, every lane gets the sum); one lane writes each logit to LDS
+    auto process = [&](int base, const u32x4 (&kv)[4]) {
       float dot[4][G];
 #pragma unroll
       for (int j = 0; j < 4; ++j)
@@ -178,7 +176,6 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
           float d = 0.f;
 #pragma unroll
           for (int u = 0; u < 4; ++u) d = __builtin_amdgcn_fdot2_f32_bf16(as_bf16x2(kv[j][u]), as_bf16x2(qr[g][u]), d, false);
-          // sum over the 16 lanes of the entry (one DPP row): every lane gets it
           d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x128, 0xf, 0xf, false));
           d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x124, 0xf, 0xf, false));
           d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x122, 0xf, 0xf, false));
@@ -192,10 +189,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
 #pragma unroll
           for (int g = 0; g < G; ++g) {
             mx[g] = fmaxf(mx[g], dot[j][g]);
-            if (c16 == ((j * G + g) & 15)) sZ[g * (C + 1) + e] = dot[j][g];   // one lane writes each
+            if (c16 == ((j * G + g) & 15)) sZ[g * (C + 1) + e] = dot[j][g];
           }
         }
       }
+    };
+    u32x4 ka[4], kb[4];
+    load_rows(0, ka);
+    load_rows(kBlk, kb);
+    for (int base = 0; base <= C; base += 2 * kBlk) {
+      process(base, ka);
+      load_rows(base + 2 * kBlk, ka);
+      process(base + kBlk, kb);
+      load_rows(base + 3 * kBlk, kb);
     }
     // H2O: candidates have position <= p - r and the score accumulates; TOVA: every entry is a
     // candidate and the score is this step's alone
