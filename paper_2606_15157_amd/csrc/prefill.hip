@@ -1906,7 +1906,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
 }
 
 // ---------------------------------------------------------------------------------------------
-// Gather: copy the retained K / V rows, 16 lanes x 16 B per row, 8 rows in flight per lane group.
+// Gather: copy the retained K / V rows, 16 lanes x 16 B per row.
 // ---------------------------------------------------------------------------------------------
 // Gather: the retained K and V rows, bit for bit.  Work items are (gather layer, kGatherRows
 // output rows), flat over the layer's (sequence, KV head, kept row) rows, so an item never spans
@@ -2091,7 +2091,8 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   }
   const int n_gather_items = P.n_gather > 0 ? P.gather_item0[P.n_gather] : 0;
   if (n_gather_items > 0) {
-    const int grid = std::min(n_gather_items, device_cus() * 8);
+    // one workgroup per item: later workgroups' reads overlap earlier ones' writes
+    const int grid = n_gather_items;
     profile_mark(kStageGather, false, stream);
     gather_kernel<<<grid, kThreads, 0, st>>>(P);
     profile_mark(kStageGather, true, stream);

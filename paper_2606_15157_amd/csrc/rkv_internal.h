@@ -16,7 +16,7 @@ constexpr int kMaxLayersPerLaunch = 32;
 constexpr int kSlice = 128;        // keys per scoring work item (4 waves x one tile of 32)
 constexpr int kMaxRowTiles = 8;    // G * ceil(w / 32) supported by the scoring kernel
 constexpr int kMaxPoolHalf = 64;   // pool_kernel / 2 supported
-constexpr int kGatherRows = 64;    // retained rows per gather work item
+constexpr int kGatherRows = 32;    // retained rows per gather work item (one workgroup each)
 constexpr int kCounterStride = 32; // words between per-job counters (one 128-byte line each)
 
 // Per-layer work description of one prefill launch group.
