@@ -831,30 +831,32 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 // Minus the reference logit of every row of every scored job, and the per-pass resets: the
 // status word and the job's slices' row sums ("not stored": NaN).
-// One workgroup per job.
+// Four workgroups per job, each with a quarter of the rows and of the resets.
 template <int NTH>
 __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
   constexpr int R = 128;
-  const int tid = threadIdx.x, job = blockIdx.x;
+  // four workgroups per job: workgroup q takes rows 32 q + [0, 32) and a quarter of the fill
+  constexpr int kParts = 4;
+  const int tid = threadIdx.x, job = blockIdx.x / kParts, q = blockIdx.x % kParts;
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, Hq = P.n_q_heads;
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
   const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
-  if (job == 0 && tid == 0) P.counters[0] = 0u;
+  if (blockIdx.x == 0 && tid == 0) P.counters[0] = 0u;
   {
     // every slice's row sums "not stored yet" (NaN): the consumers check them
     u32x4* st = reinterpret_cast<u32x4*>(P.stats + (size_t)job * P.n_slices * R);
     const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
-    for (int i = tid; i < P.n_slices * R / 4; i += 256) st[i] = nan4;
+    for (int i = tid + 256 * q; i < P.n_slices * R / 4; i += 256 * kParts) st[i] = nan4;
   }
   // 16 lanes per row, lane c taking 16-byte chunk c of the query, the row's own key and key 0
-  // (each load instruction reads whole 256-byte rows); 16 rows per pass, 8 passes
+  // (each load instruction reads whole 256-byte rows); 16 rows per pass, 2 passes
   const int c = tid & 15;
   const u32x4* ks = reinterpret_cast<const u32x4*>(ly.k + (size_t)(s * Hkv + h) * L * kHeadDim) + c;
-  u32x4 qa[8], da[8], sa[8];
-  bool valid[8];
+  u32x4 qa[2], da[2], sa[2];
+  bool valid[2];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    const int r = 16 * p + (tid >> 4);
+  for (int p = 0; p < 2; ++p) {
+    const int r = 32 * q + 16 * p + (tid >> 4);
     const int g = r / (NTH * 32), ii = r - g * (NTH * 32);
     valid[p] = g < G && ii < w;
     if (valid[p]) {
@@ -864,7 +866,7 @@ __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
     }
   }
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
+  for (int p = 0; p < 2; ++p) {
     float zd = 0.f, zs = 0.f;
     if (valid[p]) {
 #pragma unroll
@@ -885,7 +887,7 @@ __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
     zs += dppf<0x122>(zs);
     zd += dppf<0x121>(zd);
     zs += dppf<0x121>(zs);
-    if (c == 0) P.ncl[(size_t)job * R + 16 * p + (tid >> 4)] = valid[p] ? -fmaxf(zd, zs) : 0.f;
+    if (c == 0) P.ncl[(size_t)job * R + 32 * q + 16 * p + (tid >> 4)] = valid[p] ? -fmaxf(zd, zs) : 0.f;
   }
 }
 
@@ -2031,9 +2033,9 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
                     P.n_slices <= pipe_wg;
   profile_mark(kStageZero, false, stream);
   if (pipe) {
-    if (ntg == 1) prepare_kernel<1><<<n_jobs, 256, 0, st>>>(P);
-    else if (ntg == 2) prepare_kernel<2><<<n_jobs, 256, 0, st>>>(P);
-    else prepare_kernel<4><<<n_jobs, 256, 0, st>>>(P);
+    if (ntg == 1) prepare_kernel<1><<<n_jobs * 4, 256, 0, st>>>(P);
+    else if (ntg == 2) prepare_kernel<2><<<n_jobs * 4, 256, 0, st>>>(P);
+    else prepare_kernel<4><<<n_jobs * 4, 256, 0, st>>>(P);
   } else {
     const int n_lam = n_jobs * row_tiles * 32;
     const int n_cnt = kCounterStride * (1 + n_jobs);
