@@ -167,15 +167,35 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
           T[rs][i] = fmaf(e, x, T[rs][i]);
         }
   };
-  // one MFMA half interleaved with one exponential half: per group, one K fragment read, two
-  // MFMAs and eight VALU instructions
-  auto interleave = [&]() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  // one MFMA half (into a) interleaved with the exponentials of the other half (from v): step j
+  // reads K fragment j + 2, runs the two MFMAs of fragment j and the exponentials of two
+  // logits; a scheduling barrier closes each step, so every fragment is read two steps before
+  // its MFMAs.  Fragment j is (st, ks) = (j / 4, j % 4); logit u of v is (rs, ks, i) =
+  // (u / 16, (u / 4) % 4, u % 4).  The sums keep the order of valu_half.
+  auto interleaved = [&](int buf, int ks0, f32x4 (&a)[2][4], const f32x4 (&v)[2][4]) {
+    auto frag = [&](int j) {
+      const int key = 16 * (ks0 + (j & 3)) + l16, ch = 4 * (j >> 2) + lg;
+      return *reinterpret_cast<const bf16x8*>(&sK[buf][(key * 16 + (ch ^ (key & 15))) * 8]);
+    };
+    bf16x8 f[3];
+    f[0] = frag(0);
+    f[1] = frag(1);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
-      if (j < 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (j + 2 < 16) f[(j + 2) % 3] = frag(j + 2);
+      const int st = j >> 2, ks = j & 3;
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      a[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], f[j % 3], st == 0 ? z : a[0][ks], 0, 0, 0);
+      a[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], f[j % 3], st == 0 ? z : a[1][ks], 0, 0, 0);
+#pragma unroll
+      for (int uu = 0; uu < 2; ++uu) {
+        const int u = 2 * j + uu, rs = u >> 4, kv = (u >> 2) & 3, i = u & 3;
+        const float x = fmaf(v[rs][kv][i], sl2, ncs[rs][i]);
+        const float e = __builtin_amdgcn_exp2f(x);
+        Z[rs][i] += e;
+        T[rs][i] = fmaf(e, x, T[rs][i]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   f32x4 accA[2][4], accB[2][4];
@@ -187,11 +207,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
   __syncthreads();
   if (compute && n_bulk > 0) mfma_half(0, 0, accA);
   for (int kt = 0; kt < n_bulk; ++kt) {
-    if (compute) {
-      mfma_half(kt & 1, 4, accB);
-      valu_half(accA);
-      interleave();
-    }
+    if (compute) interleaved(kt & 1, 4, accB, accA);
     if (kt + 1 < n_tiles) {
       put((kt + 1) & 1);
       if (kt + 2 < n_tiles) fetch(kt + 2);
@@ -199,9 +215,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
     __syncthreads();   // tile kt + 1 published; every wave is done with tile kt's buffer
     if (compute) {
       if (kt + 1 < n_bulk) {
-        mfma_half((kt + 1) & 1, 0, accA);
-        valu_half(accB);
-        interleave();
+        interleaved((kt + 1) & 1, 0, accA, accB);
       } else {
         valu_half(accB);
       }
