@@ -148,15 +148,30 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void fullspan_rows_kernel(
 #pragma unroll
         for (int i = 0; i < 4; ++i) Z[rs][i] += __builtin_amdgcn_exp2f(fmaf(a[rs][ks][i], sl2, ncs[rs][i]));
   };
-  // one MFMA half interleaved with one exponential half: per group, one K fragment read, two
-  // MFMAs and six VALU instructions
-  auto interleave = [&]() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  // one MFMA half (into a) interleaved with the exponentials of the other half (from v): step j
+  // reads K fragment j + 2, runs the two MFMAs of fragment j and the exponentials of two
+  // logits, and a scheduling barrier closes the step.  Fragment j is (st, ks) = (j / 4, j % 4);
+  // logit u of v is (rs, ks, i) = (u / 16, (u / 4) % 4, u % 4), the order of valu_half.
+  auto interleaved = [&](int buf, int ks0, f32x4 (&a)[2][4], const f32x4 (&v)[2][4]) {
+    auto frag = [&](int j) {
+      return *reinterpret_cast<const bf16x8*>(&sK[buf][swz(16 * (ks0 + (j & 3)) + l16, 4 * (j >> 2) + lg)]);
+    };
+    bf16x8 f[3];
+    f[0] = frag(0);
+    f[1] = frag(1);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-      if (j < 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (j + 2 < 16) f[(j + 2) % 3] = frag(j + 2);
+      const int st = j >> 2, ks = j & 3;
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      a[0][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[0][st], f[j % 3], st == 0 ? z : a[0][ks], 0, 0, 0);
+      a[1][ks] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qa[1][st], f[j % 3], st == 0 ? z : a[1][ks], 0, 0, 0);
+#pragma unroll
+      for (int uu = 0; uu < 2; ++uu) {
+        const int u = 2 * j + uu, rs = u >> 4, kv = (u >> 2) & 3, i = u & 3;
+        Z[rs][i] += __builtin_amdgcn_exp2f(fmaf(v[rs][kv][i], sl2, ncs[rs][i]));
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   f32x4 accA[2][4], accB[2][4];
@@ -168,11 +183,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void fullspan_rows_kernel(
   __syncthreads();
   if (compute && n_bulk > 0) mfma_half(0, 0, accA);
   for (int kt = 0; kt < n_bulk; ++kt) {
-    if (compute) {
-      mfma_half(kt & 1, 4, accB);
-      valu_half(accA);
-      interleave();
-    }
+    if (compute) interleaved(kt & 1, 4, accB, accA);
     if (kt + 1 < n_tiles) {
       put((kt + 1) & 1);
       if (kt + 2 < n_tiles) fetch(kt + 2);
@@ -180,9 +191,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void fullspan_rows_kernel(
     __syncthreads();   // tile kt + 1 published; every wave is done with tile kt's buffer
     if (compute) {
       if (kt + 1 < n_bulk) {
-        mfma_half((kt + 1) & 1, 0, accA);
-        valu_half(accB);
-        interleave();
+        interleaved((kt + 1) & 1, 0, accA, accB);
       } else {
         valu_half(accB);
       }
@@ -316,13 +325,35 @@ __global__ __launch_bounds__(256, 2) void fullspan_cols_kernel(const PrefillLaun
         for (int ks = 0; ks < 2; ++ks) col[ks] += __builtin_amdgcn_exp2f(fmaf(a[rs][ks][i], sl2, -lm[i]));
     }
   };
-  auto interleave = [&]() {
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  // one MFMA half (row sub-tiles rs0 .. rs0 + 3 of tile `buf` into a) interleaved with the
+  // probabilities of the other half (rows vr0 .. vr0 + 3 of tile vit, from v): step j reads query
+  // fragment j + 2, runs the two MFMAs of fragment j and two logits' exponentials, and a
+  // scheduling barrier closes the step.  Fragment j is (st, rs) = (j / 4, j % 4); logit u of v is
+  // (rs, i, ks) = (u / 8, (u / 2) % 4, u % 2), the order of valu_half.
+  auto interleaved = [&](int buf, int rs0, f32x4 (&a)[4][2], int vit, int vr0, const f32x4 (&v)[4][2]) {
+    auto frag = [&](int j) {
+      return *reinterpret_cast<const bf16x8*>(&sQ[buf][swz(16 * (rs0 + (j & 3)) + l16, 4 * (j >> 2) + lg)]);
+    };
+    // the normalisers of the exponential half first (LDS reads complete in order)
+    f32x4 lm4[4];
+#pragma unroll
+    for (int vr = 0; vr < 4; ++vr) lm4[vr] = *reinterpret_cast<const f32x4*>(&sLam[vit % 3][16 * (vr0 + vr) + 4 * lg]);
+    bf16x8 f[3];
+    f[0] = frag(0);
+    f[1] = frag(1);
 #pragma unroll
     for (int j = 0; j < 16; ++j) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
-      if (j < 14) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (j + 2 < 16) f[(j + 2) % 3] = frag(j + 2);
+      const int st = j >> 2, rs = j & 3;
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      a[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[j % 3], kf[0][st], st == 0 ? z : a[rs][0], 0, 0, 0);
+      a[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f[j % 3], kf[1][st], st == 0 ? z : a[rs][1], 0, 0, 0);
+#pragma unroll
+      for (int uu = 0; uu < 2; ++uu) {
+        const int u = 2 * j + uu, vr = u >> 3, i = (u >> 1) & 3, ks = u & 1;
+        col[ks] += __builtin_amdgcn_exp2f(fmaf(v[vr][ks][i], sl2, -lm4[vr][i]));
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   f32x4 accA[4][2], accB[4][2];
@@ -373,14 +404,10 @@ __global__ __launch_bounds__(256, 2) void fullspan_cols_kernel(const PrefillLaun
   if (it < it_end) {
     mfma_half(it & 1, 0, accA);
     for (; it < it_end; ++it) {
-      mfma_half(it & 1, 4, accB);
-      valu_half(it, 0, accA);
-      interleave();
+      interleaved(it & 1, 4, accB, it, 0, accA);
       advance(it);
       if (it + 1 < it_end) {
-        mfma_half((it + 1) & 1, 0, accA);
-        valu_half(it, 4, accB);
-        interleave();
+        interleaved((it + 1) & 1, 0, accA, it, 4, accB);
       } else {
         valu_half(it, 4, accB);
       }
