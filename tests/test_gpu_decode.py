@@ -125,7 +125,8 @@ def _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers, Hq=32, H
     import torch
     G = Hq // Hkv
     recent = C // 2
-    ins = [[decode_steps(seed_workload, s, l, steps=steps) for s in range(B)] for l in range(n_layers)]
+    ins = [[decode_steps(seed_workload, s, l, steps=steps, n_q_heads=Hq, n_kv_heads=Hkv) for s in range(B)]
+           for l in range(n_layers)]
     n_close = 0
     for t in range(steps):
         p = L + t
@@ -198,4 +199,16 @@ def test_h2o_tova_composition():
     plan, state = prefill_state(rules_dec, C, L, B, n_layers)
     state["acc"] = [a if r == OP.H2O else None for a, r in zip(state["acc"], rules_dec)]
     n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers, seed_workload=13)
+    print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
+
+
+@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (16, 8), (32, 4)])
+def test_decode_group_sizes(Hq, Hkv):
+    """H2O decode on one layer and TOVA on the other at group sizes 1, 2 and 8 (the kernel's other
+    instances: 16 lanes per cache entry write each head's logit from lane (entry, head) mod 16)."""
+    B, L, steps, n_layers, C = 2, 384, 6, 2, 96
+    rules_dec = [OP.H2O, OP.TOVA]
+    plan, state = prefill_state(rules_dec, C, L, B, n_layers, Hq=Hq, Hkv=Hkv)
+    state["acc"] = [state["acc"][0], None]
+    n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers, Hq=Hq, Hkv=Hkv)
     print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
