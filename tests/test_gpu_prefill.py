@@ -137,6 +137,16 @@ def test_odd_window_and_group_shapes():
     run_case(rules, [150, 150], layers, window=20, pool_kernel=5, label="w20g2")
 
 
+@pytest.mark.parametrize("Hq,Hkv", [(8, 8), (32, 4)], ids=["g1", "g8"])
+def test_group_sizes_one_and_eight(Hq, Hkv):
+    """G = 1 (one row tile of 32, padded to four in the pipelined kernel) and G = 8 (eight row
+    tiles, the other scoring kernel), SnapKV and H2O, ragged L."""
+    L = 1100
+    rules = [OP.SNAPKV, OP.H2O]
+    layers = [[gen(7, s, l, L, Hq=Hq, Hkv=Hkv) for s in range(2)] for l in range(2)]
+    run_case(rules, [200, 200], layers, window=32, label=f"g{Hq // Hkv}")
+
+
 def test_full_route_8k_matches_oracle():
     """The 32-layer mixed route at L=8192 (StreamingLLM 0-1, SnapKV 2-15, H2O 16-27,
     SnapKV 28-31), PyramidKV-ramp budgets summing to 32 x 512, full size, every layer."""
