@@ -212,3 +212,14 @@ def test_decode_group_sizes(Hq, Hkv):
     state["acc"] = [state["acc"][0], None]
     n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers, Hq=Hq, Hkv=Hkv)
     print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
+
+
+def test_decode_capacity_past_1024():
+    """C = 1100: entries from 1024 on take the path that reads positions and accumulated scores
+    when visited (the first 1024 are requested right after the key stream)."""
+    B, L, steps, n_layers, C = 1, 1280, 4, 2, 1100
+    rules_dec = [OP.H2O, OP.TOVA]
+    plan, state = prefill_state(rules_dec, C, L, B, n_layers)
+    state["acc"] = [state["acc"][0], None]
+    n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers)
+    print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
