@@ -5,11 +5,12 @@ Test infrastructure only (see the package docstring).
 The plan of Eq. 1 (Section 3.1) gives each layer an operator and a nominal
 capacity b; this module is the operator side for the prefill phase, i.e. the
 prompt-compression handler of the common operator interface (Section 3.4).
-The retention rules are the ones the paper composes (Section 2.1): SnapKV
-scores prompt positions through a recent observation window, H2O keeps heavy
-hitters of accumulated attention, StreamingLLM keeps attention sinks plus
-recent tokens, and Full evicts nothing.  Section 3.3 fixes that SnapKV's
-capacity includes its observation window.
+The retention rules are the ones the paper composes (Section 2.1 names their
+families): SnapKV ranks prompt positions by the attention the last few prompt
+queries give them, H2O ranks by attention summed over queries, TOVA ranks by
+the attention of the newest query alone, StreamingLLM keeps the first few
+positions plus the newest ones, and Full evicts nothing.  Section 3.3 fixes
+that SnapKV's capacity includes its observation window.
 
 Notation per (sequence, layer): Hq query heads, Hkv KV heads, G = Hq / Hkv,
 head_dim d, context L, window w.  Arrays are float64 holding exact bf16 values.
@@ -29,10 +30,14 @@ Readings taken where the paper is silent:
     position as a query (the window is the whole prompt, so q holds L rows):
     S[j] is the group mean of the attention key j receives from all queries
     t >= j, H2O's accumulated attention over the prompt; same selection as H2O;
+  * TOVA (prefill): the prompt's last query (position L-1, the last row of
+    the window block) alone: S[j] is the group mean of its softmax over every
+    key 0..L-1; the top-b of [0, L) are kept, nothing is forced (Appendix C
+    runs the standalone TOVA baseline in both phases);
   * StreamingLLM: s0 = min(n_sink, b) first positions and the b-s0 last;
   * any rule with b >= L keeps all L positions;
-  * top-k order: value descending, then position ascending; the selection is
-    taken on the scores rounded to float32 (the kernel's precision);
+  * top-k order: value descending, then position ascending, on the float64
+    scores;
   * retained positions are returned in ascending order.
 """
 from __future__ import annotations
@@ -40,7 +45,7 @@ from __future__ import annotations
 import numpy as np
 
 FULL, STREAMING, SNAPKV, H2O = 0, 1, 2, 3
-TOVA = 4   # a decode rule only (oracle.decode.tova_step)
+TOVA = 4   # decode: oracle.decode.tova_step; prefill: the last query's attention
 H2O_FULL = 5
 RULE_NAMES = {FULL: "full", STREAMING: "streaming", SNAPKV: "snapkv", H2O: "h2o", TOVA: "tova",
               H2O_FULL: "h2o_full"}
@@ -136,6 +141,8 @@ def rule_layout(rule: int, b: int, L: int, w: int, n_sink: int = 4, num: int = 1
     if rule in (H2O, H2O_FULL):
         r = h2o_recent(b, num, den)
         return (L - r, b - r, L - r, L)
+    if rule == TOVA:
+        return (L, b, L, L)
     raise ValueError("unknown rule")
 
 
@@ -143,15 +150,16 @@ def evict_layer(rule: int, b: int, q_bits, k_bits, v_bits, *, window: int, pool_
                 n_sink: int = 4, recent_num: int = 1, recent_den: int = 2):
     """Prompt compression of one (sequence, layer).
 
-    q_bits [Hq, w, d] ([Hq, L, d] for H2O_FULL: every position's query), k_bits / v_bits
-    [Hkv, L, d] as bf16 bit patterns (uint16).
+    q_bits [Hq, w, d] ([Hq, L, d] for H2O_FULL: every position's query; TOVA reads its last
+    row, the query of position L-1), k_bits / v_bits [Hkv, L, d] as bf16 bit patterns (uint16).
     Returns dict:
       idx    [Hkv, b_eff] int64, ascending retained positions
       k_out, v_out [Hkv, b_eff, d] uint16 (bit copies of the retained rows)
       scores [Hkv, cand_end] float64 candidate scores (None for unscored rules)
       layout (cand_end, k, forced_lo, forced_hi) or None
-      acc    [Hkv, b_eff] float64: unpooled group-mean window score at each retained
-             position (H2O's accumulated attention; zeros for unscored rules)
+      acc    [Hkv, b_eff] float64: unpooled group-mean score at each retained position
+             (the window score for SnapKV / H2O, H2O's accumulated attention; the full-span
+             score for H2O_FULL; the last query's attention for TOVA; zeros for unscored rules)
     """
     k_bits = np.asarray(k_bits)
     Hkv, L, d = k_bits.shape
@@ -160,13 +168,15 @@ def evict_layer(rule: int, b: int, q_bits, k_bits, v_bits, *, window: int, pool_
         raise ValueError("window must be in [1, L]")
     b_eff = L if rule == FULL else min(b, L)
     layout = rule_layout(rule, b, L, w, n_sink, recent_num, recent_den)
-    scored = rule in (SNAPKV, H2O, H2O_FULL)
+    scored = rule in (SNAPKV, H2O, H2O_FULL, TOVA)
     if rule == H2O_FULL and np.asarray(q_bits).shape[1] != L:
         raise ValueError("H2O_FULL takes the queries of all L positions")
 
     A = None
     if scored:
         q = bf16_to_f64(q_bits)
+        if rule == TOVA:
+            q = q[:, -1:, :]                        # the query of position L-1 only
         k = bf16_to_f64(k_bits)
         G = q.shape[0] // Hkv
         A = window_scores(q, k)                     # [Hq, L]
@@ -193,8 +203,7 @@ def evict_layer(rule: int, b: int, q_bits, k_bits, v_bits, *, window: int, pool_
             else:
                 scores = S_unpooled[:, :cand_end]
             for h in range(Hkv):
-                # the decision is taken in float32, the precision the kernel scores in
-                sel = topk_positions(scores[h].astype(np.float32), kk)
+                sel = topk_positions(scores[h], kk)
                 rows.append(np.concatenate([sel, forced]))
         idx = np.stack(rows)
     assert idx.shape == (Hkv, b_eff)

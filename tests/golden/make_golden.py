@@ -22,9 +22,9 @@ def main():
              for avg in (128, 256, 512, 1024, 2048)}
     out = {
         "_source": "oracle.alloc.allocate (Eq. 3 with the b_min clamp and largest-remainder "
-                   "rounding, Section 3.3) on the 32-layer linear ramp 1024 -> 128; sweep points "
-                   "scale the completed 512-token vector to each total (Section 3.3), with b_min "
-                   "kept at 48",
+                   "rounding, Section 3.3) on the 32-layer linear ramp 1024 -> 128; each sweep "
+                   "point reuses the finished 512-average vector as its allocation weights at the "
+                   "new total (the budget-sweep rule of Section 3.3), b_min still 48",
         "b_min": B_MIN,
         "pyramid_512": b512,
         "sweep": sweep,

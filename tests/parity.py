@@ -52,8 +52,7 @@ def check_retained(idx_gpu, ora: dict, h: int, L: int, what=""):
     if ora["scores"] is None or k == 0:
         assert np.array_equal(idx_gpu, idx_ora), f"{what}: closed-form set differs"
         return 0
-    s32 = ora["scores"][h].astype(np.float32).astype(np.float64)
-    tau = np.sort(s32)[::-1][k - 1]
+    tau = np.sort(ora["scores"][h])[::-1][k - 1]
     amb = set(np.flatnonzero(np.abs(ora["scores"][h] - tau) <= RTOL * tau).tolist())
     sel_g = set(idx_gpu[:k].tolist())
     sel_o = set(idx_ora[:k].tolist())

@@ -269,10 +269,9 @@ def test_rule_outputs_are_valid_sets(rule, b, w):
             cand_end, kk, lo, hi = lay
             assert set(range(lo, hi)) <= set(r.tolist())
             if rule in (P.SNAPKV, P.H2O):
-                # the selected part is exactly the rank-count top-k of the float32 scores
-                s32 = out["scores"][h].astype(np.float32)
+                # the selected part is exactly the rank-count top-k of the float64 scores
                 sel = [x for x in r.tolist() if x < cand_end]
-                assert sel == P.topk_positions(s32, kk).tolist()
+                assert sel == rank_count_select(out["scores"][h].tolist(), kk)
 
 
 def test_planted_structure_is_found_on_the_single_layer_workload():
@@ -327,7 +326,7 @@ def test_full_span_brute_force_and_h2o_selection():
     r = b // 2
     np.testing.assert_allclose(out["scores"], S[:, :L - r], rtol=1e-12)
     for h in range(Hkv):
-        order = sorted(range(L - r), key=lambda j: (-np.float32(S[h, j]), j))[:b - r]
+        order = sorted(range(L - r), key=lambda j: (-S[h, j], j))[:b - r]
         assert out["idx"][h].tolist() == sorted(order) + list(range(L - r, L))
     with pytest.raises(ValueError):
         P.evict_layer(P.H2O_FULL, b, q[:, :5], k, v, window=5)   # needs every position's query
