@@ -14,15 +14,24 @@ from typing import Sequence
 
 from . import _abi
 from ._abi import FULL, STREAMING, SNAPKV, H2O, TOVA, H2O_FULL, PHASE_PREFILL, PHASE_DECODE, T_IDENTITY, T_PPL_CAP  # noqa: F401
+from ._abi import SCOPE_PREFILL, SCOPE_DECODE, SCOPE_BOTH, STATUS_TIMEOUT, STATUS_INVALID, STATUS_REPAIRED  # noqa: F401
 from ._abi import RkvError, check
 
-__all__ = ["Plan", "allocate_budgets", "evict_prefill", "decode_step", "prefill_check", "version",
-           "entropy_profile", "entropy_budgets",
-           "FULL", "STREAMING", "SNAPKV", "H2O", "TOVA", "H2O_FULL", "RkvError"]
+__all__ = ["Plan", "allocate_budgets", "evict_prefill", "decode_step", "decode_init_from_prefill", "prefill_check",
+           "rule_phases", "version", "entropy_profile", "entropy_budgets",
+           "FULL", "STREAMING", "SNAPKV", "H2O", "TOVA", "H2O_FULL", "SCOPE_PREFILL", "SCOPE_DECODE", "SCOPE_BOTH",
+           "RkvError"]
 
 
 def version() -> int:
     return _abi.lib().rkv_version()
+
+
+def rule_phases(rule: int) -> int:
+    """Phases operator `rule` declares (Section 3.4): bit 0 prefill, bit 1 decode."""
+    m = C.c_int32()
+    check(_abi.lib().rkv_rule_phases(int(rule), C.byref(m)))
+    return m.value
 
 
 def allocate_budgets(scores: Sequence[float], total: int, b_min: int, transform: int = T_IDENTITY):
@@ -64,6 +73,31 @@ class Plan:
         capacities equal the prefill ones."""
         budgets = allocate_budgets(weights, total, b_min, transform)
         return cls(rules_prefill, budgets, rules_decode, budgets if rules_decode is not None else None, **params)
+
+    @classmethod
+    def from_scoped_route(cls, rules, scopes, budgets, **params) -> "Plan":
+        """Plan of a completed route (Sections 3.1-3.2): layer l runs rules[l] at capacity
+        budgets[l] in the phases of scopes[l] (SCOPE_PREFILL, SCOPE_DECODE or SCOPE_BOTH, a tied
+        both-phase route) and FULL in the other phase; validated by rkv_plan_from_route."""
+        n = len(rules)
+        if not (len(scopes) == len(budgets) == n):
+            raise ValueError("per-layer lists must have equal length")
+        route = (_abi.RouteLayer * n)()
+        for i in range(n):
+            route[i] = _abi.RouteLayer(int(rules[i]), int(scopes[i]), int(budgets[i]))
+        p = dict(window=32, pool_kernel=7, n_sink=4, recent_num=1, recent_den=2)
+        p.update(params)
+        prm = _abi.Params(p["window"], p["pool_kernel"], p["n_sink"], p["recent_num"], p["recent_den"])
+        handle = C.c_void_p()
+        check(_abi.lib().rkv_plan_from_route(route, n, C.byref(prm), C.byref(handle)))
+        self = cls.__new__(cls)
+        self._h = handle
+        self.n_layers = n
+        self.params = prm
+        self.rules_prefill = [int(r) if s != SCOPE_DECODE else FULL for r, s in zip(rules, scopes)]
+        self.rules_decode = [int(r) if s != SCOPE_PREFILL else FULL for r, s in zip(rules, scopes)]
+        self.window = p["window"]
+        return self
 
     def to_bytes(self) -> bytes:
         """The plan's serialized record (rkv_plan_serialize)."""
@@ -139,14 +173,16 @@ def alloc_workspace(plan: Plan, batch, seq_len, n_q_heads, n_kv_heads, device="c
 
 
 def evict_prefill(plan: Plan, q_win, k, v, *, out=None, workspace=None, score_out=False, acc_out=False,
-                  stream=None):
+                  stream=None, check_status=False):
     """Compress every layer's prompt cache.
 
     q_win[l]: bf16 [B, Hq, w, d] ([B, Hq, L, d] for H2O_FULL layers; None allowed for FULL /
     STREAMING layers);
     k[l], v[l]: bf16 [B, Hkv, L, d].  Returns dict of per-layer lists: k_out, v_out (bf16
     [B, Hkv, n_l, d]), idx (int32 [B, Hkv, n_l], ascending), and optionally scores (fp32
-    [B, Hkv, L]) and acc (fp32 [B, Hkv, n_l]).  Outputs are valid after the stream syncs.
+    [B, Hkv, L]) and acc (fp32 [B, Hkv, n_l]).  Outputs are valid after the stream syncs and
+    when the workspace status word (prefill_check) has neither STATUS_TIMEOUT nor STATUS_INVALID;
+    check_status=True synchronises and raises RkvError otherwise.
     """
     import torch
     n = plan.n_layers
@@ -181,6 +217,12 @@ def evict_prefill(plan: Plan, q_win, k, v, *, out=None, workspace=None, score_ou
     call = PreparedPrefill(plan, q_win, k, v, out, workspace)
     call(stream)
     out["workspace"] = workspace
+    out["io"] = call   # keeps the marshalled pointer tables (decode_init_from_prefill uses them)
+    if check_status:
+        torch.cuda.synchronize(dev)
+        st = prefill_check(workspace)
+        if st & (STATUS_TIMEOUT | STATUS_INVALID):
+            raise RkvError(7, f"prefill status word {st:#x}: outputs invalid")
     return out
 
 
@@ -277,6 +319,35 @@ def entropy_profile(q, k, *, stream=None):
 def entropy_budgets(h, total: int, b_min: int = 32):
     """Entropy allocation: per-layer capacities from H_l by Eq. 3 with the identity transform."""
     return allocate_budgets([float(x) for x in h], total, b_min, T_IDENTITY)
+
+
+def decode_init_from_prefill(plan: Plan, prefill_out, state=None, *, stream=None):
+    """Prefill -> decode hand-off (Section 3.4, rkv_decode_init_from_prefill): the compacted prompt
+    cache of an evict_prefill result becomes the decode state of every layer whose decode operator
+    is not FULL.  `state` (per-layer lists "k_cache", "v_cache", "pos", "acc") is allocated when
+    None; entries of FULL-decode layers stay None, "acc" only for decode H2O layers.  Returns the
+    state; valid after the stream syncs."""
+    import torch
+    call = prefill_out["io"]
+    B, L, Hq, Hkv, d = (call.shape.batch, call.shape.seq_len, call.shape.n_q_heads, call.shape.n_kv_heads,
+                        call.shape.head_dim)
+    dev = call.device
+    caps = plan.retained_counts(L, PHASE_DECODE)
+    n = plan.n_layers
+    if state is None:
+        state = {"k_cache": [], "v_cache": [], "pos": [], "acc": []}
+        for l in range(n):
+            r, c = plan.rules_decode[l], caps[l]
+            live = r != FULL
+            state["k_cache"].append(torch.empty((B, Hkv, c, d), dtype=torch.bfloat16, device=dev) if live else None)
+            state["v_cache"].append(torch.empty((B, Hkv, c, d), dtype=torch.bfloat16, device=dev) if live else None)
+            state["pos"].append(torch.empty((B, Hkv, c), dtype=torch.int32, device=dev) if live else None)
+            state["acc"].append(torch.empty((B, Hkv, c), dtype=torch.float32, device=dev) if r == H2O else None)
+    st = _abi.DecodeState(_parr([_ptr(t) for t in state["k_cache"]]), _parr([_ptr(t) for t in state["v_cache"]]),
+                          _parr([_ptr(t) for t in state["pos"]]), _parr([_ptr(t) for t in state["acc"]]))
+    check(_abi.lib().rkv_decode_init_from_prefill(plan.handle, C.byref(call.shape), C.byref(call.io), C.byref(st),
+                                                  C.c_void_p(_stream_handle(stream, dev))))
+    return state
 
 
 def decode_step(plan: Plan, state, q, k, v, position: int, *, victim_out=None, stream=None):

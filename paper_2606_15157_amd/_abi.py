@@ -13,13 +13,15 @@ STATUS_NAMES = {0: "RKV_OK", 1: "RKV_ERR_INVALID_ARG", 2: "RKV_ERR_SHAPE", 3: "R
 
 FULL, STREAMING, SNAPKV, H2O, TOVA, H2O_FULL = 0, 1, 2, 3, 4, 5
 PHASE_PREFILL, PHASE_DECODE = 0, 1
+SCOPE_PREFILL, SCOPE_DECODE, SCOPE_BOTH = 0, 1, 2
 T_IDENTITY, T_PPL_CAP = 0, 1
+STATUS_TIMEOUT, STATUS_INVALID, STATUS_REPAIRED = 1, 2, 4
 
 EXPORTED = [
     "rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_destroy", "rkv_plan_num_layers",
-    "rkv_plan_serialize", "rkv_plan_deserialize",
+    "rkv_plan_serialize", "rkv_plan_deserialize", "rkv_rule_phases", "rkv_plan_from_route",
     "rkv_plan_retained_counts", "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check",
-    "rkv_decode_step", "rkv_entropy_workspace_size", "rkv_entropy_profile", "rkv_profile_enable", "rkv_profile_read", "rkv_last_error",
+    "rkv_decode_step", "rkv_decode_init_from_prefill", "rkv_entropy_workspace_size", "rkv_entropy_profile", "rkv_profile_enable", "rkv_profile_read", "rkv_last_error",
     "rkv_version",
 ]
 
@@ -27,6 +29,10 @@ EXPORTED = [
 class Layer(C.Structure):
     _fields_ = [("rule_prefill", C.c_int32), ("budget_prefill", C.c_int32),
                 ("rule_decode", C.c_int32), ("budget_decode", C.c_int32)]
+
+
+class RouteLayer(C.Structure):
+    _fields_ = [("rule", C.c_int32), ("scope", C.c_int32), ("budget", C.c_int32)]
 
 
 class Params(C.Structure):
@@ -69,6 +75,8 @@ def lib():
         L.rkv_allocate_budgets.argtypes = [C.POINTER(C.c_double), C.c_int32, C.c_int32, C.c_int64, C.c_int32,
                                            C.POINTER(C.c_int32)]
         L.rkv_plan_create.argtypes = [C.POINTER(Layer), C.c_int32, C.POINTER(Params), C.POINTER(C.c_void_p)]
+        L.rkv_rule_phases.argtypes = [C.c_int32, C.POINTER(C.c_int32)]
+        L.rkv_plan_from_route.argtypes = [C.POINTER(RouteLayer), C.c_int32, C.POINTER(Params), C.POINTER(C.c_void_p)]
         L.rkv_plan_destroy.argtypes = [C.c_void_p]
         L.rkv_plan_destroy.restype = None
         L.rkv_plan_num_layers.argtypes = [C.c_void_p, C.POINTER(C.c_int32)]
@@ -81,6 +89,8 @@ def lib():
         L.rkv_prefill_check.argtypes = [C.c_void_p, C.c_size_t, C.POINTER(C.c_int32)]
         L.rkv_decode_step.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(DecodeState), C.POINTER(DecodeInput),
                                       C.c_int32, C.c_void_p]
+        L.rkv_decode_init_from_prefill.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(PrefillIO),
+                                                   C.POINTER(DecodeState), C.c_void_p]
         L.rkv_entropy_workspace_size.argtypes = [C.POINTER(Shape), C.c_int32, C.c_int32, C.POINTER(C.c_size_t)]
         L.rkv_entropy_profile.argtypes = [C.POINTER(Shape), C.c_int32, C.c_int32, C.POINTER(C.c_void_p),
                                           C.POINTER(C.c_void_p), C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -93,6 +103,7 @@ def lib():
         for name in ("rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_num_layers", "rkv_plan_retained_counts",
                      "rkv_plan_serialize", "rkv_plan_deserialize",
                      "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check", "rkv_decode_step",
+                     "rkv_rule_phases", "rkv_plan_from_route", "rkv_decode_init_from_prefill",
                      "rkv_entropy_workspace_size", "rkv_entropy_profile",
                      "rkv_profile_enable", "rkv_profile_read", "rkv_version"):
             getattr(L, name).restype = C.c_int

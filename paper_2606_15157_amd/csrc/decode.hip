@@ -7,8 +7,8 @@
 // evicted and the new token takes its slot.  TOVA: the same probabilities; an entry's score is
 // their group mean at this step alone, every entry (the new one included) is a candidate, and
 // the smallest score is evicted (ties: smallest position).  StreamingLLM: the oldest non-sink
-// slot is replaced.  Keys are read with four lanes per 256-byte row, 64 contiguous bytes per
-// load instruction and row.
+// slot is replaced.  Keys are read with 16 lanes per 256-byte row (16 bytes each), so one
+// wave's load instruction reads four whole rows.
 #include <hip/hip_runtime.h>
 
 #include "rkv_internal.h"

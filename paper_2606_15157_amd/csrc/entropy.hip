@@ -63,7 +63,7 @@ __global__ __launch_bounds__(64 * (G > 4 ? G : 4), 2) void entropy_rows_kernel(c
   const int t0 = L - n_q + i0;             // its position
   const uint16_t* qrows = E.q[layer] + (size_t)(b * Hq + hq) * n_q * kHeadDim;
   const uint16_t* khead = E.k[layer] + (size_t)(b * Hkv + h) * L * kHeadDim;
-  if (blockIdx.x == 0 && tid == 0) E.status[0] = 0u;
+  if (blockIdx.x == 0 && tid == 0 && E.first_group) E.status[0] = 0u;   // once per call: later launches OR into it
 
   // ---- per-row reference: lanes 0..31 of each wave take one row each
   if (compute && lane < kEntRows) {

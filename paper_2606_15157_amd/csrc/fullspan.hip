@@ -437,7 +437,7 @@ __global__ __launch_bounds__(256, 2) void fullspan_cols_kernel(const PrefillLaun
 
 int launch_fullspan(const PrefillLaunch& P, void* stream) {
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int n_full = P.batch * (P.n_scored - P.n_window) * P.n_kv_heads;
+  const int n_full = P.batch * P.n_full * P.n_kv_heads;
   if (n_full <= 0) return 0;
   const int L = P.seq_len, G = P.group;
   const unsigned g_rows = (unsigned)(n_full * ((L + kFsRows - 1) / kFsRows));

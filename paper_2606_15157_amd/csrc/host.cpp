@@ -18,6 +18,21 @@ thread_local std::string g_error;
 size_t round_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 bool rule_valid(int32_t r) { return r >= RKV_FULL && r <= RKV_H2O_FULL; }
+
+// The phases each operator's adapter declares (Section 3.4): bit 0 prefill, bit 1 decode.
+// SnapKV and full-span H2O rank prompt positions by prompt queries, so they compress the prompt
+// only; the others also have an incremental-update handler.
+int32_t rule_phase_mask(int32_t r) {
+  switch (r) {
+    case RKV_SNAPKV:
+    case RKV_H2O_FULL: return 1;
+    case RKV_FULL:
+    case RKV_STREAMING:
+    case RKV_H2O:
+    case RKV_TOVA: return 3;
+    default: return 0;
+  }
+}
 constexpr int32_t kPlanMagic = 0x50564b52;   // "RKVP" as little-endian bytes
 constexpr int32_t kPlanFormat = 1;
 
@@ -31,7 +46,8 @@ struct Layout {
 Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L, bool want_scores = true) {
   Layout o{};
   const int32_t b = ly.budget_prefill;
-  o.scored = (ly.rule_prefill == RKV_SNAPKV || ly.rule_prefill == RKV_H2O || ly.rule_prefill == RKV_H2O_FULL) ? 1 : 0;
+  o.scored = (ly.rule_prefill == RKV_SNAPKV || ly.rule_prefill == RKV_H2O || ly.rule_prefill == RKV_H2O_FULL ||
+              ly.rule_prefill == RKV_TOVA) ? 1 : 0;
   if (ly.rule_prefill == RKV_FULL || b >= L) {
     o.n_keep = L; o.all = 1; o.cand_end = 0; o.k_sel = 0; o.forced_lo = 0; o.forced_hi = L;
     if (o.scored && !want_scores) o.scored = 0;
@@ -55,6 +71,10 @@ Layout prefill_layout(const rkv_layer& ly, const rkv_params& p, int32_t L, bool 
       o.cand_end = L - r; o.k_sel = b - r; o.forced_lo = L - r; o.forced_hi = L;
       break;
     }
+    case RKV_TOVA:
+      // every position is a candidate, nothing is forced
+      o.cand_end = L; o.k_sel = b; o.forced_lo = L; o.forced_hi = L;
+      break;
     default: break;
   }
   if (o.scored && o.k_sel == 0 && !want_scores) o.scored = 0;
@@ -82,8 +102,17 @@ int row_tiles(const rkv_params& p, const rkv_shape* s) {
 int kernel_row_tiles(int nt) { return nt <= 4 ? 4 : 8; }
 
 struct Group {
-  int l0, l1, n_scored, n_full;   // n_full: scored layers with full-span accumulation
+  int l0, l1, n_scored, n_full, n_tova;   // scored layers; of which full-span H2O, TOVA
 };
+
+// Scoring class of a layer in a launch group: 0 window-scored, 1 full-span H2O, 2 TOVA,
+// 3 not scored.  Slots follow this order.
+int score_class(const rkv_layer& ly, const Layout& lo) {
+  if (!lo.scored) return 3;
+  if (ly.rule_prefill == RKV_H2O_FULL) return 1;
+  if (ly.rule_prefill == RKV_TOVA) return 2;
+  return 0;
+}
 
 // Test hook: RKV_FORCE_TWO_PASS=1 selects the two-pass scoring kernel (normally used for prompts
 // too long for the single-pass one) so that it can be checked on short prompts too.
@@ -108,13 +137,14 @@ std::vector<Group> layer_groups(const rkv_plan* plan, int32_t L) {
   int n = (int)plan->layers.size();
   for (int l0 = 0; l0 < n; l0 += rkv::kMaxLayersPerLaunch) {
     int l1 = std::min(n, l0 + rkv::kMaxLayersPerLaunch);
-    int sc = 0, nf = 0;
+    int sc = 0, nf = 0, nt = 0;
     for (int l = l0; l < l1; ++l) {
-      const int scd = prefill_layout(plan->layers[l], plan->params, L).scored;
-      sc += scd;
-      nf += scd && plan->layers[l].rule_prefill == RKV_H2O_FULL;
+      const int cls = score_class(plan->layers[l], prefill_layout(plan->layers[l], plan->params, L));
+      sc += cls < 3;
+      nf += cls == 1;
+      nt += cls == 2;
     }
-    g.push_back({l0, l1, sc, nf});
+    g.push_back({l0, l1, sc, nf, nt});
   }
   return g;
 }
@@ -126,7 +156,8 @@ size_t group_workspace(const rkv_plan* plan, const rkv_shape* s, const Group& g)
   const int n_jobs = s->batch * g.n_scored * s->n_kv_heads;
   const int n_slices = (L + rkv::kSlice - 1) / rkv::kSlice;
   return rkv::prefill_workspace_layout(n_jobs, n_slices, nt * 32, L, G, plan->params.pool_kernel / 2,
-                                       s->batch * g.n_full * s->n_kv_heads).total;
+                                       s->batch * g.n_full * s->n_kv_heads,
+                                       s->batch * g.n_tova * s->n_kv_heads).total;
 }
 
 }  // namespace
@@ -162,7 +193,7 @@ int fail(int status, const std::string& msg) {
 void clear_error() { g_error.clear(); }
 
 PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half,
-                                          int n_full_jobs) {
+                                          int n_full_jobs, int n_tova_jobs) {
   PrefillWorkspace w{};
   size_t off = 0;
   w.counters = off;
@@ -175,6 +206,10 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
   off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
   w.lamf = off;
   off = round_up(off + sizeof(float) * (size_t)n_full_jobs * group * seq_len, 256);
+  w.tz = off;
+  off = round_up(off + sizeof(float) * (size_t)n_tova_jobs * group * seq_len, 256);
+  w.tstat = off;
+  off = round_up(off + sizeof(float) * 2 * (size_t)n_tova_jobs * n_slices * group, 256);
   w.S = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * seq_len, 256);
   w.Su = off;
@@ -312,10 +347,10 @@ int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params*
       return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": unknown rule");
     if (ly.budget_prefill < 0 || ly.budget_decode < 0)
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": negative budget");
+    if (!(rule_phase_mask(ly.rule_prefill) & 1))
+      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": operator not declared for prefill");
     if (ly.rule_decode == RKV_SNAPKV)
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": SnapKV compresses the prompt only, not valid in decode");
-    if (ly.rule_prefill == RKV_TOVA)
-      return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": TOVA is a decode operator, not valid in prefill");
     if (ly.rule_decode == RKV_H2O_FULL)
       return rkv::fail(RKV_ERR_PLAN, "layer " + std::to_string(l) + ": full-span accumulation is a prefill rule (decode uses RKV_H2O)");
     if (ly.rule_decode == RKV_TOVA && ly.budget_decode < 1)
@@ -331,6 +366,40 @@ int rkv_plan_create(const rkv_layer* layers, int32_t n_layers, const rkv_params*
   plan->params = p;
   *out = plan;
   return RKV_OK;
+}
+
+int rkv_rule_phases(int32_t rule, int32_t* phase_mask) {
+  rkv::clear_error();
+  if (!phase_mask) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (!rule_valid(rule)) return rkv::fail(RKV_ERR_INVALID_ARG, "unknown rule");
+  *phase_mask = rule_phase_mask(rule);
+  return RKV_OK;
+}
+
+int rkv_plan_from_route(const rkv_route_layer* route, int32_t n_layers, const rkv_params* params, rkv_plan** out) {
+  rkv::clear_error();
+  if (!route || !params || !out) return rkv::fail(RKV_ERR_INVALID_ARG, "null pointer");
+  if (n_layers < 1) return rkv::fail(RKV_ERR_INVALID_ARG, "n_layers must be >= 1");
+  std::vector<rkv_layer> layers((size_t)n_layers);
+  for (int l = 0; l < n_layers; ++l) {
+    const rkv_route_layer& r = route[l];
+    const std::string at = "layer " + std::to_string(l) + ": ";
+    if (!rule_valid(r.rule)) return rkv::fail(RKV_ERR_INVALID_ARG, at + "unknown rule");
+    if (r.scope < RKV_SCOPE_PREFILL || r.scope > RKV_SCOPE_BOTH) return rkv::fail(RKV_ERR_INVALID_ARG, at + "unknown scope");
+    // the phases the scope activates must all be declared by the operator (for BOTH: the
+    // intersection of the prefill and decode declarations)
+    const int32_t need = r.scope == RKV_SCOPE_PREFILL ? 1 : (r.scope == RKV_SCOPE_DECODE ? 2 : 3);
+    if ((rule_phase_mask(r.rule) & need) != need)
+      return rkv::fail(RKV_ERR_PLAN, at + (r.scope == RKV_SCOPE_BOTH
+                                               ? "a tied both-phase route needs an operator declared for both phases"
+                                               : "operator not declared for the scope's phase"));
+    const bool pre = need & 1, dec = need & 2;
+    layers[l].rule_prefill = pre ? r.rule : RKV_FULL;
+    layers[l].budget_prefill = pre ? r.budget : 0;
+    layers[l].rule_decode = dec ? r.rule : RKV_FULL;
+    layers[l].budget_decode = dec ? r.budget : 0;
+  }
+  return rkv_plan_create(layers.data(), n_layers, params, out);
 }
 
 void rkv_plan_destroy(rkv_plan* plan) { delete plan; }
@@ -436,18 +505,22 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
   const int n = (int)plan->layers.size();
   const int G = shape->n_q_heads / shape->n_kv_heads;
   const int nt = row_tiles(p, shape);
-  bool any_scored = false;
+  bool any_window = false, any_g_bound = false;
   for (int l = 0; l < n; ++l) {
     Layout lo = prefill_layout(plan->layers[l], p, L);
-    any_scored |= lo.scored != 0;
+    const int cls = score_class(plan->layers[l], lo);
+    any_window |= cls == 0;
+    any_g_bound |= cls == 1 || cls == 2;
     if (!io->k[l] || !io->v[l]) return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null k or v");
     if (!io->k_out[l] || !io->v_out[l] || !io->idx_out[l])
       if (lo.n_keep > 0) return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null output");
     if (lo.scored && (!io->q_win || !io->q_win[l]))
       return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": scoring rule needs q_win");
   }
-  if (any_scored && nt > rkv::kMaxRowTiles)
+  if (any_window && nt > rkv::kMaxRowTiles)
     return rkv::fail(RKV_ERR_UNSUPPORTED, "G * ceil(window / 32) must be <= 8");
+  if (any_g_bound && G != 1 && G != 2 && G != 4 && G != 8)
+    return rkv::fail(RKV_ERR_UNSUPPORTED, "TOVA and full-span H2O layers need n_q_heads / n_kv_heads in {1, 2, 4, 8}");
   size_t need = 256;
   std::vector<Group> groups = layer_groups(plan, L);
   for (const Group& g : groups) need = std::max(need, group_workspace(plan, shape, g));
@@ -457,9 +530,12 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     return rkv::fail(RKV_ERR_WORKSPACE, "workspace too small: need " + std::to_string(need) + " bytes");
 
   const int ktiles = kernel_row_tiles(nt);
+  bool first = true;
   for (const Group& g : groups) {
     rkv::PrefillLaunch P;
     std::memset(&P, 0, sizeof(P));
+    P.first_group = first ? 1 : 0;
+    first = false;
     P.n_layers = g.l1 - g.l0;
     P.batch = shape->batch;
     P.seq_len = L;
@@ -479,24 +555,23 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     // scoring kernel looks a slot's tensors up with one load)
     int order[rkv::kMaxLayersPerLaunch];
     Layout lays[rkv::kMaxLayersPerLaunch];
-    int n_window = 0;
+    int n_class[4] = {0, 0, 0, 0};
     {
-      // window-scored layers, then full-span H2O, then the unscored ones
+      // window-scored layers, then full-span H2O, then TOVA, then the unscored ones
       int n = 0;
-      for (int pass = 0; pass < 3; ++pass)
+      for (int pass = 0; pass < 4; ++pass)
         for (int i = 0; i < P.n_layers; ++i) {
           const int l = g.l0 + i;
           const bool want = (io->score_out && io->score_out[l]) || (io->acc_out && io->acc_out[l]);
           const Layout lo = prefill_layout(plan->layers[l], p, L, want);
-          const bool full = plan->layers[l].rule_prefill == RKV_H2O_FULL;
-          const int cls = !lo.scored ? 2 : (full ? 1 : 0);
-          if (cls == pass) {
+          if (score_class(plan->layers[l], lo) == pass) {
             lays[n] = lo;
             order[n++] = i;
-            n_window += pass == 0;
+            ++n_class[pass];
           }
         }
     }
+    const int n_window = n_class[0];
     for (int i = 0; i < P.n_layers; ++i) {
       const int l = g.l0 + order[i];
       const Layout& lo = lays[i];
@@ -526,6 +601,7 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     }
     P.n_scored = slot;
     P.n_window = n_window;
+    P.n_full = n_class[1];
     P.n_gather = n_gather;
     P.gather_item0[0] = 0;
     for (int i = 0; i < n_gather; ++i) {
@@ -534,15 +610,18 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     }
     P.want_unpooled = want_unpooled ? 1 : 0;
     const int n_jobs = shape->batch * slot * shape->n_kv_heads;
-    const int n_full_jobs = shape->batch * (slot - n_window) * shape->n_kv_heads;
+    const int n_full_jobs = shape->batch * n_class[1] * shape->n_kv_heads;
+    const int n_tova_jobs = shape->batch * n_class[2] * shape->n_kv_heads;
     rkv::PrefillWorkspace W = rkv::prefill_workspace_layout(n_jobs, P.n_slices, ktiles * 32, L, G, P.pool_half,
-                                                            n_full_jobs);
+                                                            n_full_jobs, n_tova_jobs);
     char* base = (char*)ws;
     P.counters = (uint32_t*)(base + W.counters);
     P.stats = (float*)(base + W.stats);
     P.lam = (float*)(base + W.lam);
     P.ncl = (float*)(base + W.ncl);
     P.lamf = (float*)(base + W.lamf);
+    P.tz = (float*)(base + W.tz);
+    P.tstat = (float*)(base + W.tstat);
     P.S = (float*)(base + W.S);
     P.Su = (float*)(base + W.Su);
     P.edge = (float*)(base + W.edge);
@@ -599,12 +678,14 @@ int rkv_entropy_profile(const rkv_shape* shape, int32_t n_layers, int32_t n_q, c
   if (G != 1 && G != 2 && G != 4 && G != 8)
     return rkv::fail(RKV_ERR_UNSUPPORTED, "entropy profile needs n_q_heads / n_kv_heads in {1, 2, 4, 8}");
   const size_t per_layer = (size_t)shape->batch * shape->n_q_heads * n_q;
+  for (int l = 0; l < n_layers; ++l)
+    if (!q[l] || !k[l]) return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null q or k");
   for (int l0 = 0; l0 < n_layers; l0 += rkv::kMaxLayersPerLaunch) {
     rkv::EntropyLaunch E;
     std::memset(&E, 0, sizeof(E));
     E.n_layers = std::min(n_layers - l0, rkv::kMaxLayersPerLaunch);
+    E.first_group = l0 == 0 ? 1 : 0;
     for (int i = 0; i < E.n_layers; ++i) {
-      if (!q[l0 + i] || !k[l0 + i]) return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l0 + i) + ": null q or k");
       E.q[i] = (const uint16_t*)q[l0 + i];
       E.k[i] = (const uint16_t*)k[l0 + i];
     }
@@ -634,13 +715,31 @@ int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_deco
     return rkv::fail(RKV_ERR_INVALID_ARG, "state and input arrays are required");
   const rkv_params& p = plan->params;
   const int n = (int)plan->layers.size();
+  const int G = shape->n_q_heads / shape->n_kv_heads;
+  // every layer is checked before anything is enqueued
+  bool any = false;
+  for (int l = 0; l < n; ++l) {
+    const rkv_layer& ly = plan->layers[l];
+    if (ly.rule_decode == RKV_FULL) continue;
+    any = true;
+    const int C = ly.budget_decode;
+    if (position < C) return rkv::fail(RKV_ERR_SHAPE, "position must be >= the layer's capacity");
+    const bool need_acc = ly.rule_decode == RKV_H2O;
+    if (!state->k_cache[l] || !state->v_cache[l] || !state->pos[l] || (need_acc && (!state->acc || !state->acc[l])) ||
+        !input->q[l] || !input->k[l] || !input->v[l])
+      return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null decode buffer");
+    if ((size_t)(G + 1) * (C + 1) * sizeof(float) > 150 * 1024)
+      return rkv::fail(RKV_ERR_UNSUPPORTED, "decode capacity too large for one workgroup's LDS");
+  }
+  if (any && G != 1 && G != 2 && G != 4 && G != 8)
+    return rkv::fail(RKV_ERR_UNSUPPORTED, "decode needs n_q_heads / n_kv_heads in {1, 2, 4, 8}");
   for (int l0 = 0; l0 < n; l0 += rkv::kMaxLayersPerLaunch) {
     rkv::DecodeLaunch D;
     std::memset(&D, 0, sizeof(D));
     D.batch = shape->batch;
     D.n_q_heads = shape->n_q_heads;
     D.n_kv_heads = shape->n_kv_heads;
-    D.group = shape->n_q_heads / shape->n_kv_heads;
+    D.group = G;
     D.position = position;
     D.n_sink = p.n_sink;
     D.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
@@ -649,11 +748,7 @@ int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_deco
       const rkv_layer& ly = plan->layers[l];
       if (ly.rule_decode == RKV_FULL) continue;
       const int C = ly.budget_decode;
-      if (position < C) return rkv::fail(RKV_ERR_SHAPE, "position must be >= the layer's capacity");
       const bool need_acc = ly.rule_decode == RKV_H2O;
-      if (!state->k_cache[l] || !state->v_cache[l] || !state->pos[l] || (need_acc && (!state->acc || !state->acc[l])) ||
-          !input->q[l] || !input->k[l] || !input->v[l])
-        return rkv::fail(RKV_ERR_INVALID_ARG, "layer " + std::to_string(l) + ": null decode buffer");
       rkv::DecodeLayer& d = D.layer[cnt++];
       d.k_cache = (uint16_t*)state->k_cache[l];
       d.v_cache = (uint16_t*)state->v_cache[l];
@@ -669,13 +764,59 @@ int rkv_decode_step(const rkv_plan* plan, const rkv_shape* shape, const rkv_deco
       max_cap = std::max(max_cap, C);
     }
     if (!cnt) continue;
-    const int G = shape->n_q_heads / shape->n_kv_heads;
-    if (G != 1 && G != 2 && G != 4 && G != 8)
-      return rkv::fail(RKV_ERR_UNSUPPORTED, "decode needs n_q_heads / n_kv_heads in {1, 2, 4, 8}");
-    if ((size_t)(G + 1) * (max_cap + 1) * sizeof(float) > 150 * 1024)
-      return rkv::fail(RKV_ERR_UNSUPPORTED, "decode capacity too large for one workgroup's LDS");
     D.n_layers = cnt;
     int err = rkv::launch_decode(D, max_cap, stream);
+    if (err) return rkv::fail(RKV_ERR_HIP, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)err));
+  }
+  return RKV_OK;
+}
+
+int rkv_decode_init_from_prefill(const rkv_plan* plan, const rkv_shape* shape, const rkv_prefill_io* prefill,
+                                 const rkv_decode_state* state, void* stream) {
+  rkv::clear_error();
+  if (!plan || !prefill || !state) return rkv::fail(RKV_ERR_INVALID_ARG, "null plan, prefill io or state");
+  int st = validate_shape(shape);
+  if (st) return st;
+  const int n = (int)plan->layers.size();
+  const int L = shape->seq_len;
+  const int64_t rows = (int64_t)shape->batch * shape->n_kv_heads;
+  std::vector<rkv::CopyTask> tasks;
+  for (int l = 0; l < n; ++l) {
+    const rkv_layer& ly = plan->layers[l];
+    if (ly.rule_decode == RKV_FULL) continue;
+    const std::string at = "layer " + std::to_string(l) + ": ";
+    const Layout lo = prefill_layout(ly, plan->params, L);
+    const int C = ly.budget_decode;
+    if (lo.n_keep != C)
+      return rkv::fail(RKV_ERR_SHAPE, at + "decode capacity " + std::to_string(C) + " differs from the prefill retained count " +
+                                          std::to_string(lo.n_keep));
+    if (!prefill->k_out || !prefill->v_out || !prefill->idx_out || !prefill->k_out[l] || !prefill->v_out[l] ||
+        !prefill->idx_out[l])
+      return rkv::fail(RKV_ERR_INVALID_ARG, at + "null prefill output");
+    if (!state->k_cache || !state->v_cache || !state->pos || !state->k_cache[l] || !state->v_cache[l] || !state->pos[l])
+      return rkv::fail(RKV_ERR_INVALID_ARG, at + "null decode buffer");
+    const int64_t kv_bytes = rows * C * rkv::kHeadDim * 2, pos_bytes = rows * C * 4;
+    tasks.push_back({prefill->k_out[l], state->k_cache[l], kv_bytes});
+    tasks.push_back({prefill->v_out[l], state->v_cache[l], kv_bytes});
+    tasks.push_back({prefill->idx_out[l], state->pos[l], pos_bytes});
+    if (ly.rule_decode == RKV_H2O) {
+      if (!state->acc || !state->acc[l]) return rkv::fail(RKV_ERR_INVALID_ARG, at + "decode H2O needs acc");
+      const bool scores = ly.rule_prefill != RKV_FULL && ly.rule_prefill != RKV_STREAMING;
+      const float* src = prefill->acc_out ? prefill->acc_out[l] : nullptr;
+      if (scores && !src)
+        return rkv::fail(RKV_ERR_INVALID_ARG, at + "decode H2O is seeded from the prefill acc_out, which is null");
+      tasks.push_back({src, state->acc[l], pos_bytes});   // null source: zero seed
+    }
+  }
+  // drop copies onto themselves (a caller decoding in the prefill outputs)
+  tasks.erase(std::remove_if(tasks.begin(), tasks.end(), [](const rkv::CopyTask& t) { return t.src == t.dst; }),
+              tasks.end());
+  for (size_t t0 = 0; t0 < tasks.size(); t0 += rkv::kMaxCopies) {
+    rkv::CopyLaunch C;
+    std::memset(&C, 0, sizeof(C));
+    C.n_tasks = (int32_t)std::min<size_t>(rkv::kMaxCopies, tasks.size() - t0);
+    for (int i = 0; i < C.n_tasks; ++i) C.task[i] = tasks[t0 + i];
+    int err = rkv::launch_copies(C, stream);
     if (err) return rkv::fail(RKV_ERR_HIP, std::string("kernel launch failed: ") + hipGetErrorString((hipError_t)err));
   }
   return RKV_OK;

@@ -109,10 +109,12 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 // for all memory operations (earlier stores included) before every one of those stores.
 __device__ __forceinline__ void loads_done() { __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8)); }
 
-// Zeroes the counters and marks every per-row normaliser "not written" (NaN).
-__global__ void reset_counters(uint32_t* counters, int n, uint32_t* lam, int n_lam) {
+// Zeroes the counters (the status word at counters[0] only in the call's first launch group, so
+// that it covers the whole call) and marks every per-row normaliser "not written" (NaN).
+__global__ void reset_counters(uint32_t* counters, int n, uint32_t* lam, int n_lam, int clear_status) {
   const int i0 = blockIdx.x * blockDim.x + threadIdx.x, stride = gridDim.x * blockDim.x;
-  for (int i = i0; i < n; i += stride) counters[i] = 0u;
+  for (int i = i0; i < n; i += stride)
+    if (i > 0 || clear_status) counters[i] = 0u;
   for (int i = i0; i < n_lam; i += stride) lam[i] = 0xffffffffu;
 }
 
@@ -457,25 +459,39 @@ __device__ __forceinline__ void wait_vmcnt() {
 // inline assembly so that the compiler does not conservatively wait for it before unrelated
 // LDS reads; the issuing wave waits for it explicitly (vmcnt) before a barrier hands the data
 // on.  lds_base must be wave-uniform.
+// M0 is reserved by the compiler (it may hold a value across this statement), so the
+// assembly saves it in a scratch SGPR and restores it after the DMA instruction has read it.
 __device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "s"(lds_base)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %2\n\ts_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(lds_base)
+      : "memory");
 }
 // The same with a wave-uniform base address in SGPRs and a 32-bit per-lane byte offset.
 __device__ __forceinline__ void dma16s(const void* base, uint32_t off, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "s"(lds_base)
-               : "memory", "m0");
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"(lds_base)
+      : "memory");
 }
 // Two of those 4 KiB apart: [base + off] -> lds_base and [base + 4096 + off] -> lds_base + 4096
 // (+ 16 lane).  The instruction offset applies to the global and to the LDS address alike, so
 // one base and one M0 value serve both.
 __device__ __forceinline__ void dma16s_pair(const char* base, uint32_t off, uint32_t lds_base) {
+  uint32_t saved;
   asm volatile(
-      "s_mov_b32 m0, %2\n\ts_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, %1 offset:-4096\n\t"
-      "global_load_lds_dwordx4 %0, %1" ::"v"(off),
-      "s"(base + 4096), "s"(lds_base + 4096u)
-      : "memory", "m0");
+      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2 offset:-4096\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base + 4096), "s"(lds_base + 4096u)
+      : "memory");
 }
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
@@ -841,7 +857,8 @@ __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, Hq = P.n_q_heads;
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
   const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
-  if (blockIdx.x == 0 && tid == 0) P.counters[0] = 0u;
+  if (blockIdx.x == 0 && tid == 0 && P.first_group) P.counters[0] = 0u;   // once per call
+  if (q == 0 && tid == 0) P.counters[(size_t)kCounterStride * (1 + job) + 1] = 0u;   // the job's repair flag
   {
     // every slice's row sums "not stored yet" (NaN): the consumers check them
     u32x4* st = reinterpret_cast<u32x4*>(P.stats + (size_t)job * P.n_slices * R);
@@ -909,7 +926,6 @@ __device__ __forceinline__ bf16x8 frag16(const uint16_t* base, int row, int chun
 template <int NTH>
 __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const PrefillLaunch P, int n_wg) {
   constexpr int R = 128;
-  constexpr int NG = 4 / NTH;
   __shared__ __attribute__((aligned(16))) uint16_t sQ[2][R * kHeadDim];
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kSlice * kHeadDim];
   __shared__ __attribute__((aligned(16))) float sNcl[2][R];
@@ -1228,7 +1244,11 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       wait_vmcnt<0>();
     }
     const float z = v[0];
-    if (z == __builtin_inff() && (l16 & 3) == 0) atomicOr(status, 2u);
+    if (z == __builtin_inff() && (l16 & 3) == 0) {
+      // a key far above the row's reference: the job is rescored exactly before selection
+      atomicOr(status, RKV_STATUS_REPAIRED);
+      atomicOr(P.counters + (size_t)kCounterStride * (1 + j.job) + 1, 1u);
+    }
     // z >= 1 for every valid row (the reference key contributes 1); padding rows have z = 0, and
     // a row left NaN after a time-out gets 0
     if ((l16 & 3) == 0)
@@ -1324,7 +1344,6 @@ __global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const
   __shared__ float2 sStat[kWaves][R];
   __shared__ __attribute__((aligned(16))) float sLam[R];   // -normaliser in logit units, pass B item
   __shared__ float sCol[NG][kSlice];
-  __shared__ float sFoldP[4][R];
   __shared__ int sFold;
 
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
@@ -1532,6 +1551,148 @@ __device__ __forceinline__ uint32_t rank_bits(float v) {
 }
 
 // ---------------------------------------------------------------------------------------------
+// Exact rescoring of one window-scored job (the repair path).  The pipelined scoring kernel takes
+// its exponentials against a fixed per-row reference; a row with a key far above it overflows
+// the row sum, and the kernel flags the job (word 1 of the job's counter line).  The selection
+// workgroup of a flagged job recomputes the job's scores here, in plain fp32 arithmetic with a
+// running maximum per row (no reference, so nothing overflows), before it ranks them:
+//   pass 1: per window row r, m_r = max_j x_rj and s_r = sum_j exp2(x_rj - m_r) over its visible
+//           keys, x = q.k log2(e)/sqrt(d) (thread = (row, key lane); lanes combined via LDS);
+//   pass 2: per key j, A_g[j] = sum over head g's rows of exp2(x_rj - m_r) / s_r, in chunks of
+//           blockDim keys that include the pool halo; S gets the pooled (SnapKV prefix) or plain
+//           group mean, Su the plain group mean, as the scoring kernels store them.
+// It is slow (two passes of scalar FMAs over the job) and only runs for flagged jobs.  Needs
+// G * w <= 128 (the pipelined kernel's limit) and kRepairLds bytes of LDS at `lds`.
+// ---------------------------------------------------------------------------------------------
+constexpr int kRepairRows = 128;
+constexpr int kRepairKeyLanes = 8;   // blockDim / 128 at most
+constexpr int kRepairLds = (kRepairRows * kHeadDim * 2) + 4 * (2 * kRepairRows + 2 * kRepairKeyLanes * kRepairRows + 8 * 1024);
+
+__device__ __noinline__ void rescore_exact(const uint16_t* qjob, const uint16_t* khead, float* S, float* Su, int L,
+                                           int w, int G, int ph, int snap, float sl2, float* lds) {
+  const int T = blockDim.x, tid = threadIdx.x;
+  const int R = G * w;
+  uint32_t* sQ = reinterpret_cast<uint32_t*>(lds);   // [128][64] bf16 pairs of the job's query rows
+  float* sM = lds + kRepairRows * kHeadDim / 2;        // [128] row maxima (log2 units)
+  float* sR = sM + kRepairRows;                        // [128] reciprocal row sums
+  float* sPm = sR + kRepairRows;                       // [key lanes][128] partial maxima
+  float* sPs = sPm + kRepairKeyLanes * kRepairRows;    // [key lanes][128] partial sums
+  float* sA = sPs + kRepairKeyLanes * kRepairRows;     // [G][T] column sums of a chunk
+  const float NEG_INF = -__builtin_inff();
+  for (int e = tid; e < kRepairRows * kHeadDim / 2; e += T)
+    sQ[e] = (e >> 6) < R ? reinterpret_cast<const uint32_t*>(qjob)[e] : 0u;
+  __syncthreads();
+  // ---- pass 1
+  const int nkl = T / kRepairRows, row = tid % kRepairRows, kl = tid / kRepairRows;
+  {
+    float m = NEG_INF, sum = 0.f;
+    if (row < R) {
+      const int last = L - w + row % w;   // the row's own position
+      uint32_t q[64];
+#pragma unroll
+      for (int c = 0; c < 64; ++c) q[c] = sQ[row * 64 + c];
+      for (int j = kl; j <= last; j += nkl) {
+        const u32x4* kr = reinterpret_cast<const u32x4*>(khead + (size_t)j * kHeadDim);
+        float z = 0.f;
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+          const u32x4 kv = kr[c];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const uint32_t qq = q[4 * c + u];
+            z = fmaf(__uint_as_float(qq << 16), __uint_as_float(kv[u] << 16), z);
+            z = fmaf(__uint_as_float(qq & 0xffff0000u), __uint_as_float(kv[u] & 0xffff0000u), z);
+          }
+        }
+        const float x = z * sl2;
+        if (x > m) {
+          sum = sum * __builtin_amdgcn_exp2f(m - x) + 1.f;
+          m = x;
+        } else {
+          sum += __builtin_amdgcn_exp2f(x - m);
+        }
+      }
+    }
+    sPm[kl * kRepairRows + row] = m;
+    sPs[kl * kRepairRows + row] = sum;
+  }
+  __syncthreads();
+  if (tid < kRepairRows) {
+    float m = NEG_INF, sum = 0.f;
+    for (int k = 0; k < nkl; ++k) {
+      const float pm = sPm[k * kRepairRows + tid], ps = sPs[k * kRepairRows + tid];
+      if (!(ps > 0.f)) continue;
+      if (!(sum > 0.f)) {
+        m = pm;
+        sum = ps;
+      } else {
+        const float M = fmaxf(m, pm);
+        sum = sum * __builtin_amdgcn_exp2f(m - M) + ps * __builtin_amdgcn_exp2f(pm - M);
+        m = M;
+      }
+    }
+    sM[tid] = m;
+    sR[tid] = sum > 0.f ? 1.f / sum : 0.f;
+  }
+  __syncthreads();
+  // ---- pass 2
+  const int core = T - 2 * ph, npre = L - w;
+  const float inv_g = 1.f / (float)G;
+  for (int c0 = 0; c0 < L; c0 += core) {
+    const int j = c0 - ph + tid;
+    const bool valid = j >= 0 && j < L;
+    uint32_t kk[64];
+    if (valid) {
+      const u32x4* kr = reinterpret_cast<const u32x4*>(khead + (size_t)j * kHeadDim);
+#pragma unroll
+      for (int c = 0; c < 16; ++c) {
+        const u32x4 kv = kr[c];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) kk[4 * c + u] = kv[u];
+      }
+    }
+    for (int g = 0; g < G; ++g) {
+      float acc = 0.f;
+      if (valid) {
+        for (int ii = 0; ii < w; ++ii) {
+          if (j > L - w + ii) continue;   // row ii of the window does not see key j
+          const int r = g * w + ii;
+          float z = 0.f;
+#pragma unroll
+          for (int c = 0; c < 64; ++c) {
+            const uint32_t qq = sQ[r * 64 + c];
+            z = fmaf(__uint_as_float(qq << 16), __uint_as_float(kk[c] << 16), z);
+            z = fmaf(__uint_as_float(qq & 0xffff0000u), __uint_as_float(kk[c] & 0xffff0000u), z);
+          }
+          acc += __builtin_amdgcn_exp2f(z * sl2 - sM[r]) * sR[r];
+        }
+      }
+      sA[g * T + tid] = acc;
+    }
+    __syncthreads();
+    if (tid >= ph && tid < ph + core && valid) {
+      float su = 0.f, sc = 0.f;
+      for (int g = 0; g < G; ++g) su += sA[g * T + tid];
+      if (snap && j < npre) {
+        const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
+        for (int g = 0; g < G; ++g) {
+          float mx = NEG_INF;
+          for (int t = lo; t <= hi; ++t) mx = fmaxf(mx, sA[g * T + tid + (t - j)]);
+          sc += mx;
+        }
+        S[j] = sc * inv_g;
+      } else {
+        S[j] = su * inv_g;
+      }
+      Su[j] = su * inv_g;
+    }
+    __syncthreads();
+  }
+  __threadfence();
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------------------------
 // Selection: one workgroup per job.
 // ---------------------------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P) {
@@ -1554,7 +1715,15 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
   float* Srow = P.S + (size_t)job * L;
   const int n_score = ly.all ? (snap ? L - w : L) : ly.cand_end;
   const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
-  const bool fix = snap && ph > 0 && n_score > 0 && NC > 1;
+  // a window-scored job flagged by the pipelined kernel is rescored exactly first; its scores
+  // are then complete (no slice-border pool repair)
+  const bool repaired =
+      slot < P.n_window &&
+      __hip_atomic_load(P.counters + (size_t)kCounterStride * (1 + job) + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+  if (repaired)
+    rescore_exact(ly.q + (size_t)(s * P.n_q_heads + h * G) * w * kHeadDim, ly.k + (size_t)bh * L * kHeadDim, Srow,
+                  P.Su + (size_t)job * L, L, w, G, ph, snap ? 1 : 0, P.scale_log2, reinterpret_cast<float*>(smem));
+  const bool fix = snap && ph > 0 && n_score > 0 && NC > 1 && !repaired;
   const int n_edge = fix ? NC * G * E : 0;
   const bool cached = n_score + n_edge <= cache_cap;
   float* sEdge = sCache + n_score;
@@ -1733,7 +1902,15 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   const float* Srow = P.S + (size_t)job * L;
   const int n = ly.all ? (snap ? L - w : L) : ly.cand_end;   // candidate (and reported) positions
   const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
-  const bool fix = snap && ph > 0 && n > 0 && NC > 1;
+  // a window-scored job flagged by the pipelined kernel is rescored exactly first; its scores
+  // are then complete (no slice-border pool repair)
+  const bool repaired =
+      slot < P.n_window &&
+      __hip_atomic_load(P.counters + (size_t)kCounterStride * (1 + job) + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+  if (repaired)
+    rescore_exact(ly.q + (size_t)(s * P.n_q_heads + h * G) * w * kHeadDim, ly.k + (size_t)bh * L * kHeadDim,
+                  P.S + (size_t)job * L, P.Su + (size_t)job * L, L, w, G, ph, snap ? 1 : 0, P.scale_log2, sDyn);
+  const bool fix = snap && ph > 0 && n > 0 && NC > 1 && !repaired;
   const int n_edge = fix ? NC * G * E : 0, n_fix = fix ? (NC - 1) * twoP : 0;
   float* sEdge = sDyn;
   float* sFix = sDyn + n_edge;
@@ -2040,7 +2217,7 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
     const int n_lam = n_jobs * row_tiles * 32;
     const int n_cnt = kCounterStride * (1 + n_jobs);
     const int blocks = std::max(1, std::min(64, (std::max(n_lam, n_cnt) + 255) / 256));
-    reset_counters<<<blocks, 256, 0, st>>>(P.counters, n_cnt, reinterpret_cast<uint32_t*>(P.lam), n_lam);
+    reset_counters<<<blocks, 256, 0, st>>>(P.counters, n_cnt, reinterpret_cast<uint32_t*>(P.lam), n_lam, P.first_group);
   }
   profile_mark(kStageZero, true, stream);   // the status word is cleared even without jobs
   if (n_jobs > 0) {
@@ -2062,10 +2239,17 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
     else err = launch_score<8, 8>(P, st, stream);
     if (err) return err;
   }
-  if (n_sel > n_jobs) {
+  if (P.n_full > 0) {
     // H2O layers with full-span accumulation: their own two passes, then the shared selection
     profile_mark(kStageScore, false, stream);
     int err = launch_fullspan(P, stream);
+    profile_mark(kStageScore, true, stream);
+    if (err) return err;
+  }
+  if (P.n_scored > P.n_window + P.n_full) {
+    // TOVA layers: the last query's attention over every key, then the shared selection
+    profile_mark(kStageScore, false, stream);
+    int err = launch_tova(P, stream);
     profile_mark(kStageScore, true, stream);
     if (err) return err;
   }
@@ -2086,7 +2270,7 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
                                             (1 + P.group));
     profile_mark(kStageSelect, false, stream);
     if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - 2 * kHistBins * 4 - 256)
-      select_regs_kernel<<<n_sel, kSelThreads, dyn, st>>>(P);
+      select_regs_kernel<<<n_sel, kSelThreads, std::max(dyn, (size_t)kRepairLds), st>>>(P);
     else
       select_kernel<<<n_sel, kThreads, kSelectLds, st>>>(P);
     profile_mark(kStageSelect, true, stream);

@@ -42,14 +42,16 @@ struct PrefillLayer {
 // One prefill launch group (up to 32 layers).  A scored "job" is a (scored layer slot,
 // sequence, KV head) triple, job = (slot * B + b) * Hkv + h; its keys are cut into n_slices
 // slices of kSlice keys, the scoring work items.  The scored layers come first in `layer`
-// (window-scored ones, then H2O with full-span accumulation), so slot s is layer[s]
+// (window-scored ones, then H2O with full-span accumulation, then TOVA), so slot s is layer[s]
 // (slot_layer[s] == s).
 struct PrefillLaunch {
   PrefillLayer layer[kMaxLayersPerLaunch];
   int32_t n_layers;
   int32_t n_scored;       // scored layer slots
-  int32_t n_window;       // of which window-scored (slots 0 .. n_window-1; the rest: H2O full span)
+  int32_t n_window;       // window-scored slots 0 .. n_window-1
+  int32_t n_full;         // full-span H2O slots n_window .. n_window+n_full-1; TOVA slots follow
   int32_t n_gather;       // layers with retained rows (gather list)
+  int32_t first_group;    // 1 in the call's first launch group: its first kernel clears the status word
   int32_t batch, seq_len, n_q_heads, n_kv_heads, window;
   int32_t group;          // G = Hq / Hkv
   int32_t row_tiles_per_group;  // ceil(w / 32)
@@ -66,6 +68,8 @@ struct PrefillLaunch {
                           //         pipelined kernel keeps the reciprocal row sum 1 / Z here instead
   float* ncl;             // [J][R]  pipelined kernel: minus the per-row reference logit (0 for padding rows)
   float* lamf;            // [J_full][G][L]  full-span H2O: log2 normaliser of every query row
+  float* tz;              // [J_tova][G][L]  TOVA: log2-scaled logits of the last query per head
+  float* tstat;           // [J_tova][n_slices][G][2]  TOVA: per-slice (max, sum of exp2(x - max))
   float* S;               // [J][L]  ranking score
   float* Su;              // [J][L]  unpooled group-mean score (SnapKV layers, if wanted)
   float* edge;            // [J][n_slices][G][4 * pool_half]  per-query-head column sums at slice edges
@@ -78,10 +82,10 @@ static_assert(sizeof(PrefillLaunch) <= 4000, "kernel argument block too large");
 
 // Workspace layout for one launch group.
 struct PrefillWorkspace {
-  size_t counters, stats, lam, ncl, lamf, S, Su, edge, end, total;
+  size_t counters, stats, lam, ncl, lamf, tz, tstat, S, Su, edge, end, total;
 };
 PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half,
-                                          int n_full_jobs);
+                                          int n_full_jobs, int n_tova_jobs);
 
 // Error reporting (thread-local last error).
 int fail(int status, const std::string& msg);
@@ -90,6 +94,7 @@ void clear_error();
 // Kernel launchers (prefill.hip / decode.hip).  Return a hipError_t as int.
 int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream);
 int launch_fullspan(const PrefillLaunch& P, void* stream);   // fullspan.hip
+int launch_tova(const PrefillLaunch& P, void* stream);       // tova.hip
 
 struct DecodeLayer {
   uint16_t* k_cache; uint16_t* v_cache; int32_t* pos; float* acc;
@@ -117,10 +122,26 @@ struct EntropyLaunch {
   float* rows;        // [n_layers, B, Hq, n_q] row entropies (nats)
   float* h;           // [n_layers] mean row entropy
   double* partial;    // [n_layers, B * Hkv * ceil(n_q / 32)] per-workgroup sums of row entropies
-  uint32_t* status;   // 0, or 1 if some row entropy is not finite
+  uint32_t* status;   // bit 0: some row entropy is not finite; bit 2: a block was recomputed exactly
+  int32_t first_group;  // 1 in the call's first launch: it clears the status word
 };
 
 int launch_entropy(const EntropyLaunch& E, void* stream);
+
+// Prefill -> decode hand-off (handoff.hip): up to kMaxCopies buffer copies per launch; a null
+// source zero-fills the destination.  Sizes are in bytes, multiples of 4.
+constexpr int kMaxCopies = 4 * kMaxLayersPerLaunch;
+struct CopyTask {
+  const void* src;
+  void* dst;
+  int64_t bytes;
+};
+struct CopyLaunch {
+  CopyTask task[kMaxCopies];
+  int32_t n_tasks;
+};
+static_assert(sizeof(CopyLaunch) <= 4000, "kernel argument block too large");
+int launch_copies(const CopyLaunch& C, void* stream);
 
 // Stage timing with HIP events (enabled through rkv_profile_enable).
 enum Stage { kStageZero = 0, kStageScore = 1, kStageSelect = 2, kStageGather = 3, kStageDecode = 4 };

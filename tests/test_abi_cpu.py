@@ -31,7 +31,7 @@ def test_library_exports_every_declared_function():
     for name in names:
         assert hasattr(L, name), name
     assert sorted(names) == sorted(_abi.EXPORTED)
-    assert rkv.version() == 1
+    assert rkv.version() == 2
 
 
 # ------------------------------------------------------------------ allocator vs the oracle
@@ -97,8 +97,9 @@ def test_plan_validation():
     with pytest.raises(rkv.RkvError) as e:
         rkv.Plan([rkv.H2O], [64], [rkv.H2O], [1])
     assert e.value.status == 3
+    rkv.Plan([rkv.TOVA], [64])                                       # TOVA compresses the prompt too
     with pytest.raises(rkv.RkvError) as e:
-        rkv.Plan([rkv.TOVA], [64])                                   # TOVA is decode-only
+        rkv.Plan([rkv.H2O_FULL], [64], [rkv.H2O_FULL], [64])         # full-span H2O is prefill-only
     assert e.value.status == 3
     with pytest.raises(rkv.RkvError) as e:
         rkv.Plan([rkv.H2O], [64], [rkv.TOVA], [0])
@@ -234,3 +235,100 @@ def test_entropy_profile_argument_errors():
     assert L.rkv_entropy_workspace_size(C.byref(sh3), 2, 64, C.byref(size)) == 0
     assert L.rkv_entropy_profile(C.byref(sh3), 2, 64, fake, fake, C.c_void_p(FAKE), C.c_void_p(FAKE),
                                  C.c_void_p(FAKE), C.c_void_p(FAKE), 1 << 20, None) == 4
+
+
+# ------------------------------------------------------------------ Section 3.4 declarations, tied routes
+
+def test_rule_phase_declarations():
+    """R_pre, R_dec and their intersection (Section 3.4): SnapKV and full-span H2O compress the
+    prompt only; FULL, StreamingLLM, H2O and TOVA are declared for both phases."""
+    assert rkv.rule_phases(rkv.SNAPKV) == 1
+    assert rkv.rule_phases(rkv.H2O_FULL) == 1
+    for r in (rkv.FULL, rkv.STREAMING, rkv.H2O, rkv.TOVA):
+        assert rkv.rule_phases(r) == 3
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.rule_phases(9)
+    assert e.value.status == 1
+
+
+def layers_of(plan):
+    import struct
+    blob = plan.to_bytes()
+    w = struct.unpack("<%di" % (len(blob) // 4), blob)
+    return [tuple(w[8 + 4 * i: 12 + 4 * i]) for i in range(w[2])]
+
+
+def test_scoped_routes_and_tied_both_phase_plans():
+    """A completed route (Sections 3.1-3.2): the operator runs in its scope's phases and FULL
+    in the other; a tied both-phase layer uses one operator, which must lie in the
+    intersection of the prefill and decode declarations."""
+    P, D, Bo = rkv.SCOPE_PREFILL, rkv.SCOPE_DECODE, rkv.SCOPE_BOTH
+    # the paper's system composition: H2O on layers 0-15, TOVA on 16-31, 512 each, both phases
+    plan = rkv.Plan.from_scoped_route([rkv.H2O] * 16 + [rkv.TOVA] * 16, [Bo] * 32, [512] * 32)
+    assert layers_of(plan) == [(rkv.H2O, 512, rkv.H2O, 512)] * 16 + [(rkv.TOVA, 512, rkv.TOVA, 512)] * 16
+    assert plan.rules_prefill == [rkv.H2O] * 16 + [rkv.TOVA] * 16
+    assert plan.retained_counts(8192, rkv.PHASE_DECODE) == [512] * 32
+    # prefill-only and decode-only scopes put FULL in the inactive phase
+    plan = rkv.Plan.from_scoped_route([rkv.SNAPKV, rkv.TOVA, rkv.STREAMING], [P, D, Bo], [100, 64, 32])
+    assert layers_of(plan) == [(rkv.SNAPKV, 100, rkv.FULL, 0), (rkv.FULL, 0, rkv.TOVA, 64),
+                               (rkv.STREAMING, 32, rkv.STREAMING, 32)]
+    # operators outside the scope's declarations
+    for rules, scopes in (([rkv.SNAPKV], [Bo]), ([rkv.H2O_FULL], [Bo]), ([rkv.SNAPKV], [D])):
+        with pytest.raises(rkv.RkvError) as e:
+            rkv.Plan.from_scoped_route(rules, scopes, [64])
+        assert e.value.status == 3
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan.from_scoped_route([rkv.H2O], [3], [64])           # unknown scope
+    assert e.value.status == 1
+    with pytest.raises(rkv.RkvError) as e:
+        rkv.Plan.from_scoped_route([rkv.H2O], [Bo], [1])           # decode H2O needs capacity >= 2
+    assert e.value.status == 3
+    # serialization keeps a tied plan tied
+    plan = rkv.Plan.from_scoped_route([rkv.H2O, rkv.TOVA], [Bo, Bo], [40, 50])
+    again = rkv.Plan.from_bytes(plan.to_bytes())
+    assert layers_of(again) == layers_of(plan)
+
+
+def test_prefill_accepts_tova_and_rejects_unsupported_groups():
+    plan = rkv.Plan([rkv.TOVA], [128])
+    assert call_prefill(plan, (1, 1024, 24, 8, 128)) == 4     # G = 3: TOVA needs G in {1, 2, 4, 8}
+    assert call_prefill(plan, (1, 1024, 32, 8, 128), ws_bytes=1024) == 5   # reaches the workspace check
+
+
+def test_decode_validation_precedes_every_launch():
+    """A bad layer in the second launch group (layer 32) is reported before the first group is
+    enqueued: on a host without a GPU an enqueue would fail with RKV_ERR_HIP instead."""
+    L = _abi.lib()
+    n = 33
+    plan = rkv.Plan([rkv.H2O] * n, [64] * n, [rkv.H2O] * n, [64] * n)
+    fake = rkv._parr([FAKE] * n)
+    acc = rkv._parr([FAKE] * (n - 1) + [None])
+    st_ = _abi.DecodeState(fake, fake, fake, acc)
+    inp = _abi.DecodeInput(fake, fake, fake, None)
+    sh = _abi.Shape(1, 1, 32, 8, 128)
+    assert L.rkv_decode_step(plan.handle, C.byref(sh), C.byref(st_), C.byref(inp), 100, None) == 1
+    assert "layer 32" in L.rkv_last_error().decode()
+
+
+def test_decode_init_from_prefill_argument_errors():
+    """The prefill -> decode hand-off (Section 3.4) checks every layer before any copy."""
+    L = _abi.lib()
+    plan = rkv.Plan([rkv.SNAPKV, rkv.H2O], [128, 100], [rkv.FULL, rkv.H2O], [0, 100])
+    fake = rkv._parr([FAKE, FAKE])
+    sh = _abi.Shape(1, 1024, 32, 8, 128)
+    io = _abi.PrefillIO(fake, fake, fake, fake, fake, fake, None, fake)
+    st_ = _abi.DecodeState(fake, fake, fake, fake)
+    assert L.rkv_decode_init_from_prefill(plan.handle, C.byref(sh), None, C.byref(st_), None) == 1
+    # decode capacity 100 against a prefill retained count of min(100, 50) = 50
+    sh_short = _abi.Shape(1, 50, 32, 8, 128)
+    assert L.rkv_decode_init_from_prefill(plan.handle, C.byref(sh_short), C.byref(io), C.byref(st_), None) == 2
+    # the H2O seed: acc_out is required when the prefill operator scores
+    io_noacc = _abi.PrefillIO(fake, fake, fake, fake, fake, fake, None, None)
+    assert L.rkv_decode_init_from_prefill(plan.handle, C.byref(sh), C.byref(io_noacc), C.byref(st_), None) == 1
+    assert "acc" in L.rkv_last_error().decode()
+    # a decode layer without its cache buffers
+    st_null = _abi.DecodeState(rkv._parr([FAKE, None]), fake, fake, fake)
+    assert L.rkv_decode_init_from_prefill(plan.handle, C.byref(sh), C.byref(io), C.byref(st_null), None) == 1
+    # prefill FULL keeps L positions; a decode capacity below L cannot take them over
+    plan2 = rkv.Plan([rkv.FULL], [0], [rkv.H2O], [64])
+    assert L.rkv_decode_init_from_prefill(plan2.handle, C.byref(sh), C.byref(io), C.byref(st_), None) == 2

@@ -17,8 +17,9 @@ GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
 def run_case(rules, budgets, layers, *, window, pool_kernel=7, n_sink=4, num=1, den=2, check_acc=True,
-             label=""):
-    """layers: list (per layer) of list (per sequence) of dicts with q/k/v bits."""
+             label="", status=0):
+    """layers: list (per layer) of list (per sequence) of dicts with q/k/v bits.  `status`: the
+    workspace status word the call must leave (0, or RKV_STATUS_REPAIRED for a repaired job)."""
     import torch
     import paper_2606_15157_amd as rkv
     plan = rkv.Plan(rules, budgets, window=window, pool_kernel=pool_kernel, n_sink=n_sink, recent_num=num,
@@ -30,7 +31,7 @@ def run_case(rules, budgets, layers, *, window, pool_kernel=7, n_sink=4, num=1, 
         v_t.append(bits_to_torch(np.stack([x["v"] for x in seqs])))
     out = rkv.evict_prefill(plan, q_t, k_t, v_t, score_out=True, acc_out=True)
     torch.cuda.synchronize()
-    assert rkv.prefill_check(out["workspace"]) == 0, "a scoring work item timed out"
+    assert rkv.prefill_check(out["workspace"]) == status, "unexpected status word"
     n_amb = 0
     for l, seqs in enumerate(layers):
         idx = out["idx"][l].cpu().numpy()
@@ -43,6 +44,8 @@ def run_case(rules, budgets, layers, *, window, pool_kernel=7, n_sink=4, num=1, 
                                  pool_kernel=pool_kernel, n_sink=n_sink, recent_num=num, recent_den=den)
             L = x["k"].shape[1]
             su = oracle_unpooled(x["q"], x["k"]) if rules[l] in (OP.SNAPKV, OP.H2O) else None
+            if rules[l] == OP.TOVA:
+                su = ora["scores"]   # TOVA's score covers every position; acc carries it
             for h in range(x["k"].shape[0]):
                 what = f"{label} layer {l} seq {s} head {h}"
                 if ora["scores"] is not None:
@@ -190,29 +193,69 @@ def test_other_scoring_kernels_match_oracle(monkeypatch, mode):
              label=f"k{mode}_777")
 
 
-def test_reference_overflow_is_reported(monkeypatch):
-    """The pipelined kernel takes its exponentials against each row's logit with its own key and
-    with the first key.  One window row (query head 5, row 7) is set to 4 in every dimension and
-    one prefix key (position 300) to 4 in every dimension: that row's logit there is
-    4 * 4 * 128 / sqrt(128) = 181, about 170 natural-log units above its reference, beyond the
-    fp32 exponent range.  The kernel must report the overflow in the status word (bit 1) instead
-    of returning scores silently.  The exact (running-maximum) two-pass kernel, selected through
-    the test hook, still matches the oracle on the same input (the other rows keep ordinary
-    logits, so the scores stay distinct)."""
-    import paper_2606_15157_amd as rkv
-    import torch
-    L, w = 1024, 32
+def overflow_input(L=1024, w=32):
+    """One window row (query head 5, row 7) set to 4 in every dimension and one prefix key
+    (position 300) to 4 in every dimension: that row's logit there is 4 * 4 * 128 / sqrt(128) =
+    181, about 170 natural-log units above the row's reference (its logits with its own key and
+    with key 0), beyond the fp32 exponent range of the pipelined kernel's row sums."""
     x = gen(12, 0, 0, L)
     q = x["q"].copy()
     k = x["k"].copy()
     four = f32_to_bf16_bits(np.full(128, 4.0, np.float32))
     q[5, 7, :] = four
     k[:, 300, :] = four
-    y = {"q": q, "k": k, "v": x["v"]}
-    plan = rkv.Plan([OP.SNAPKV], [128], window=w)
-    out = rkv.evict_prefill(plan, [bits_to_torch(q[None])], [bits_to_torch(k[None])],
-                            [bits_to_torch(x["v"][None])])
-    torch.cuda.synchronize()
-    assert rkv.prefill_check(out["workspace"]) & 2, "overflow of the row sum was not reported"
+    return {"q": q, "k": k, "v": x["v"]}
+
+
+def test_reference_overflow_is_repaired(monkeypatch):
+    """The overflowing job is flagged by the pipelined kernel and rescored exactly by its
+    selection workgroup, through the default path: scores, retained sets, rows and acc match
+    the oracle, and the status word says RKV_STATUS_REPAIRED (outputs valid).  The exact
+    running-maximum two-pass kernel (test hook) agrees on the same input with a clean status."""
+    y = overflow_input()
+    run_case([OP.SNAPKV, OP.H2O], [128, 128], [[y], [y]], window=32, label="ref_overflow", status=4)
     monkeypatch.setenv("RKV_FORCE_TWO_PASS", "1")
-    run_case([OP.SNAPKV], [128], [[y]], window=w, label="ref_overflow_two_pass")
+    run_case([OP.SNAPKV], [128], [[y]], window=32, label="ref_overflow_two_pass")
+
+
+def test_status_word_spans_every_launch_group():
+    """33 layers take two launch groups.  The overflow planted in layer 0 (first group) must still
+    be visible in the status word after the second group ran, and both groups' layers (0, the
+    repaired one, and 32) match the oracle."""
+    L = 1024
+    y = overflow_input(L)
+    layers = [[y]] + [[gen(14, 0, l, L)] for l in range(1, 33)]
+    run_case([OP.SNAPKV] * 33, [128] * 33, layers, window=32, label="two_groups", status=4)
+
+
+def test_bench_call_matches_debug_call_at_full_size():
+    """bench.py's exact call at the 8K route (no score or acc output: the pipelined kernel stores no
+    unpooled scores, the selection writes no scores) gives indices and rows bitwise equal to the
+    call with debug outputs, whose results the full-route test checks against the oracle; and
+    here every layer's retained set is checked against the oracle too."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    g = json.load(open(os.path.join(GOLDEN, "budgets.json")))
+    budgets = g["pyramid_512"]
+    rules = mixed_route()
+    xs = [gen(2, 0, l, 8192) for l in range(32)]
+    plan = rkv.Plan(rules, budgets, window=32, pool_kernel=7)
+    q = [bits_to_torch(x["q"][None]) for x in xs]
+    k = [bits_to_torch(x["k"][None]) for x in xs]
+    v = [bits_to_torch(x["v"][None]) for x in xs]
+    out = rkv.alloc_outputs(plan, 1, 8, 8192, 128, "cuda")
+    ws = rkv.alloc_workspace(plan, 1, 8192, 32, 8, "cuda")
+    call = rkv.PreparedPrefill(plan, q, k, v, out, ws)
+    for _ in range(3):   # as bench.py: repeated passes over one workspace
+        call(torch.cuda.current_stream())
+    torch.cuda.synchronize()
+    assert rkv.prefill_check(ws) == 0
+    dbg = rkv.evict_prefill(plan, q, k, v, score_out=True, acc_out=True)
+    torch.cuda.synchronize()
+    for l in range(32):
+        for key in ("idx", "k_out", "v_out"):
+            assert torch.equal(out[key][l], dbg[key][l]), (key, l)
+        ora = OP.evict_layer(rules[l], budgets[l], xs[l]["q"], xs[l]["k"], xs[l]["v"], window=32, pool_kernel=7)
+        idx = out["idx"][l].cpu().numpy()
+        for h in range(8):
+            check_retained(idx[0, h], ora, h, 8192, f"bench call layer {l} head {h}")
