@@ -1561,14 +1561,15 @@ __device__ __forceinline__ uint32_t rank_bits(float v) {
 //   pass 2: per key j, A_g[j] = sum over head g's rows of exp2(x_rj - m_r) / s_r, in chunks of
 //           blockDim keys that include the pool halo; S gets the pooled (SnapKV prefix) or plain
 //           group mean, Su the plain group mean, as the scoring kernels store them.
-// It is slow (two passes of scalar FMAs over the job) and only runs for flagged jobs.  Needs
+// It is slow (two passes of scalar FMAs over the job) and only runs for flagged jobs; inlined,
+// with the query rows read from LDS, so the selection kernels need no stack.  Needs
 // G * w <= 128 (the pipelined kernel's limit) and kRepairLds bytes of LDS at `lds`.
 // ---------------------------------------------------------------------------------------------
 constexpr int kRepairRows = 128;
 constexpr int kRepairKeyLanes = 8;   // blockDim / 128 at most
 constexpr int kRepairLds = (kRepairRows * kHeadDim * 2) + 4 * (2 * kRepairRows + 2 * kRepairKeyLanes * kRepairRows + 8 * 1024);
 
-__device__ __noinline__ void rescore_exact(const uint16_t* qjob, const uint16_t* khead, float* S, float* Su, int L,
+__device__ __forceinline__ void rescore_exact(const uint16_t* qjob, const uint16_t* khead, float* S, float* Su, int L,
                                            int w, int G, int ph, int snap, float sl2, float* lds) {
   const int T = blockDim.x, tid = threadIdx.x;
   const int R = G * w;
@@ -1588,20 +1589,17 @@ __device__ __noinline__ void rescore_exact(const uint16_t* qjob, const uint16_t*
     float m = NEG_INF, sum = 0.f;
     if (row < R) {
       const int last = L - w + row % w;   // the row's own position
-      uint32_t q[64];
-#pragma unroll
-      for (int c = 0; c < 64; ++c) q[c] = sQ[row * 64 + c];
+      const u32x4* qr = reinterpret_cast<const u32x4*>(sQ + row * 64);
       for (int j = kl; j <= last; j += nkl) {
         const u32x4* kr = reinterpret_cast<const u32x4*>(khead + (size_t)j * kHeadDim);
         float z = 0.f;
-#pragma unroll
+#pragma unroll 4
         for (int c = 0; c < 16; ++c) {
-          const u32x4 kv = kr[c];
+          const u32x4 kv = kr[c], qv = qr[c];
 #pragma unroll
           for (int u = 0; u < 4; ++u) {
-            const uint32_t qq = q[4 * c + u];
-            z = fmaf(__uint_as_float(qq << 16), __uint_as_float(kv[u] << 16), z);
-            z = fmaf(__uint_as_float(qq & 0xffff0000u), __uint_as_float(kv[u] & 0xffff0000u), z);
+            z = fmaf(__uint_as_float(qv[u] << 16), __uint_as_float(kv[u] << 16), z);
+            z = fmaf(__uint_as_float(qv[u] & 0xffff0000u), __uint_as_float(kv[u] & 0xffff0000u), z);
           }
         }
         const float x = z * sl2;
@@ -1641,16 +1639,8 @@ __device__ __noinline__ void rescore_exact(const uint16_t* qjob, const uint16_t*
   for (int c0 = 0; c0 < L; c0 += core) {
     const int j = c0 - ph + tid;
     const bool valid = j >= 0 && j < L;
-    uint32_t kk[64];
-    if (valid) {
-      const u32x4* kr = reinterpret_cast<const u32x4*>(khead + (size_t)j * kHeadDim);
-#pragma unroll
-      for (int c = 0; c < 16; ++c) {
-        const u32x4 kv = kr[c];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) kk[4 * c + u] = kv[u];
-      }
-    }
+    // the key row is re-read per window row (L2 hits) so that no 64-register copy is live
+    const u32x4* kr = reinterpret_cast<const u32x4*>(khead + (size_t)(valid ? j : 0) * kHeadDim);
     for (int g = 0; g < G; ++g) {
       float acc = 0.f;
       if (valid) {
@@ -1658,11 +1648,15 @@ __device__ __noinline__ void rescore_exact(const uint16_t* qjob, const uint16_t*
           if (j > L - w + ii) continue;   // row ii of the window does not see key j
           const int r = g * w + ii;
           float z = 0.f;
+          const u32x4* qr = reinterpret_cast<const u32x4*>(sQ + r * 64);
+#pragma unroll 4
+          for (int c = 0; c < 16; ++c) {
+            const u32x4 qv = qr[c], kv = kr[c];
 #pragma unroll
-          for (int c = 0; c < 64; ++c) {
-            const uint32_t qq = sQ[r * 64 + c];
-            z = fmaf(__uint_as_float(qq << 16), __uint_as_float(kk[c] << 16), z);
-            z = fmaf(__uint_as_float(qq & 0xffff0000u), __uint_as_float(kk[c] & 0xffff0000u), z);
+            for (int u = 0; u < 4; ++u) {
+              z = fmaf(__uint_as_float(qv[u] << 16), __uint_as_float(kv[u] << 16), z);
+              z = fmaf(__uint_as_float(qv[u] & 0xffff0000u), __uint_as_float(kv[u] & 0xffff0000u), z);
+            }
           }
           acc += __builtin_amdgcn_exp2f(z * sl2 - sM[r]) * sR[r];
         }
