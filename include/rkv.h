@@ -253,6 +253,19 @@ int rkv_prefill_workspace_size(const rkv_plan* plan, const rkv_shape* shape, siz
 int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_prefill_io* io,
                       void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): rkv_prefill_evict with the library's own workspace,
+ * a static device array of 64 MiB per GPU (held until the process ends; enough for a 32-layer
+ * route of one 8192-token sequence).  Arguments, outputs and errors are those of
+ * rkv_prefill_evict; a call needing more than 64 MiB (rkv_prefill_workspace_size) fails with
+ * RKV_ERR_WORKSPACE before anything is enqueued.  status_out: NULL, or a device uint32 that
+ * receives the call's status word (RKV_STATUS_* bits) on `stream` after the pass.  Allocates
+ * nothing: no hipMalloc / hipFree, no allocating library routine.  Every call on one GPU shares
+ * the array; calls that overlap on one GPU (several streams or threads) race and must be
+ * serialised by the caller. */
+int rkv_prefill_evict_noalloc(const rkv_plan* plan, const rkv_shape* shape, const rkv_prefill_io* io,
+                              uint32_t* status_out, void* stream);
+
 /* Implementation call (failure reporting of rkv_prefill_evict): synchronously read the status
  * word a previous rkv_prefill_evict left in `ws` (RKV_STATUS_* bits; 0 = clean).  Outputs are
  * valid unless RKV_STATUS_TIMEOUT or RKV_STATUS_INVALID is set.  Uses a blocking copy (waits

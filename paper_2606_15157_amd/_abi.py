@@ -20,7 +20,7 @@ STATUS_TIMEOUT, STATUS_INVALID, STATUS_REPAIRED = 1, 2, 4
 EXPORTED = [
     "rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_destroy", "rkv_plan_num_layers",
     "rkv_plan_serialize", "rkv_plan_deserialize", "rkv_rule_phases", "rkv_plan_from_route",
-    "rkv_plan_retained_counts", "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check",
+    "rkv_plan_retained_counts", "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_evict_noalloc", "rkv_prefill_check",
     "rkv_decode_step", "rkv_decode_init_from_prefill", "rkv_entropy_workspace_size", "rkv_entropy_profile", "rkv_profile_enable", "rkv_profile_read", "rkv_last_error",
     "rkv_version",
 ]
@@ -86,6 +86,8 @@ def lib():
         L.rkv_prefill_workspace_size.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(C.c_size_t)]
         L.rkv_prefill_evict.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(PrefillIO), C.c_void_p, C.c_size_t,
                                         C.c_void_p]
+        L.rkv_prefill_evict_noalloc.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(PrefillIO), C.c_void_p,
+                                                C.c_void_p]
         L.rkv_prefill_check.argtypes = [C.c_void_p, C.c_size_t, C.POINTER(C.c_int32)]
         L.rkv_decode_step.argtypes = [C.c_void_p, C.POINTER(Shape), C.POINTER(DecodeState), C.POINTER(DecodeInput),
                                       C.c_int32, C.c_void_p]
@@ -103,7 +105,7 @@ def lib():
         for name in ("rkv_allocate_budgets", "rkv_plan_create", "rkv_plan_num_layers", "rkv_plan_retained_counts",
                      "rkv_plan_serialize", "rkv_plan_deserialize",
                      "rkv_prefill_workspace_size", "rkv_prefill_evict", "rkv_prefill_check", "rkv_decode_step",
-                     "rkv_rule_phases", "rkv_plan_from_route", "rkv_decode_init_from_prefill",
+                     "rkv_rule_phases", "rkv_plan_from_route", "rkv_decode_init_from_prefill", "rkv_prefill_evict_noalloc",
                      "rkv_entropy_workspace_size", "rkv_entropy_profile",
                      "rkv_profile_enable", "rkv_profile_read", "rkv_version"):
             getattr(L, name).restype = C.c_int
