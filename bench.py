@@ -9,8 +9,11 @@ paper, b_min 48).  Window 32, max-pool 7.  Synthetic seeded N(0,1) Q/K/V with pl
 heavy-hitter and recency structure.
 
 One step = one full eviction pass over all 32 layers (window scoring, softmax, window sum,
-pooling, group mean, per-head top-k, K/V gather), inputs resident in HBM.
-Prints one JSON line.
+pooling, group mean, per-head top-k, K/V gather), inputs resident in HBM.  Beside the headline
+line's roofline (the scoring kernel) the record carries the other measured configurations: the
+single-layer latency (L = 1024), the batch-8 budget sweep, the 32K long-context routes, the
+H2O / TOVA composition, decode steps, the entropy profile, full-span H2O, a measured copy ceiling
+and the CPU oracle.  Prints one JSON line.
 """
 from __future__ import annotations
 
@@ -162,8 +165,8 @@ def entropy_measure(dev, reps=3, n_layers=32, L=4096):
 def fullspan_measure(dev, reps=3):
     """The 8K route with its H2O layers (16-27) accumulating over every prompt query instead of
     the window (their queries: all 8192 positions).  Same budgets; random bf16 inputs.  The
-    full-span layers dominate: two passes over the causal logits each,
-    2 x sum_t (t + 1) x 2 d flop per query head."""
+    full-span layers dominate: their causal logits, sum_t (t + 1) x 2 d flop per query head
+    (counted once)."""
     import torch
     import paper_2606_15157_amd as rkv
     from synth.workloads import mixed_route, pyramid_weights
@@ -192,13 +195,212 @@ def fullspan_measure(dev, reps=3):
         raise RuntimeError("full-span pass reported a failure")
     ms = e0.elapsed_time(e1) / reps
     n_full = sum(1 for r in rules if r == rkv.H2O_FULL)
-    flop = n_full * HQ * (L_CTX * (L_CTX + 1) // 2) * D * 2 * 2
+    # the method's work: every causal logit once (the kernels compute them twice, in the row-normaliser
+    # and the column-sum pass; that second pass is an implementation choice and is not counted)
+    flop = n_full * HQ * (L_CTX * (L_CTX + 1) // 2) * D * 2
     log(f"full-span route: {ms:.3f} ms per pass ({flop / (ms * 1e-3) / 1e12:.0f} TFLOP/s on the full-span logits)")
     del q, k, v, out, ws, call
     torch.cuda.empty_cache()
     return {"workload": "32-layer mixed route at L=8192 with H2O layers 16-27 accumulating over all 8192 queries",
             "ms_per_pass": ms, "full_span_flop": flop, "achieved_TFLOPs": flop / (ms * 1e-3) / 1e12,
-            "peak_TFLOPs": 2500.0, "layer_tokens_per_s": N_LAYERS * L_CTX / (ms * 1e-3)}
+            "peak_TFLOPs": 2500.0, "mfma_frac": flop / (ms * 1e-3) / 1e12 / 2500.0,
+            "layer_tokens_per_s": N_LAYERS * L_CTX / (ms * 1e-3)}
+
+
+def percentiles(samples_ms):
+    """median / p10 / p90 / mean of per-step durations in microseconds."""
+    import numpy as np
+    a = np.asarray(samples_ms, dtype=np.float64) * 1e3
+    return {"median_us": float(np.median(a)), "p10_us": float(np.percentile(a, 10)),
+            "p90_us": float(np.percentile(a, 90)), "mean_us": float(a.mean()), "n": int(a.size)}
+
+
+def time_steps(fn, stream, steps, warmup):
+    """Run fn(stream) warmup times, then `steps` times with a HIP event pair around each call on
+    `stream`; returns the per-step durations (ms)."""
+    import torch
+    for _ in range(warmup):
+        fn(stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record(stream)
+        fn(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
+def route_bytes(rules, budgets, B, L, Hq=HQ, Hkv=HKV, d=D, w=W):
+    """Algorithmic bytes of one pass: every window-scored layer's K and window queries read once, every
+    retained K / V row read and written once, every retained index written once."""
+    from synth.workloads import SNAPKV, H2O
+    score = sum(B * (Hkv * L * d * 2 + Hq * w * d * 2) for r in rules if r in (SNAPKV, H2O))
+    keep = sum(min(b, L) for b in budgets)
+    return score, score + B * Hkv * keep * (d * 2 * 4 + 4)
+
+
+def route_flop(rules, B, L, Hq=HQ, d=D, w=W):
+    """Window logits of the window-scored layers: B Hq w L 2 d per layer (masked keys included)."""
+    from synth.workloads import SNAPKV, H2O
+    return sum(B * Hq * w * L * d * 2 for r in rules if r in (SNAPKV, H2O))
+
+
+def run_route(dev, rules, budgets, B, L, w, workload, steps, warmup, n_hh):
+    """Time the eviction pass of one route over seeded device inputs (same recipe as the parity
+    tests' large shapes); returns per-step stats, the score-stage time and the byte accounting."""
+    import torch
+    import paper_2606_15157_amd as rkv
+    from synth import prefill_layer_torch
+    xs = [prefill_layer_torch(workload, l, batch=B, seq_len=L, window=w, n_hh=n_hh) for l in range(len(rules))]
+    q, k, v = [x["q"] for x in xs], [x["k"] for x in xs], [x["v"] for x in xs]
+    del xs
+    plan = rkv.Plan(rules, budgets, window=w, pool_kernel=POOL)
+    out = rkv.alloc_outputs(plan, B, HKV, L, D, dev)
+    ws = rkv.alloc_workspace(plan, B, L, HQ, HKV, dev)
+    call = rkv.PreparedPrefill(plan, q, k, v, out, ws)
+    stream = torch.cuda.current_stream(dev)
+    per = time_steps(call, stream, steps, warmup)
+    if rkv.prefill_check(ws) != 0:
+        raise RuntimeError("eviction pass reported a failure")
+    rkv.profile_enable(rkv.STAGE_SCORE)
+    for _ in range(max(3, steps // 2)):
+        call(stream)
+    torch.cuda.synchronize()
+    n, tot = rkv.profile_read()
+    rkv.profile_enable(-1)
+    score_ms = tot / max(n, 1)
+    sb, pb = route_bytes(rules, budgets, B, L, w=w)
+    flop = route_flop(rules, B, L, w=w)
+    st = percentiles(per)
+    ms = st["median_us"] * 1e-3
+    res = {"steps": percentiles(per), "score_us": score_ms * 1e3, "algorithmic_bytes": pb,
+           "score_algorithmic_bytes": sb, "hbm_frac": pb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+           "score_hbm_frac": sb / (score_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+           "score_mfma_frac": flop / (score_ms * 1e-3) / 1e12 / 2500.0,
+           "layer_tokens_per_s": B * len(rules) * L / (ms * 1e-3)}
+    del q, k, v, out, ws, call
+    torch.cuda.empty_cache()
+    return res
+
+
+def c1_measure(dev, steps=200, warmup=20):
+    """Latency of one eviction call on the single-layer workload: L = 1024, SnapKV, budget 128,
+    32 / 8 heads (and the same layer under H2O, StreamingLLM and Full); the pass is far below the
+    HBM time scale (3.4 MB), so only its time is reported."""
+    import torch
+    import paper_2606_15157_amd as rkv
+    from synth import prefill_layer_torch
+    x = prefill_layer_torch(1, 0, batch=1, seq_len=1024, window=W, n_hh=16)
+    out = {}
+    for name, rule in (("snapkv", rkv.SNAPKV), ("h2o", rkv.H2O), ("streaming", rkv.STREAMING), ("full", rkv.FULL)):
+        plan = rkv.Plan([rule], [128], window=W, pool_kernel=POOL)
+        o = rkv.alloc_outputs(plan, 1, HKV, 1024, D, dev)
+        ws = rkv.alloc_workspace(plan, 1, 1024, HQ, HKV, dev)
+        call = rkv.PreparedPrefill(plan, [x["q"]], [x["k"]], [x["v"]], o, ws)
+        per = time_steps(call, torch.cuda.current_stream(dev), steps, warmup)
+        out[name] = percentiles(per)
+        log(f"c1 {name}: median {out[name]['median_us']:.1f} us")
+    return {"workload": "one layer, L=1024, batch 1, 32 q / 8 kv heads, d=128, w=32, pool 7, budget 128", **out}
+
+
+def c3_measure(dev, steps=10, warmup=2):
+    """Budget sweep on the 32-layer mixed route at L = 8192, batch 8 distinct sequences: average
+    budgets 128 / 256 / 512 / 1024 / 2048 per layer, each the completed 512 vector rescaled to the
+    new total (Section 3.3's sweep rule, b_min 48)."""
+    import paper_2606_15157_amd as rkv
+    from synth.workloads import mixed_route, pyramid_weights
+    rules = mixed_route(N_LAYERS)
+    b512 = rkv.allocate_budgets(pyramid_weights(N_LAYERS), N_LAYERS * 512, B_MIN)
+    res = {}
+    for avg in (128, 256, 512, 1024, 2048):
+        budgets = rkv.allocate_budgets(b512, N_LAYERS * avg, B_MIN)
+        r = run_route(dev, rules, budgets, 8, L_CTX, W, 3, steps, warmup, 16)
+        res[str(avg)] = r
+        log(f"c3 avg {avg}: {r['steps']['median_us']:.0f} us/pass, {r['hbm_frac']:.3f} of HBM peak")
+    return {"workload": "32-layer mixed route, L=8192, batch 8, 32 q / 8 kv heads, d=128, w=32, pool 7", **res}
+
+
+def c4_measure(dev, steps=5, warmup=2):
+    """Long context: L = 32768, batch 4, w = 64, average budget 1024 (the completed 512 vector
+    rescaled), all-SnapKV, all-H2O and the mixed route; 64 planted heavy hitters per head."""
+    import paper_2606_15157_amd as rkv
+    from synth.workloads import pyramid_weights, route_by_name
+    b512 = rkv.allocate_budgets(pyramid_weights(N_LAYERS), N_LAYERS * 512, B_MIN)
+    budgets = rkv.allocate_budgets(b512, N_LAYERS * 1024, B_MIN)
+    res = {}
+    for route in ("snapkv", "h2o", "mixed"):
+        r = run_route(dev, route_by_name(route, N_LAYERS), budgets, 4, 32768, 64, 4, steps, warmup, 64)
+        res[route] = r
+        log(f"c4 {route}: {r['steps']['median_us']:.0f} us/pass, {r['hbm_frac']:.3f} of HBM peak")
+    return {"workload": "32 layers, L=32768, batch 4, 32 q / 8 kv heads, d=128, w=64, pool 7, average budget 1024",
+            **res}
+
+
+def composition_measure(dev, steps=10, warmup=3):
+    """Appendix E's composition as a tied both-phase plan (H2O on layers 0-15, TOVA on 16-31, 512
+    positions per layer in both phases), batch 1 at the appendix's prompt lengths: the prefill
+    eviction pass (H2O window scoring plus TOVA's last-query scoring, selection, gather) and the
+    prefill-to-decode hand-off.  Eviction work only; the paper's table measures whole-model runs."""
+    import torch
+    import paper_2606_15157_amd as rkv
+    from synth import prefill_layer_torch
+    rules = [rkv.H2O] * 16 + [rkv.TOVA] * 16
+    res = {}
+    for L in (4096, 8192, 16384, 32768):
+        plan = rkv.Plan.from_scoped_route(rules, [rkv.SCOPE_BOTH] * N_LAYERS, [512] * N_LAYERS, window=W)
+        xs = [prefill_layer_torch(6, l, batch=1, seq_len=L, window=W, n_hh=16) for l in range(N_LAYERS)]
+        q, k, v = [x["q"] for x in xs], [x["k"] for x in xs], [x["v"] for x in xs]
+        del xs
+        out = rkv.alloc_outputs(plan, 1, HKV, L, D, dev, acc_out=True)
+        ws = rkv.alloc_workspace(plan, 1, L, HQ, HKV, dev)
+        call = rkv.PreparedPrefill(plan, q, k, v, out, ws)
+        stream = torch.cuda.current_stream(dev)
+        per = time_steps(call, stream, steps, warmup)
+        if rkv.prefill_check(ws) != 0:
+            raise RuntimeError("composition pass reported a failure")
+        out["io"] = call
+        state = rkv.decode_init_from_prefill(plan, out)
+        hand = time_steps(lambda st: rkv.decode_init_from_prefill(plan, out, state, stream=st), stream, steps, warmup)
+        st_ = percentiles(per)
+        res[str(L)] = {"prefill_pass": st_, "handoff": percentiles(hand),
+                       "prompt_tokens_per_s": L / (st_["median_us"] * 1e-6)}
+        log(f"composition L={L}: prefill eviction {st_['median_us']:.0f} us, hand-off "
+            f"{res[str(L)]['handoff']['median_us']:.1f} us")
+        del q, k, v, out, ws, call, state
+        torch.cuda.empty_cache()
+    return {"workload": "H2O 0-15 / TOVA 16-31 tied in both phases, 512 positions per layer, batch 1, "
+                        "32 q / 8 kv heads, d=128", **res}
+
+
+def copy_ceiling(dev, nbytes=1 << 30, reps=5):
+    """A plain 1 GiB device-to-device copy (read + write bytes over its time): the HBM rate a
+    streaming kernel reaches on this GPU, reported beside the 8 TB/s vendor peak."""
+    import torch
+    src = torch.empty(nbytes // 2, dtype=torch.bfloat16, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def kernel_source_hash():
@@ -224,6 +426,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the single-layer latency, batch-8 budget sweep and 32K long-context legs")
     ap.add_argument("--no-entropy", action="store_true", help="skip the entropy-profile measurement")
     ap.add_argument("--no-fullspan", action="store_true", help="skip the full-span H2O route measurement")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -272,15 +476,19 @@ def main():
 
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    step_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
     torch.cuda.synchronize()
     w0 = time.perf_counter()
     e0.record(stream)
-    for _ in range(args.steps):
+    for a, b in step_ev:
+        a.record(stream)
         call(stream)
+        b.record(stream)
     e1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms_step = e0.elapsed_time(e1) / args.steps
+    step_stats = percentiles([a.elapsed_time(b) for a, b in step_ev])
     log(f"timed {args.steps} steps: {ms_step * 1e3:.1f} us/step (wall {wall / args.steps * 1e6:.1f} us/step)")
     if rkv.prefill_check(ws) != 0:
         raise RuntimeError("scoring work items timed out in the timed region")
@@ -312,6 +520,7 @@ def main():
 
     score_bytes, pass_bytes = algorithmic_bytes(rules, budgets)
     score_gbps = score_bytes / (stage_ms["score"] * 1e-3) / 1e9
+    score_flop = route_flop(rules, 1, L_CTX)
     pass_gbps = pass_bytes / (ms_step * 1e-3) / 1e9
     traffic = traffic_record()
     value = N_LAYERS * L_CTX / (ms_step * 1e-3)
@@ -340,7 +549,15 @@ def main():
             "algorithmic_bytes": pass_bytes,
             "achieved_GBps": pass_gbps,
             "hbm_frac": pass_gbps / HBM_PEAK_GBPS,
+            "steps": step_stats,
             "stage_us": {kk: vv * 1e3 for kk, vv in stage_ms.items()},
+        },
+        "score_mfma": {
+            "kernel": SCORE_KERNEL,
+            "flop_per_launch": score_flop,
+            "achieved_TFLOPs": score_flop / (stage_ms["score"] * 1e-3) / 1e12,
+            "peak_TFLOPs": 2500.0,
+            "frac": score_flop / (stage_ms["score"] * 1e-3) / 1e12 / 2500.0,
         },
         "roofline": {
             "kernel": SCORE_KERNEL,
@@ -353,9 +570,16 @@ def main():
             "algorithmic_bytes_per_launch": score_bytes,
         },
     }
+    del out, ws, call, q, k, v
+    torch.cuda.empty_cache()
+    rec["copy_ceiling_GBps"] = copy_ceiling(dev)
+    log(f"copy ceiling: {rec['copy_ceiling_GBps']:.0f} GB/s")
+    if not args.no_configs:
+        rec["c1_latency"] = c1_measure(dev)
+        rec["c3_budget_sweep"] = c3_measure(dev)
+        rec["c4_long_context"] = c4_measure(dev)
+        rec["h2o_tova_composition"] = composition_measure(dev)
     if not args.no_decode:
-        del out, ws, call, q, k, v
-        torch.cuda.empty_cache()
         rec["decode"] = decode_measure(dev)
     if not args.no_entropy:
         rec["entropy"] = entropy_measure(dev)
@@ -364,6 +588,7 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle ...")
         rec["cpu_baseline"] = cpu_baseline(xs, rules, budgets, args.cpu_seconds)
+        rec["cpu_baseline"]["cpu_model"] = cpu_model()
     print(json.dumps(rec), flush=True)
 
 
