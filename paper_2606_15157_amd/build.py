@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "librkv.so")
-SOURCES = ["host.cpp", "prefill.hip", "decode.hip", "entropy.hip", "fullspan.hip", "tova.hip", "handoff.hip", "noalloc.hip"]
+SOURCES = ["host.cpp", "prefill.hip", "decode.hip", "entropy.hip", "fullspan.hip", "tova.hip", "handoff.hip", "noalloc.hip", "window.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

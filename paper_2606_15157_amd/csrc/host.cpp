@@ -114,8 +114,9 @@ int score_class(const rkv_layer& ly, const Layout& lo) {
   return 0;
 }
 
-// Test hook: RKV_FORCE_TWO_PASS=1 selects the two-pass scoring kernel (normally used for prompts
-// too long for the single-pass one) so that it can be checked on short prompts too.
+// Test hook for layouts the pipelined scoring kernel would take: RKV_FORCE_TWO_PASS=1 selects the
+// two-kernel window path (normally used for prompts too long for the pipelined kernel), 2 the
+// running-maximum single-pass kernel, so that both can be checked on short prompts too.
 int force_two_pass() {
   const char* e = std::getenv("RKV_FORCE_TWO_PASS");
   return e ? std::max(0, std::atoi(e)) : 0;

@@ -2224,6 +2224,11 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
       else if (ntg == 2) score_pipe_kernel<2><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
       else score_pipe_kernel<4><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
       profile_mark(kStageScore, true, stream);
+    } else if (P.force_two_pass != 2) {
+      // longer prompts and eight row tiles: row normalisers, then column sums (window.hip)
+      profile_mark(kStageScore, false, stream);
+      err = launch_window(P, row_tiles, stream);
+      profile_mark(kStageScore, true, stream);
     } else if (row_tiles == 4 && ntg == 1) err = launch_score<4, 1>(P, st, stream);
     else if (row_tiles == 4 && ntg == 2) err = launch_score<4, 2>(P, st, stream);
     else if (row_tiles == 4) err = launch_score<4, 4>(P, st, stream);

@@ -95,6 +95,7 @@ void clear_error();
 int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream);
 int launch_fullspan(const PrefillLaunch& P, void* stream);   // fullspan.hip
 int launch_tova(const PrefillLaunch& P, void* stream);       // tova.hip
+int launch_window(const PrefillLaunch& P, int row_tiles, void* stream);   // window.hip
 
 struct DecodeLayer {
   uint16_t* k_cache; uint16_t* v_cache; int32_t* pos; float* acc;

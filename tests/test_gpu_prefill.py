@@ -180,12 +180,11 @@ def test_repeat_runs_are_bitwise_identical():
             assert torch.equal(a[key][l], b[key][l]), (key, l)
 
 
-@pytest.mark.parametrize("mode", ["1", "2"], ids=["two_pass", "single_pass"])
+@pytest.mark.parametrize("mode", ["1", "2"], ids=["window_two_kernel", "single_pass"])
 def test_other_scoring_kernels_match_oracle(monkeypatch, mode):
-    """The two-pass scoring kernel (prompts whose slices do not all fit in the resident
-    workgroups; eight row tiles) and the running-maximum single-pass kernel, forced through the
-    test hook on layouts the pipelined kernel would otherwise take: the 1K case and a ragged
-    length."""
+    """The two-kernel window path (row normalisers, then column sums: prompts of more than 64
+    slices, eight row tiles) and the running-maximum single-pass kernel, forced through the test
+    hook on layouts the pipelined kernel would otherwise take: the 1K case and a ragged length."""
     monkeypatch.setenv("RKV_FORCE_TWO_PASS", mode)
     run_case([OP.SNAPKV, OP.H2O], [128, 128], [[gen(1, 0, 0, 1024)], [gen(1, 0, 1, 1024)]], window=32,
              label=f"k{mode}_1k")
@@ -210,12 +209,15 @@ def overflow_input(L=1024, w=32):
 def test_reference_overflow_is_repaired(monkeypatch):
     """The overflowing job is flagged by the pipelined kernel and rescored exactly by its
     selection workgroup, through the default path: scores, retained sets, rows and acc match
-    the oracle, and the status word says RKV_STATUS_REPAIRED (outputs valid).  The exact
-    running-maximum two-pass kernel (test hook) agrees on the same input with a clean status."""
+    the oracle, and the status word says RKV_STATUS_REPAIRED (outputs valid).  The two-kernel
+    window path (test hook) flags and repairs the same job; the running-maximum single-pass kernel
+    computes it directly, with a clean status."""
     y = overflow_input()
     run_case([OP.SNAPKV, OP.H2O], [128, 128], [[y], [y]], window=32, label="ref_overflow", status=4)
     monkeypatch.setenv("RKV_FORCE_TWO_PASS", "1")
-    run_case([OP.SNAPKV], [128], [[y]], window=32, label="ref_overflow_two_pass")
+    run_case([OP.SNAPKV, OP.H2O], [128, 128], [[y], [y]], window=32, label="ref_overflow_window", status=4)
+    monkeypatch.setenv("RKV_FORCE_TWO_PASS", "2")
+    run_case([OP.SNAPKV], [128], [[y]], window=32, label="ref_overflow_single_pass")
 
 
 def test_status_word_spans_every_launch_group():
