@@ -114,23 +114,12 @@ int score_class(const rkv_layer& ly, const Layout& lo) {
   return 0;
 }
 
-// Test hook for layouts the pipelined scoring kernel would take: RKV_FORCE_TWO_PASS=1 selects the
-// two-kernel window path (normally used for prompts too long for the pipelined kernel), 2 the
-// running-maximum single-pass kernel, so that both can be checked on short prompts too.
-int force_two_pass() {
-  const char* e = std::getenv("RKV_FORCE_TWO_PASS");
-  return e ? std::max(0, std::atoi(e)) : 0;
-}
-
-// Two-pass scoring: pass B trails pass A by this many items in each workgroup (RKV_SCORE_LAG
-// overrides it for tuning runs).
-int score_lag() {
-  static int lag = -1;
-  if (lag < 0) {
-    const char* e = std::getenv("RKV_SCORE_LAG");
-    lag = e ? std::max(0, std::atoi(e)) : 6;
-  }
-  return lag;
+// Test hook: RKV_FORCE_WINDOW=1 selects the window scoring kernels (normally used for prompts of
+// more than 64 slices and for eight row tiles) on layouts the pipelined kernel would take, so
+// that they can be checked on short prompts too.
+int force_window() {
+  const char* e = std::getenv("RKV_FORCE_WINDOW");
+  return e && std::atoi(e) > 0 ? 1 : 0;
 }
 
 std::vector<Group> layer_groups(const rkv_plan* plan, int32_t L) {
@@ -199,8 +188,9 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
   size_t off = 0;
   w.counters = off;
   off = round_up(off + sizeof(uint32_t) * kCounterStride * (1 + (size_t)n_jobs), 256);
-  w.stats = off;
-  off = round_up(off + sizeof(float) * 2 * (size_t)n_jobs * n_slices * rows, 256);
+  w.stats = off;   // only the pipelined kernel (four row tiles, at most kPipeMaxSlices slices) uses it
+  const bool pipe_layout = rows == kPipeRows && n_slices <= kPipeMaxSlices;
+  off = round_up(off + sizeof(float) * (pipe_layout ? (size_t)n_jobs * n_slices * kPipeRows : 0), 256);
   w.lam = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
   w.ncl = off;
@@ -548,8 +538,7 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     P.n_slices = (L + rkv::kSlice - 1) / rkv::kSlice;
     P.pool_half = p.pool_kernel / 2;
     P.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)shape->head_dim));
-    P.score_lag = score_lag();
-    P.force_two_pass = force_two_pass();
+    P.force_window = force_window();
     int slot = 0, n_gather = 0;
     bool want_unpooled = false;
     // scored layers first, so that scored slot s is entry s of the layer table (the pipelined

@@ -6,26 +6,23 @@
 //   S[j]    = mean_g maxpool(A[g])[j]  (SnapKV)  or  mean_g A[g][j]  (H2O)
 // A row's softmax is normalised over every key while the window sum runs over rows, so a row's
 // normaliser is known only once every key of the job has been seen.  Work items are (job,
-// slice of 128 keys); each of the four waves of a workgroup takes one 32-key tile of the slice.
-//   single-pass scoring kernel (persistent; every slice of a job in flight at once): a slice
-//     streams its K tile from HBM once, keeps the exponentials of its logits in registers,
-//     publishes one log2-normaliser per window row and counts itself in; the job's first slice
-//     folds them into the job's normalisers once all have counted in; every slice then turns its
-//     exponentials into probabilities, sums them over the window rows, pools (SnapKV) and
-//     averages over the query group;
-//   two-pass scoring kernel (prompts too long for every slice of a job to be in flight): pass A
-//     streams the tile and publishes its statistics, pass B re-reads it a fixed number of items
-//     later (L2 / MALL) and recomputes the logits with the normalisers known;
-//   select kernels (one workgroup per job): repair the pooled score next to slice borders, find
-//     the k-th largest score with three radix-histogram passes and write the retained positions
-//     in ascending order;
+// slice of 128 keys).
+//   prepare + pipelined scoring kernel (four row tiles, at most 64 slices per job): persistent,
+//     one eight-wave workgroup per CU, three items in flight; each slice streams its K tile
+//     once, publishes per-row sums against a fixed per-row reference logit, and turns its
+//     exponentials into probabilities once every slice of the job has published (the kernel's
+//     own comment below has the schedule);
+//   window kernels (window.hip; longer prompts and eight row tiles): row normalisers, then
+//     column sums, each streaming K once;
+//   select kernels (one workgroup per job): repair the pooled score next to slice borders (or
+//     rescore a job flagged for a reference overflow exactly), find the k-th largest score with
+//     three radix-histogram passes and write the retained positions in ascending order;
 //   gather kernel: copies the retained K and V rows.
 //
 // Data handed between workgroups of one launch goes through device-coherent loads and stores
-// (they bypass the XCD-local caches); a slice counts itself in only after a vmcnt(0) wait has
-// retired its statistics stores, and normalisers are written once over a NaN "not written"
-// mark, so no agent-scope fence (which would flush and invalidate L2) is needed.  Every wait is
-// bounded: on time-out the workspace status word is set and the kernel carries on.
+// (they bypass the XCD-local caches) over a NaN "not stored" mark, so no agent-scope fence
+// (which would flush and invalidate L2) is needed.  Every wait is bounded: on time-out the
+// workspace status word is set and the kernel carries on.
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -38,7 +35,6 @@ namespace rkv {
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -49,58 +45,10 @@ constexpr uint32_t kSpinLimit = 1u << 21;
 constexpr int kHistBins = 2048;
 constexpr int kSelectLds = 128 * 1024;   // dynamic LDS of the select kernel (scores cached up to ~30K keys)
 
-// Cache policy of a device-coherent buffer load (sc1: served from the device-wide coherence point).
-constexpr int kCoherent = 16;
-
-__device__ __forceinline__ void store_coherent(float* p, float v) {
-  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_coherent(const float* p) {
-  return __uint_as_float(__hip_atomic_load(reinterpret_cast<const uint32_t*>(p), __ATOMIC_RELAXED,
-                                           __HIP_MEMORY_SCOPE_AGENT));
-}
 __device__ __forceinline__ void store_coherent2(float* p, float a, float b) {
   const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
   __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ float2 load_coherent2(const float* p) {
-  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
-}
-// Wait until this wave's memory operations have completed (ordering only, no cache flush).
-__device__ __forceinline__ void vmem_release() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));
-}
-__device__ __forceinline__ void vmem_acquire() {
-  __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-}
-// Bounded wait (one thread) until *flag >= target.
-__device__ __forceinline__ void wait_at_least(uint32_t* flag, uint32_t target, uint32_t* status) {
-  uint32_t it = 0;
-  while (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-    __builtin_amdgcn_s_sleep(1);
-    if (++it > kSpinLimit) {
-      atomicOr(status, 1u);
-      break;
-    }
-  }
-  vmem_acquire();
-}
-
-// Online combination of (max, sum) pairs in log2 units; empty pairs (sum 0) are skipped.
-__device__ __forceinline__ void combine_ms(float& M, float& S, float m, float l) {
-  if (!(l > 0.f)) return;
-  if (m > M) {
-    S = S * __builtin_amdgcn_exp2f(M - m) + l;
-    M = m;
-  } else {
-    S += l * __builtin_amdgcn_exp2f(m - M);
-  }
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
 // Index of this wave in the workgroup, as a wave-uniform (scalar) value.
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6)); }
 
@@ -110,12 +58,11 @@ __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane
 __device__ __forceinline__ void loads_done() { __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8)); }
 
 // Zeroes the counters (the status word at counters[0] only in the call's first launch group, so
-// that it covers the whole call) and marks every per-row normaliser "not written" (NaN).
-__global__ void reset_counters(uint32_t* counters, int n, uint32_t* lam, int n_lam, int clear_status) {
+// that it covers the whole call) before the window scoring kernels.
+__global__ void reset_counters(uint32_t* counters, int n, int clear_status) {
   const int i0 = blockIdx.x * blockDim.x + threadIdx.x, stride = gridDim.x * blockDim.x;
   for (int i = i0; i < n; i += stride)
     if (i > 0 || clear_status) counters[i] = 0u;
-  for (int i = i0; i < n_lam; i += stride) lam[i] = 0xffffffffu;
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -148,306 +95,9 @@ __device__ __forceinline__ void dpp_halve(float (&v)[V], int bit) {
     }
   }
 }
-// Reduce-scatter of V values per lane over the 32 lanes of each half-wave.  Afterwards lane l
-// holds max(V / 32, 1) sums: value i is the sum of original value 32 i + sel(l) (V >= 32), or
-// of value sel(l) & 15 (V = 16, duplicated in lanes l and l ^ 1), where
-// sel(l) = bit4(l) | bit3(l) << 1 | bit2(l) << 2 | bit1(l) << 3 | bit0(l) << 4.
-template <int V>
-__device__ __forceinline__ void reduce_scatter32(float (&v)[V], int lane) {
-  static_assert(V == 16 || V == 32 || V == 64 || V == 128, "unsupported value count");
-  constexpr int N1 = V / 2;
-#pragma unroll
-  for (int i = 0; i < N1; ++i) {   // lanes l and l ^ 16: rows 0/1 and 2/3 of 16 lanes swap halves
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v[2 * i]), __float_as_uint(v[2 * i + 1]), false,
-                                                    false);
-    v[i] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-  }
-  dpp_halve<0x128, N1, V>(v, (lane >> 3) & 1);        // row_ror:8   -> lane l ^ 8
-  dpp_halve<0x141, N1 / 2, V>(v, (lane >> 2) & 1);    // row_half_mirror -> 7 - l within 8
-  dpp_halve<0x4E, N1 / 4, V>(v, (lane >> 1) & 1);     // quad_perm [2,3,0,1] -> l ^ 2
-  dpp_halve<0xB1, N1 / 8, V>(v, lane & 1);            // quad_perm [1,0,3,2] -> l ^ 1
-}
-// The same reduce-scatter on NV accumulator vectors in place (value i = e[i / 16][i % 16]).
-template <int CTRL, int N, int NV>
-__device__ __forceinline__ void dpp_halve_v(f32x16 (&e)[NV], int bit) {
-  if constexpr (N == 1) {
-    e[0][0] += dppf<CTRL>(e[0][0]);
-  } else {
-#pragma unroll
-    for (int i = 0; i < N / 2; ++i) {
-      const float a = e[(2 * i) >> 4][(2 * i) & 15], b = e[(2 * i + 1) >> 4][(2 * i + 1) & 15];
-      const float keep = bit ? b : a, send = bit ? a : b;
-      e[i >> 4][i & 15] = keep + dppf<CTRL>(send);
-    }
-  }
-}
-template <int NV>
-__device__ __forceinline__ void reduce_scatter32_v(f32x16 (&e)[NV], int lane) {
-  constexpr int V = NV * 16;
-  static_assert(V == 16 || V == 32 || V == 64 || V == 128, "unsupported value count");
-  constexpr int N1 = V / 2;
-#pragma unroll
-  for (int i = 0; i < N1; ++i) {
-    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(e[(2 * i) >> 4][(2 * i) & 15]),
-                                                    __float_as_uint(e[(2 * i + 1) >> 4][(2 * i + 1) & 15]), false, false);
-    e[i >> 4][i & 15] = __uint_as_float(r[0]) + __uint_as_float(r[1]);
-  }
-  dpp_halve_v<0x128, N1, NV>(e, (lane >> 3) & 1);
-  dpp_halve_v<0x141, N1 / 2, NV>(e, (lane >> 2) & 1);
-  dpp_halve_v<0x4E, N1 / 4, NV>(e, (lane >> 1) & 1);
-  dpp_halve_v<0xB1, N1 / 8, NV>(e, lane & 1);
-}
-__device__ __forceinline__ int rs_sel(int lane) {
-  return ((lane >> 4) & 1) | (((lane >> 3) & 1) << 1) | (((lane >> 2) & 1) << 2) | (((lane >> 1) & 1) << 3) |
-         ((lane & 1) << 4);
-}
-
 // ---------------------------------------------------------------------------------------------
 // Operand staging.
 // ---------------------------------------------------------------------------------------------
-// The job's query rows in LDS: R rows of 256 B in 16-byte chunks, chunk c of row r at
-// position 16 r + (c ^ (r & 15)), so the 32 rows one MFMA fragment read touches sit in distinct
-// banks.  Loaded by LDS DMA (each wave instruction fills 1 KB); padding rows (query head >= G
-// or window row >= w) are filled from row 0 and masked later.
-template <int NRT, int NTH>
-__device__ __forceinline__ void issue_q_to_lds(uint16_t* sQ, const uint16_t* qjob, int G, int w) {
-  constexpr int R = NRT * 32;
-  constexpr int kPerWave = R * 16 / kThreads;   // instructions per wave, 4 rows each
-  constexpr int kHeadRows = NTH * 32;           // padded rows per query head
-  const int lane = threadIdx.x & 63, wv = wave_id();
-  const int lr = lane >> 4;
-  // instruction i fills rows r0 = 4 (4 i + wv) .. r0 + 3: the low four row bits are (4 wv & 15) | lr
-  // for every i, so the chunk swizzle and the lane's byte offset are the same for all of them, and
-  // the four rows never straddle two query heads
-  const int c = (lane & 15) ^ (((4 * wv) & 15) | lr);
-  const uint32_t lane_off = (uint32_t)(lr * kHeadDim + c * 8) * 2u;
-  const uint32_t pad_off = (uint32_t)(c * 8) * 2u;
-#pragma unroll
-  for (int i = 0; i < kPerWave; ++i) {
-    const int r0 = 4 * (i * kWaves + wv);
-    const int g = r0 / kHeadRows, ii0 = r0 - g * kHeadRows;
-    const bool ok = g < G && ii0 + lr < w;
-    const uint32_t off = ok ? (uint32_t)((g * w + ii0) * kHeadDim) * 2u + lane_off : pad_off;
-    __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(reinterpret_cast<const char*>(qjob) + off),
-        (__attribute__((address_space(3))) void*)(sQ + r0 * kHeadDim), 16, 0, 0);
-  }
-}
-__device__ __forceinline__ bf16x8 q_frag(const uint16_t* sQ, int row, int chunk) {
-  return *reinterpret_cast<const bf16x8*>(sQ + (row * 16 + (chunk ^ (row & 15))) * 8);
-}
-// A-operand lanes of one 32-key tile: key `key` (clamped into the job), dims 64*hf + [0, 64).
-__device__ __forceinline__ void load_k_tile(u32x4 (&kf)[8], const uint16_t* khead, int key, int L, int hf) {
-  key = key < L ? key : L - 1;
-  const u32x4* kp = reinterpret_cast<const u32x4*>(khead + (size_t)key * kHeadDim + hf * 64);
-#pragma unroll
-  for (int st = 0; st < 8; ++st) kf[st] = kp[st];
-}
-
-// The item's 128-key K tile in LDS, laid out like the query block (key r's 16-byte chunk c at
-// position 16 r + (c ^ (r & 15))); keys past the prompt repeat its last key (masked later).
-__device__ __forceinline__ void issue_k_to_lds(uint16_t* sK, const uint16_t* khead, int key0, int L) {
-  constexpr int kPerWave = kSlice * 16 / kThreads;   // instructions per wave, 4 keys each
-  const int lane = threadIdx.x & 63, wv = wave_id();
-  const int lr = lane >> 4;
-  const int c = (lane & 15) ^ (((4 * wv) & 15) | lr);
-#pragma unroll
-  for (int i = 0; i < kPerWave; ++i) {
-    const int r0 = 4 * (i * kWaves + wv);
-    const int key = min(key0 + r0 + lr, L - 1);
-    __builtin_amdgcn_global_load_lds(
-        (const __attribute__((address_space(1))) void*)(khead + (size_t)key * kHeadDim + c * 8),
-        (__attribute__((address_space(3))) void*)(sK + r0 * kHeadDim), 16, 0, 0);
-  }
-}
-
-struct JobRef {
-  int job, slice, slot, s, h;
-};
-__device__ __forceinline__ JobRef decode_item(int64_t it, int nsl, int B, int Hkv) {
-  JobRef r;
-  r.job = (int)(it / nsl);
-  r.slice = (int)(it - (int64_t)r.job * nsl);
-  r.h = r.job % Hkv;
-  r.s = (r.job / Hkv) % B;
-  r.slot = r.job / (Hkv * B);
-  return r;
-}
-// Moves an item reference forward by n_wg items (= dj jobs and ds slices) with carries, so a
-// persistent workgroup walks its items without divisions.
-__device__ __forceinline__ void advance(JobRef& r, int dj, int ds, int nsl, int B, int Hkv) {
-  r.slice += ds;
-  int j = dj;
-  if (r.slice >= nsl) {
-    r.slice -= nsl;
-    ++j;
-  }
-  r.job += j;
-  r.h += j;
-  while (r.h >= Hkv) {
-    r.h -= Hkv;
-    if (++r.s == B) {
-      r.s = 0;
-      ++r.slot;
-    }
-  }
-}
-
-// Group mean, max-pool inside the slice (SnapKV, clipped to the prefix [0, L - w)), scores and
-// the slice-edge column sums the select kernel uses to redo the pool next to slice borders.
-// sCol[g][kl] holds the window column sum of key cbase + kl for query head g (SnapKV with G > 1)
-// or the sum over the group (otherwise).  Thread = (key, query-head half) for SnapKV.
-template <int NG>
-__device__ __forceinline__ void store_scores(const PrefillLaunch& P, bool snap, int job, int slice, int cbase,
-                                             const float (*sCol)[kSlice], float inv_g) {
-  const int tid = threadIdx.x, L = P.seq_len, w = P.window, G = P.group, nsl = P.n_slices;
-  const float NEG_INF = -__builtin_inff();
-  float* Srow = P.S + (size_t)job * L;
-  if (snap) {
-    const int kl = tid >> 1, kk = cbase + kl, npre = L - w, ph = P.pool_half;
-    const int g0 = (tid & 1) * ((G + 1) >> 1), g1 = min(G, g0 + ((G + 1) >> 1));
-    float su = 0.f, sc = 0.f;
-    if (kk < L) {
-      const int lo = max(kk - ph, cbase) - cbase, hi = min(min(kk + ph, cbase + kSlice - 1), npre - 1) - cbase;
-      for (int g = g0; g < g1; ++g) {
-        const float* cg = sCol[NG > 1 ? g : 0];
-        su += cg[kl];
-        float m = NEG_INF;
-        if (ph == 3) {   // the common 7-wide pool: independent reads
-          float x[7];
-#pragma unroll
-          for (int u = 0; u < 7; ++u) {
-            const int q = kl - 3 + u;
-            x[u] = (q >= lo && q <= hi) ? cg[q] : NEG_INF;
-          }
-#pragma unroll
-          for (int u = 0; u < 7; ++u) m = fmaxf(m, x[u]);
-        } else {
-          for (int u = lo; u <= hi; ++u) m = fmaxf(m, cg[u]);
-        }
-        sc += m;
-      }
-    }
-    su += __shfl_xor(su, 1);
-    sc += __shfl_xor(sc, 1);
-    if ((tid & 1) == 0 && kk < L) {
-      su *= inv_g;
-      Srow[kk] = kk < npre ? sc * inv_g : su;
-      if (P.want_unpooled) P.Su[(size_t)job * L + kk] = su;
-    }
-    if (ph > 0) {
-      const int E = 4 * ph, twoP = 2 * ph;
-      float* ed = P.edge + ((size_t)job * nsl + slice) * G * E;
-      for (int e = tid; e < G * E; e += kThreads) {
-        const int g = e / E, o = e - g * E;
-        const int kl2 = o < twoP ? o : kSlice - twoP + (o - twoP);
-        ed[e] = (cbase + kl2 < L) ? sCol[NG > 1 ? g : 0][kl2] : 0.f;
-      }
-    }
-  } else if (tid < kSlice && cbase + tid < L) {
-    Srow[cbase + tid] = sCol[0][tid] * inv_g;
-  }
-}
-
-// Fold used by the two-pass kernel: the job's per-slice log2 normalisers (one per row) are read
-// straight into registers, 16 slices per thread and batch (thread = row pair, slice group), as
-// device-coherent loads, then combined per row (max first, then the sum of exp2 against it) and
-// across the slice groups in LDS.
-template <int R>
-__device__ void fold_job_regs(const PrefillLaunch& P, int job, float2 (*sPart)[R]) {
-  constexpr int kPairs = R / 2;
-  constexpr int kGroups = kThreads / kPairs;   // slice groups
-  constexpr int kBatch = 16;
-  static_assert(kGroups >= 1 && kGroups <= kWaves, "partials fit the statistics buffer");
-  const int tid = threadIdx.x, nsl = P.n_slices;
-  const int pr = tid % kPairs, j = tid / kPairs;
-  const float NEG_INF = -__builtin_inff();
-  const float* st = P.stats + (size_t)job * nsl * R + 2 * pr;
-  float M0 = NEG_INF, Z0 = 0.f, M1 = NEG_INF, Z1 = 0.f;
-  for (int c0 = j; c0 < nsl; c0 += kGroups * kBatch) {
-    float2 v[kBatch];
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int c = c0 + u * kGroups;
-      v[u] = c < nsl ? load_coherent2(st + (size_t)c * R) : make_float2(NEG_INF, NEG_INF);
-    }
-    float m0 = NEG_INF, m1 = NEG_INF;
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      m0 = fmaxf(m0, v[u].x);
-      m1 = fmaxf(m1, v[u].y);
-    }
-    float z0 = 0.f, z1 = 0.f;
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      z0 += m0 > NEG_INF ? __builtin_amdgcn_exp2f(v[u].x - m0) : 0.f;
-      z1 += m1 > NEG_INF ? __builtin_amdgcn_exp2f(v[u].y - m1) : 0.f;
-    }
-    combine_ms(M0, Z0, m0, z0);
-    combine_ms(M1, Z1, m1, z1);
-  }
-  sPart[j][2 * pr] = make_float2(M0, Z0);
-  sPart[j][2 * pr + 1] = make_float2(M1, Z1);
-  __syncthreads();
-  if (tid < R) {
-    float m = sPart[0][tid].x, z = sPart[0][tid].y;
-#pragma unroll
-    for (int q = 1; q < kGroups; ++q) combine_ms(m, z, sPart[q][tid].x, sPart[q][tid].y);
-    store_coherent(P.lam + (size_t)job * R + tid, z > 0.f ? m + __log2f(z) : __builtin_inff());
-  }
-}
-
-// Fold used by the single-pass kernel.  Every slice of the job has published one log2-normaliser
-// per row (its tile max plus log2 of its sum, -inf for no visible key); they are copied into
-// sBuf (the query block's LDS space, R * 256 B, free at this point) by device-coherent LDS DMA,
-// 64 slices per round, and combined per row (thread = row, slice group).  The job's normalisers
-// go to memory and to sLam.
-template <int R>
-__device__ void fold_job_fused(const PrefillLaunch& P, int job, uint16_t* sBuf, float2 (*sPart)[R], float* sLam) {
-  constexpr int kGroups = kThreads / R;          // slice groups
-  constexpr int kChunk = 64;                     // slices per LDS round: 64 * R * 4 B = R * 256 B
-  static_assert(kGroups >= 1 && kGroups <= kWaves, "partials fit the statistics buffer");
-  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), nsl = P.n_slices;
-  const int r = tid % R, j = tid / R;
-  const float NEG_INF = -__builtin_inff();
-  const char* src = reinterpret_cast<const char*>(P.stats + (size_t)job * nsl * R);
-  const float* sF = reinterpret_cast<const float*>(sBuf);
-  float M = NEG_INF, Z = 0.f;
-  for (int c0 = 0; c0 < nsl; c0 += kChunk) {
-    const int n = min(kChunk, nsl - c0);
-    const int bytes = n * R * (int)sizeof(float), n_inst = (bytes + 1023) >> 10;   // 1 KiB per wave instruction
-    for (int i = wv; i < n_inst; i += kWaves) {
-      const int o = i * 1024 + lane * 16;
-      const char* g = src + (size_t)c0 * R * sizeof(float) + (o < bytes ? o : 0);
-      __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void*)g,
-                                       (__attribute__((address_space(3))) void*)(sBuf + i * 512), 16, 0, kCoherent);
-    }
-    loads_done();
-    __syncthreads();
-    // this chunk's maximum first, then the sum of exp2 against it (independent terms)
-    float m = NEG_INF;
-#pragma unroll 8
-    for (int c = j; c < n; c += kGroups) m = fmaxf(m, sF[c * R + r]);
-    float z = 0.f;
-    if (m > NEG_INF) {
-#pragma unroll 8
-      for (int c = j; c < n; c += kGroups) z += __builtin_amdgcn_exp2f(sF[c * R + r] - m);
-    }
-    combine_ms(M, Z, m, z);
-    __syncthreads();
-  }
-  sPart[j][r] = make_float2(M, Z);
-  __syncthreads();
-  if (tid < R) {
-    float m = sPart[0][tid].x, z = sPart[0][tid].y;
-#pragma unroll
-    for (int q = 1; q < kGroups; ++q) combine_ms(m, z, sPart[q][tid].x, sPart[q][tid].y);
-    const float lam = z > 0.f ? m + __log2f(z) : __builtin_inff();
-    store_coherent(P.lam + (size_t)job * R + tid, lam);
-    sLam[tid] = lam;
-  }
-}
-
 // s_waitcnt vmcnt(N) (expcnt and lgkmcnt not waited for).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
@@ -468,16 +118,6 @@ __device__ __forceinline__ void dma16(const void* src, uint32_t lds_base) {
       "global_load_lds_dwordx4 %1, off\n\ts_mov_b32 m0, %0"
       : "=&s"(saved)
       : "v"(src), "s"(lds_base)
-      : "memory");
-}
-// The same with a wave-uniform base address in SGPRs and a 32-bit per-lane byte offset.
-__device__ __forceinline__ void dma16s(const void* base, uint32_t off, uint32_t lds_base) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\ts_mov_b32 m0, %3\n\ts_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, %2\n\ts_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(off), "s"(base), "s"(lds_base)
       : "memory");
 }
 // Two of those 4 KiB apart: [base + off] -> lds_base and [base + 4096 + off] -> lds_base + 4096
@@ -548,252 +188,6 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_waitcnt(0xc07f);   // vmcnt 63 (no wait), expcnt 7 (no wait), lgkmcnt 0
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-}
-
-// issue_q_to_lds through dma16: the compiler then inserts no waits for it before unrelated LDS
-// reads; the consumer waits for vmcnt explicitly before its barrier.
-template <int NRT, int NTH>
-__device__ __forceinline__ void issue_q_to_lds_asm(uint16_t* sQ, const uint16_t* qjob, int G, int w) {
-  constexpr int R = NRT * 32;
-  constexpr int kPerWave = R * 16 / kThreads;
-  constexpr int kHeadRows = NTH * 32;
-  const int lane = threadIdx.x & 63, wv = wave_id();
-  const int lr = lane >> 4;
-  const int c = (lane & 15) ^ (((4 * wv) & 15) | lr);
-  const uint32_t lane_off = (uint32_t)(lr * kHeadDim + c * 8) * 2u;
-  const uint32_t pad_off = (uint32_t)(c * 8) * 2u;
-#pragma unroll
-  for (int i = 0; i < kPerWave; ++i) {
-    const int r0 = 4 * (i * kWaves + wv);
-    const int g = r0 / kHeadRows, ii0 = r0 - g * kHeadRows;
-    const bool ok = g < G && ii0 + lr < w;
-    const uint32_t off = ok ? (uint32_t)((g * w + ii0) * kHeadDim) * 2u + lane_off : pad_off;
-    dma16(reinterpret_cast<const char*>(qjob) + off, lds_addr(sQ + r0 * kHeadDim));
-  }
-}
-
-// ---------------------------------------------------------------------------------------------
-// Single-pass scoring (prompts whose slices of one job fit in the resident workgroups at once).
-// Workgroup w takes items w, w + n_wg, ...; per item the four waves each multiply one 32-key
-// tile of K (A operand, straight from HBM) by the job's query rows (B operand, LDS):
-//   phase A: lane = window row, registers = 16 keys -> tile row max, e = exp2(z - max) and row
-//     sums stay in the lane; the slice publishes one log2-normaliser per row and counts itself
-//     in; the last slice of the job folds all slices into the job's normalisers (NaN until
-//     written);
-//   phase B: once the job's normalisers are there, e is rescaled into probabilities and summed
-//     over the window rows with a 32-lane reduce-scatter (permlane16 swap + DPP), per query head
-//     for SnapKV, over the group for H2O; pooling and the group mean give S.
-// The job's first slice to count itself in folds the job once it reaches its own wait (it has
-// the most slack, so the fold never lands on the job's straggler).  Three workgroups share a CU
-// (four row tiles), so while one waits the others compute.
-// ---------------------------------------------------------------------------------------------
-template <int NRT, int NTH>
-__global__ __launch_bounds__(kThreads, NRT <= 4 ? 3 : 1) void score_fused_kernel(const PrefillLaunch P, int n_wg) {
-  constexpr int R = NRT * 32;
-  constexpr int NG = NRT / NTH;
-  __shared__ __attribute__((aligned(16))) uint16_t sQ[R * kHeadDim];
-  __shared__ float2 sStat[kWaves][R];
-  __shared__ float sLam[R];
-  __shared__ float sCol[NG][kSlice];
-  __shared__ int sFlag;
-
-  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
-  const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
-  const int nsl = P.n_slices;
-  const int n_jobs = B * P.n_window * Hkv;
-  const int64_t n_items = (int64_t)n_jobs * nsl;
-  const float sl2 = P.scale_log2;
-  const float inv_g = 1.f / (float)G;
-  const float NEG_INF = -__builtin_inff();
-  uint32_t* status = P.counters;
-  const bool padded_rows = (G * NTH < NRT) || (w != NTH * 32);
-
-  const int64_t first = blockIdx.x;
-  if (first >= n_items) return;
-  const int T = (int)((n_items - 1 - first) / n_wg + 1);
-  const int dj = n_wg / nsl, ds = n_wg - dj * nsl;   // item stride n_wg in (jobs, slices)
-  u32x4 kf[8];
-
-  // the item's query block (LDS DMA) and this wave's K tile (registers)
-  auto issue_loads = [&](const PipeRef& j) {
-    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
-    issue_q_to_lds_asm<NRT, NTH>(sQ, ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim, G, w);
-    load_k_tile(kf, ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim, j.slice * kSlice + wv * 32 + ln, L, hf);
-  };
-
-  // ---- phase A: logits and exponentials; lane = window row ln of row tile rt, registers = keys
-  // tile_key0 + 8(r/4) + 4hf + r%4; the tile row maxima (log2 units, 0 for rows with no visible
-  // key) go to mw, the per-wave (max, sum) pairs to sStat
-  auto phase_a = [&](const PipeRef& j, f32x16 (&e)[NRT], float (&mw)[NRT]) {
-    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // the item's query block and K tile
-    lds_barrier();
-    const int tile_key0 = j.slice * kSlice + wv * 32;
-    const bool mask_a = padded_rows || tile_key0 + 32 > L - w;
-#pragma unroll
-    for (int rt = 0; rt < NRT; ++rt) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) e[rt][r] = 0.f;
-#pragma unroll
-      for (int st = 0; st < 8; ++st)
-        e[rt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[st]), q_frag(sQ, rt * 32 + ln, 8 * hf + st), e[rt],
-                                                        0, 0, 0);
-      if (__builtin_expect(mask_a, 0)) {
-        const int g = rt / NTH, ii = (rt - g * NTH) * 32 + ln;
-        const int last = (g < G && ii < w) ? min(L - 1, L - w + ii) : -1;
-        const int lim = last - tile_key0 - 4 * hf;   // register r holds key tile_key0 + 4 hf + 8 (r / 4) + r % 4
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (8 * (r >> 2) + (r & 3) > lim) e[rt][r] = NEG_INF;
-      }
-      // both half-waves hold the same rows, other keys
-      float m = fmaxf(e[rt][0], e[rt][1]);
-#pragma unroll
-      for (int r = 2; r < 16; ++r) m = fmaxf(m, e[rt][r]);
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-      m = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-      mw[rt] = m == NEG_INF ? 0.f : m * sl2;
-      float z = 0.f;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        e[rt][r] = __builtin_amdgcn_exp2f(fmaf(e[rt][r], sl2, -mw[rt]));
-        z += e[rt][r];
-      }
-      const auto sz = __builtin_amdgcn_permlane32_swap(__float_as_uint(z), __float_as_uint(z), false, false);
-      z = __uint_as_float(sz[0]) + __uint_as_float(sz[1]);
-      if (hf == 0) sStat[wv][rt * 32 + ln] = make_float2(mw[rt], z);
-    }
-    lds_barrier();
-  };
-
-  // ---- publish the slice's statistics and count it in (the stores retire first).  Returns
-  // whether this slice came first: that workgroup folds the job once it has to wait for it anyway
-  // (the first slice has the most slack, so folding never lands on the job's straggler).
-  auto publish = [&](const PipeRef& j) -> bool {
-    if (tid < R) {
-      float M = NEG_INF, Z = 0.f;
-#pragma unroll
-      for (int v = 0; v < kWaves; ++v) combine_ms(M, Z, sStat[v][tid].x, sStat[v][tid].y);
-      store_coherent(P.stats + ((size_t)j.job * nsl + j.slice) * R + tid, Z > 0.f ? M + __log2f(Z) : NEG_INF);
-    }
-    vmem_release();
-    lds_barrier();
-    uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + j.job);
-    if (tid == 0) sFlag = (int)__hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    lds_barrier();
-    return sFlag == 0;
-  };
-
-  // ---- the folder: wait (bounded, one lane) until every slice has counted itself in, then fold
-  // (the normalisers go to memory over their NaN marks and to sLam); the query block's LDS space
-  // stages the statistics (the next block loads after the wait)
-  auto fold = [&](const PipeRef& j) {
-    if (tid == 0) {
-      uint32_t* cnt = P.counters + (size_t)kCounterStride * (1 + j.job);
-      uint32_t it = 0;
-      while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < (uint32_t)nsl) {
-        __builtin_amdgcn_s_sleep(1);
-        if (++it > kSpinLimit) {
-          atomicOr(status, 1u);
-          break;
-        }
-      }
-    }
-    lds_barrier();
-    vmem_acquire();
-    fold_job_fused<R>(P, j.job, sQ, sStat, sLam);
-  };
-
-  // ---- wait (bounded) for the job's normalisers: wave 0 reads all of them at once until none is
-  // still marked "not written"
-  auto wait_lam = [&](const PipeRef& j) {
-    const float* lj = P.lam + (size_t)j.job * R;
-    uint32_t it = 0;
-    while (true) {
-      float v[R / 64];
-#pragma unroll
-      for (int u = 0; u < R / 128; ++u) {
-        const float2 x = load_coherent2(lj + 128 * u + 2 * lane);
-        v[2 * u] = x.x;
-        v[2 * u + 1] = x.y;
-      }
-      bool ok = true;
-#pragma unroll
-      for (int u = 0; u < R / 64; ++u) ok = ok && (v[u] == v[u]);
-      const bool done = __builtin_amdgcn_ballot_w64(!ok) == 0;
-      if (done || ++it > kSpinLimit) {
-        if (!done && lane == 0) atomicOr(status, 1u);
-#pragma unroll
-        for (int u = 0; u < R / 128; ++u) {
-          sLam[128 * u + 2 * lane] = v[2 * u] == v[2 * u] ? v[2 * u] : __builtin_inff();
-          sLam[128 * u + 2 * lane + 1] = v[2 * u + 1] == v[2 * u + 1] ? v[2 * u + 1] : __builtin_inff();
-        }
-        break;
-      }
-      __builtin_amdgcn_s_sleep(1);
-    }
-  };
-
-  // ---- phase B: probabilities and their sums over the window rows (across lanes), then scores
-  auto phase_b = [&](const PipeRef& j, f32x16 (&e)[NRT], const float (&mw)[NRT]) {
-    const bool snap = P.layer[P.slot_layer[j.slot]].rule == RKV_SNAPKV;
-    float alpha[NRT];
-#pragma unroll
-    for (int rt = 0; rt < NRT; ++rt) alpha[rt] = __builtin_amdgcn_exp2f(mw[rt] - sLam[rt * 32 + ln]);   // +inf -> 0
-    const int sel = rs_sel(lane);
-    if (snap && NG > 1) {
-      // per query head: fold the head's row tiles into e[g] (in place; head g's sources come
-      // after index g, so nothing is overwritten before it is read)
-#pragma unroll
-      for (int g = 0; g < NG; ++g)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float x = alpha[g * NTH] * e[g * NTH][r];
-#pragma unroll
-          for (int u = 1; u < NTH; ++u) x = fmaf(alpha[g * NTH + u], e[g * NTH + u][r], x);
-          e[g][r] = x;
-        }
-      f32x16 (&ev)[NG] = *reinterpret_cast<f32x16(*)[NG]>(&e[0]);
-      reduce_scatter32_v<NG>(ev, lane);
-#pragma unroll
-      for (int i = 0; i < NG / 2; ++i) {
-        const int vi = 32 * i + sel, g = vi >> 4, r = vi & 15;
-        sCol[g][wv * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)] = ev[i >> 4][i & 15];
-      }
-    } else {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = alpha[0] * e[0][r];
-#pragma unroll
-        for (int rt = 1; rt < NRT; ++rt) x = fmaf(alpha[rt], e[rt][r], x);
-        e[0][r] = x;
-      }
-      f32x16 (&ev)[1] = *reinterpret_cast<f32x16(*)[1]>(&e[0]);
-      reduce_scatter32_v<1>(ev, lane);
-      if ((lane & 1) == 0) {
-        const int r = sel & 15;
-        sCol[0][wv * 32 + 8 * (r >> 2) + 4 * hf + (r & 3)] = ev[0][0];
-      }
-    }
-    lds_barrier();
-    store_scores<NG>(P, snap, j.job, j.slice, j.slice * kSlice, sCol, inv_g);
-  };
-
-  f32x16 e[NRT];
-  float mw[NRT];
-  PipeRef jc = pipe_item(first, nsl, B, Hkv);
-  issue_loads(jc);
-#pragma unroll 1
-  for (int t = 0; t < T; ++t) {
-    phase_a(jc, e, mw);
-    if (publish(jc)) fold(jc);
-    else if (wv == 0) wait_lam(jc);
-    lds_barrier();
-    PipeRef jn = jc;
-    pipe_advance(jn, dj, ds, nsl, B, Hkv);
-    if (t + 1 < T) issue_loads(jn);   // sQ is free; the loads land during phase B
-    phase_b(jc, e, mw);
-    jc = jn;
-  }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1321,225 +715,6 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   }
 }
 
-// ---------------------------------------------------------------------------------------------
-// Scoring.  NRT = row tiles (query heads x row tiles per head, padded), NTH = row tiles per head.
-// Workgroup w owns items first = w, w + n_wg, ...; iteration t runs pass A of its item t and
-// pass B of its item t - lag:
-//   A: logits with keys as the MFMA A operand (lane = window row, registers = 16 keys), the
-//      tile row max and sum of exp2 inside the lane, folded over the four waves and published
-//      per slice; the slice counts itself in at the start of the next iteration (after its
-//      stores have completed), and the job's last slice folds the normalisers;
-//   B: the same logits with the queries as the A operand (lane = key, registers = 16 rows),
-//      accumulator started at -normaliser, so exp2 gives probabilities; the column sums over
-//      the window rows stay inside the lane.
-// Pass B re-reads a K tile this workgroup streamed `lag` iterations earlier (L2 / MALL hits);
-// `lag` covers the iterations a job spans, so a workgroup never waits on its own later work.
-// ---------------------------------------------------------------------------------------------
-template <int NRT, int NTH>
-__global__ __launch_bounds__(kThreads, NRT <= 4 ? 2 : 1) void score_kernel(const PrefillLaunch P, int n_wg, int lag) {
-  constexpr int R = NRT * 32;
-  constexpr int NG = NRT / NTH;
-  __shared__ __attribute__((aligned(16))) uint16_t sQA[R * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t sQB[R * kHeadDim];
-  __shared__ float2 sStat[kWaves][R];
-  __shared__ __attribute__((aligned(16))) float sLam[R];   // -normaliser in logit units, pass B item
-  __shared__ float sCol[NG][kSlice];
-  __shared__ int sFold;
-
-  const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), hf = lane >> 5, ln = lane & 31;
-  const int L = P.seq_len, w = P.window, G = P.group, Hkv = P.n_kv_heads, B = P.batch, Hq = P.n_q_heads;
-  const int nsl = P.n_slices;
-  const int n_jobs = B * P.n_window * Hkv;
-  const int64_t n_items = (int64_t)n_jobs * nsl;
-  const float sl2 = P.scale_log2;
-  const float inv_g = 1.f / (float)G;
-  const float NEG_INF = -__builtin_inff();
-  uint32_t* status = P.counters;
-  const bool padded_rows = (G * NTH < NRT) || (w != NTH * 32);
-
-  const int64_t first = blockIdx.x;
-  if (first >= n_items) return;
-  const int T = (int)((n_items - 1 - first) / n_wg + 1);
-  const int dj = n_wg / nsl, ds = n_wg - dj * nsl;   // item stride n_wg in (jobs, slices)
-  auto step = [&](JobRef r) {
-    advance(r, dj, ds, nsl, B, Hkv);
-    return r;
-  };
-  auto q_of = [&](const JobRef& j) -> const uint16_t* {
-    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
-    return ly.q + (size_t)(j.s * Hq + j.h * G) * w * kHeadDim;
-  };
-  auto k_tile = [&](u32x4 (&dst)[8], const JobRef& j) {
-    const PrefillLayer& ly = P.layer[P.slot_layer[j.slot]];
-    load_k_tile(dst, ly.k + (size_t)(j.s * Hkv + j.h) * L * kHeadDim, j.slice * kSlice + wv * 32 + ln, L, hf);
-  };
-
-  u32x4 kA[8], kB[8];   // each reloaded as soon as its MFMAs have consumed it
-  const JobRef j0 = decode_item(first, nsl, B, Hkv);
-  issue_q_to_lds<NRT, NTH>(sQA, q_of(j0), G, w);
-  k_tile(kA, j0);
-  uint32_t arrived = 0;   // thread 0: arrival count returned for the previous pass A item
-  JobRef ja = j0, jb = j0, jp = j0;   // pass A item t, pass B item t - lag, pass A item t - 1
-  float lam_pre = 0.f;   // thread tid < R: normaliser of the next pass B item, loaded an iteration early
-
-#pragma unroll 1
-  for (int t = 0; t < T + lag; ++t) {
-    const bool doA = t < T, doB = t >= lag;
-    __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xf << 8));   // operands of this iteration, stats stores of t-1
-    lds_barrier();
-    const bool had_prev = t >= 1 && t - 1 < T;
-    if (had_prev && tid == 0)
-      arrived = __hip_atomic_fetch_add(P.counters + (size_t)kCounterStride * (1 + jp.job), 1u, __ATOMIC_RELAXED,
-                                        __HIP_MEMORY_SCOPE_AGENT);
-    // this iteration's pass B normaliser (loaded last iteration) and the next one's, issued now so
-    // that nothing queues in front of it
-    const float lam_cur = lam_pre;
-    if (t + 1 >= lag && t + 1 - lag < T && tid < R) {
-      const JobRef jq = t + 1 == lag ? j0 : step(jb);
-      lam_pre = load_coherent(P.lam + (size_t)jq.job * R + tid);
-    }
-
-    // ============================================================ pass B: window column sums
-    const JobRef jbn = step(jb), jan = step(ja);   // the items after this iteration's
-    if (doB) {
-      const PrefillLayer& ly = P.layer[P.slot_layer[jb.slot]];
-      const bool snap = ly.rule == RKV_SNAPKV;
-      const int cbase = jb.slice * kSlice, key = cbase + wv * 32 + ln;
-      if (tid < R) {
-        float lam = lam_cur;
-        uint32_t it = 0;
-        while (lam != lam) {   // not folded when prefetched (bounded wait)
-          __builtin_amdgcn_s_sleep(2);
-          lam = load_coherent(P.lam + (size_t)jb.job * R + tid);
-          if (++it > kSpinLimit) {
-            atomicOr(status, 1u);
-            lam = __builtin_inff();
-          }
-        }
-        sLam[tid] = -lam / sl2;
-      }
-      lds_barrier();
-      // lane = key, registers = rows rt*32 + 8(r/4) + 4hf + r%4; accumulators start at -normaliser
-      const bool edge_tile = cbase + wv * 32 + 32 > L - w;
-      float col[NG];
-#pragma unroll
-      for (int g = 0; g < NG; ++g) col[g] = 0.f;
-#pragma unroll
-      for (int rt = 0; rt < NRT; ++rt) {
-        f32x16 acc;
-#pragma unroll
-        for (int q4 = 0; q4 < 4; ++q4) {
-          const float4 lv = *reinterpret_cast<const float4*>(sLam + rt * 32 + 8 * q4 + 4 * hf);
-          acc[4 * q4] = lv.x;
-          acc[4 * q4 + 1] = lv.y;
-          acc[4 * q4 + 2] = lv.z;
-          acc[4 * q4 + 3] = lv.w;
-        }
-#pragma unroll
-        for (int st = 0; st < 8; ++st)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(q_frag(sQB, rt * 32 + ln, 8 * hf + st), as_bf16x8(kB[st]), acc,
-                                                        0, 0, 0);
-        if (rt == NRT - 1 && t + 1 - lag < T) k_tile(kB, jbn);   // next pass B tile (L2 / MALL)
-        float sum = 0.f;
-        if (__builtin_expect(edge_tile, 0)) {
-          // rows see keys up to L - w + ii; register r holds row ii = (rt % NTH) 32 + 4 hf + 8 (r / 4) + r % 4
-          const int lim = L - w + (rt % NTH) * 32 + 4 * hf - key;
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float pr = __builtin_amdgcn_exp2f(acc[r] * sl2);
-            sum += (key < L && 8 * (r >> 2) + (r & 3) >= -lim) ? pr : 0.f;
-          }
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(acc[r] * sl2);
-        }
-        col[rt / NTH] += sum;
-      }
-      // both half-waves hold the same key, other rows
-      if (snap && NG > 1) {
-#pragma unroll
-        for (int g = 0; g < NG; ++g) {
-          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(col[g]), __float_as_uint(col[g]), false, false);
-          if (hf == 0) sCol[g][wv * 32 + ln] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-        }
-      } else {
-        float c = col[0];
-#pragma unroll
-        for (int g = 1; g < NG; ++g) c += col[g];
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(c), __float_as_uint(c), false, false);
-        if (hf == 0) sCol[0][wv * 32 + ln] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
-      }
-      lds_barrier();
-      if (t + 1 - lag < T) issue_q_to_lds<NRT, NTH>(sQB, q_of(jbn), G, w);   // sQB no longer read
-
-      store_scores<NG>(P, snap, jb.job, jb.slice, cbase, sCol, inv_g);
-    } else if (t + 1 - lag == 0) {
-      issue_q_to_lds<NRT, NTH>(sQB, q_of(j0), G, w);
-      k_tile(kB, j0);
-    }
-
-    // ============================================================ pass A: row statistics
-    if (doA) {
-      const int tile_key0 = ja.slice * kSlice + wv * 32;
-      const bool mask_a = padded_rows || tile_key0 + 32 > L - w;
-#pragma unroll
-      for (int rt = 0; rt < NRT; ++rt) {
-        f32x16 acc;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-#pragma unroll
-        for (int st = 0; st < 8; ++st)
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kA[st]), q_frag(sQA, rt * 32 + ln, 8 * hf + st), acc,
-                                                        0, 0, 0);
-        if (rt == NRT - 1 && t + 1 < T) k_tile(kA, jan);   // next pass A tile from HBM
-        // lane = window row ln of row tile rt, registers = keys tile_key0 + 8(r/4) + 4hf + r%4
-        if (__builtin_expect(mask_a, 0)) {
-          const int g = rt / NTH, ii = (rt - g * NTH) * 32 + ln;
-          const int last = (g < G && ii < w) ? min(L - 1, L - w + ii) : -1;
-          const int lim = last - tile_key0 - 4 * hf;   // register r holds key tile_key0 + 4 hf + 8 (r / 4) + r % 4
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (8 * (r >> 2) + (r & 3) > lim) acc[r] = NEG_INF;
-        }
-        // both half-waves hold the same rows, other keys
-        float m = fmaxf(acc[0], acc[1]);
-#pragma unroll
-        for (int r = 2; r < 16; ++r) m = fmaxf(m, acc[r]);
-        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
-        m = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
-        const float mw = m == NEG_INF ? 0.f : m * sl2;
-        float z = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) z += __builtin_amdgcn_exp2f(fmaf(acc[r], sl2, -mw));
-        const auto sz = __builtin_amdgcn_permlane32_swap(__float_as_uint(z), __float_as_uint(z), false, false);
-        z = __uint_as_float(sz[0]) + __uint_as_float(sz[1]);
-        if (hf == 0) sStat[wv][rt * 32 + ln] = make_float2(mw, z);
-      }
-      lds_barrier();
-      if (t + 1 < T) issue_q_to_lds<NRT, NTH>(sQA, q_of(jan), G, w);   // sQA no longer read
-      if (tid < R) {
-        float M = NEG_INF, Z = 0.f;
-#pragma unroll
-        for (int v = 0; v < kWaves; ++v) combine_ms(M, Z, sStat[v][tid].x, sStat[v][tid].y);
-        store_coherent(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + tid, Z > 0.f ? M + __log2f(Z) : NEG_INF);
-      }
-    }
-
-    // ============================================================ the previous item's arrival
-    if (had_prev) {
-      lds_barrier();   // sStat is read above
-      if (tid == 0) sFold = (arrived == (uint32_t)(nsl - 1)) ? jp.job : -1;
-      lds_barrier();
-      if (sFold >= 0) fold_job_regs<R>(P, sFold, sStat);
-    }
-    if (doA) {
-      jp = ja;
-      ja = jan;
-    }
-    if (doB) jb = jbn;
-  }
-}
-
 // Ranking key of a score: its bit pattern, whose unsigned order is the numeric order for the
 // non-negative scores the scoring kernels produce.  Patterns with the sign bit set (which no
 // valid score has) rank as +0, so the radix passes, which look at bits 0-30 only, and the
@@ -1551,8 +726,8 @@ __device__ __forceinline__ uint32_t rank_bits(float v) {
 }
 
 // ---------------------------------------------------------------------------------------------
-// Exact rescoring of one window-scored job (the repair path).  The pipelined scoring kernel takes
-// its exponentials against a fixed per-row reference; a row with a key far above it overflows
+// Exact rescoring of one window-scored job (the repair path).  The window scoring kernels take
+// their exponentials against a fixed per-row reference; a row with a key far above it overflows
 // the row sum, and the kernel flags the job (word 1 of the job's counter line).  The selection
 // workgroup of a flagged job recomputes the job's scores here, in plain fp32 arithmetic with a
 // running maximum per row (no reference, so nothing overflows), before it ranks them:
@@ -1563,11 +738,13 @@ __device__ __forceinline__ uint32_t rank_bits(float v) {
 //           group mean, Su the plain group mean, as the scoring kernels store them.
 // It is slow (two passes of scalar FMAs over the job) and only runs for flagged jobs; inlined,
 // with the query rows read from LDS, so the selection kernels need no stack.  Needs
-// G * w <= 128 (the pipelined kernel's limit) and kRepairLds bytes of LDS at `lds`.
+// G * w <= kRepairRows (256, every window-scored layout), blockDim >= kRepairRows and kRepairLds
+// bytes of LDS at `lds`.
 // ---------------------------------------------------------------------------------------------
-constexpr int kRepairRows = 128;
-constexpr int kRepairKeyLanes = 8;   // blockDim / 128 at most
+constexpr int kRepairRows = kMaxRowTiles * 32;   // G * w of the window-scored layouts
+constexpr int kRepairKeyLanes = 4;               // blockDim / kRepairRows at most
 constexpr int kRepairLds = (kRepairRows * kHeadDim * 2) + 4 * (2 * kRepairRows + 2 * kRepairKeyLanes * kRepairRows + 8 * 1024);
+static_assert(kRepairLds <= kSelectLds, "the repair runs in the selection kernels' dynamic LDS");
 
 __device__ __forceinline__ void rescore_exact(const uint16_t* qjob, const uint16_t* khead, float* S, float* Su, int L,
                                            int w, int G, int ph, int snap, float sl2, float* lds) {
@@ -2150,13 +1327,6 @@ int device_cus() {
   return cached;
 }
 
-template <typename K>
-int resident_groups(K kernel) {
-  int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess || per_cu < 1) per_cu = 1;
-  return per_cu * device_cus();
-}
-
 // Resident workgroups of the pipelined kernel (one per CU; the same for every NTH).
 int resident_pipe_groups() {
   int per_cu = 0;
@@ -2164,28 +1334,6 @@ int resident_pipe_groups() {
       per_cu < 1)
     per_cu = 1;
   return per_cu * device_cus();
-}
-
-template <int NRT, int NTH>
-int launch_score(const PrefillLaunch& P, hipStream_t st, void* stream) {
-  const int64_t n_items = (int64_t)P.batch * P.n_window * P.n_kv_heads * P.n_slices;
-  if (n_items <= 0) return 0;
-  static const int fused_wg = resident_groups(score_fused_kernel<NRT, NTH>);
-  static const int lagged_wg = resident_groups(score_kernel<NRT, NTH>);
-  profile_mark(kStageScore, false, stream);
-  if (P.n_slices <= fused_wg / 2 && P.force_two_pass != 1) {
-    // every workgroup is resident and a job's slices are all in flight while they wait
-    const int n_wg = (int)std::min<int64_t>(n_items, fused_wg);
-    score_fused_kernel<NRT, NTH><<<n_wg, kThreads, 0, st>>>(P, n_wg);
-  } else {
-    const int n_wg = (int)std::min<int64_t>(n_items, lagged_wg);
-    // pass B trails pass A by `lag` items: at least the iterations one job spans inside a
-    // workgroup plus one for the fold, and enough to absorb the drift between workgroups
-    const int lag = std::max(P.score_lag, (P.n_slices + n_wg - 1) / n_wg + 2);
-    score_kernel<NRT, NTH><<<n_wg, kThreads, 0, st>>>(P, n_wg, lag);
-  }
-  profile_mark(kStageScore, true, stream);
-  return 0;
 }
 
 }  // namespace
@@ -2197,10 +1345,10 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   const int n_sel = P.batch * P.n_scored * P.n_kv_heads;
   const int ntg = P.row_tiles_per_group;
   // the pipelined kernel takes four row tiles when a job has at most 64 slices (8192 keys) and
-  // every slice of a job fits in the resident workgroups (RKV_FORCE_TWO_PASS selects the older
-  // kernels for tests: 1 two-pass, 2 single-pass)
+  // every slice of a job fits in the resident workgroups; other layouts take the window kernels
+  // (window.hip), which the test hook RKV_FORCE_WINDOW=1 selects everywhere
   static const int pipe_wg = resident_pipe_groups();
-  const bool pipe = n_jobs > 0 && row_tiles == 4 && P.force_two_pass == 0 && P.n_slices <= 64 &&
+  const bool pipe = n_jobs > 0 && row_tiles == 4 && P.force_window == 0 && P.n_slices <= kPipeMaxSlices &&
                     P.n_slices <= pipe_wg;
   profile_mark(kStageZero, false, stream);
   if (pipe) {
@@ -2208,35 +1356,25 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
     else if (ntg == 2) prepare_kernel<2><<<n_jobs * 4, 256, 0, st>>>(P);
     else prepare_kernel<4><<<n_jobs * 4, 256, 0, st>>>(P);
   } else {
-    const int n_lam = n_jobs * row_tiles * 32;
     const int n_cnt = kCounterStride * (1 + n_jobs);
-    const int blocks = std::max(1, std::min(64, (std::max(n_lam, n_cnt) + 255) / 256));
-    reset_counters<<<blocks, 256, 0, st>>>(P.counters, n_cnt, reinterpret_cast<uint32_t*>(P.lam), n_lam, P.first_group);
+    const int blocks = std::max(1, std::min(64, (n_cnt + 255) / 256));
+    reset_counters<<<blocks, 256, 0, st>>>(P.counters, n_cnt, P.first_group);
   }
   profile_mark(kStageZero, true, stream);   // the status word is cleared even without jobs
   if (n_jobs > 0) {
-    int err = 0;
+    profile_mark(kStageScore, false, stream);
     if (pipe) {
       const int64_t n_items = (int64_t)n_jobs * P.n_slices;
       const int n_wg = (int)std::min<int64_t>(n_items, pipe_wg);
-      profile_mark(kStageScore, false, stream);
       if (ntg == 1) score_pipe_kernel<1><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
       else if (ntg == 2) score_pipe_kernel<2><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
       else score_pipe_kernel<4><<<n_wg, kPipeThreads, 0, st>>>(P, n_wg);
-      profile_mark(kStageScore, true, stream);
-    } else if (P.force_two_pass != 2) {
-      // longer prompts and eight row tiles: row normalisers, then column sums (window.hip)
-      profile_mark(kStageScore, false, stream);
-      err = launch_window(P, row_tiles, stream);
-      profile_mark(kStageScore, true, stream);
-    } else if (row_tiles == 4 && ntg == 1) err = launch_score<4, 1>(P, st, stream);
-    else if (row_tiles == 4 && ntg == 2) err = launch_score<4, 2>(P, st, stream);
-    else if (row_tiles == 4) err = launch_score<4, 4>(P, st, stream);
-    else if (ntg == 1) err = launch_score<8, 1>(P, st, stream);
-    else if (ntg == 2) err = launch_score<8, 2>(P, st, stream);
-    else if (ntg == 4) err = launch_score<8, 4>(P, st, stream);
-    else err = launch_score<8, 8>(P, st, stream);
-    if (err) return err;
+    } else {
+      // longer prompts and eight row tiles: row normalisers, then column sums
+      const int err = launch_window(P, row_tiles, stream);
+      if (err) return err;
+    }
+    profile_mark(kStageScore, true, stream);
   }
   if (P.n_full > 0) {
     // H2O layers with full-span accumulation: their own two passes, then the shared selection

@@ -59,14 +59,12 @@ struct PrefillLaunch {
   int32_t pool_half;      // pool_kernel / 2
   int32_t want_unpooled;  // write the unpooled group-mean score (acc seeding of SnapKV layers)
   float scale_log2;       // log2(e) / sqrt(d)
-  int32_t score_lag;      // two-pass scoring: items between pass A and pass B of the same item
-  int32_t force_two_pass; // use the two-pass scoring kernel even where the single-pass one applies
+  int32_t force_window;   // test hook: the window kernels even where the pipelined one applies
   // workspace regions
   uint32_t* counters;     // [0] status; job j's slice-arrival counter at [kCounterStride * (1 + j)]
-  float* stats;           // [J][n_slices][R][2]  per-slice row max (log2 units) and sum of exp2
-  float* lam;             // [J][R]  per-row log2 softmax normaliser (+inf for rows without keys); the
-                          //         pipelined kernel keeps the reciprocal row sum 1 / Z here instead
-  float* ncl;             // [J][R]  pipelined kernel: minus the per-row reference logit (0 for padding rows)
+  float* stats;           // [J][n_slices][128]  pipelined kernel: per-slice row sums (NaN until stored)
+  float* lam;             // [J][R]  window kernels: per-row log2 softmax normaliser (+inf for padding rows)
+  float* ncl;             // [J][128]  pipelined kernel: minus the per-row reference logit (0 for padding rows)
   float* lamf;            // [J_full][G][L]  full-span H2O: log2 normaliser of every query row
   float* tz;              // [J_tova][G][L]  TOVA: log2-scaled logits of the last query per head
   float* tstat;           // [J_tova][n_slices][G][2]  TOVA: per-slice (max, sum of exp2(x - max))
@@ -86,6 +84,8 @@ struct PrefillWorkspace {
 };
 PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half,
                                           int n_full_jobs, int n_tova_jobs);
+constexpr int kPipeRows = 128;      // window rows of a job in the pipelined scoring kernel
+constexpr int kPipeMaxSlices = 64;  // slices per job it takes (a lane reads four of 16 slices' row sums)
 
 // Error reporting (thread-local last error).
 int fail(int status, const std::string& msg);

@@ -180,24 +180,23 @@ def test_repeat_runs_are_bitwise_identical():
             assert torch.equal(a[key][l], b[key][l]), (key, l)
 
 
-@pytest.mark.parametrize("mode", ["1", "2"], ids=["window_two_kernel", "single_pass"])
-def test_other_scoring_kernels_match_oracle(monkeypatch, mode):
-    """The two-kernel window path (row normalisers, then column sums: prompts of more than 64
-    slices, eight row tiles) and the running-maximum single-pass kernel, forced through the test
-    hook on layouts the pipelined kernel would otherwise take: the 1K case and a ragged length."""
-    monkeypatch.setenv("RKV_FORCE_TWO_PASS", mode)
+def test_window_kernels_match_oracle_on_short_prompts(monkeypatch):
+    """The window scoring kernels (row normalisers, then column sums: prompts of more than 64
+    slices, eight row tiles), forced through the test hook on layouts the pipelined kernel would
+    otherwise take: the 1K case and a ragged length."""
+    monkeypatch.setenv("RKV_FORCE_WINDOW", "1")
     run_case([OP.SNAPKV, OP.H2O], [128, 128], [[gen(1, 0, 0, 1024)], [gen(1, 0, 1, 1024)]], window=32,
-             label=f"k{mode}_1k")
+             label="win_1k")
     run_case([OP.SNAPKV, OP.H2O], [100, 100], [[gen(7, 0, 0, 777)], [gen(7, 0, 1, 777)]], window=32,
-             label=f"k{mode}_777")
+             label="win_777")
 
 
 def overflow_input(L=1024, w=32):
     """One window row (query head 5, row 7) set to 4 in every dimension and one prefix key
     (position 300) to 4 in every dimension: that row's logit there is 4 * 4 * 128 / sqrt(128) =
     181, about 170 natural-log units above the row's reference (its logits with its own key and
-    with key 0), beyond the fp32 exponent range of the pipelined kernel's row sums."""
-    x = gen(12, 0, 0, L)
+    with key 0), beyond the fp32 exponent range of the scoring kernels' row sums."""
+    x = gen(12, 0, 0, L, w=w)
     q = x["q"].copy()
     k = x["k"].copy()
     four = f32_to_bf16_bits(np.full(128, 4.0, np.float32))
@@ -207,17 +206,21 @@ def overflow_input(L=1024, w=32):
 
 
 def test_reference_overflow_is_repaired(monkeypatch):
-    """The overflowing job is flagged by the pipelined kernel and rescored exactly by its
-    selection workgroup, through the default path: scores, retained sets, rows and acc match
-    the oracle, and the status word says RKV_STATUS_REPAIRED (outputs valid).  The two-kernel
-    window path (test hook) flags and repairs the same job; the running-maximum single-pass kernel
-    computes it directly, with a clean status."""
+    """The overflowing job is flagged by the scoring kernel and rescored exactly by its selection
+    workgroup: scores, retained sets, rows and acc match the oracle, and the status word says
+    RKV_STATUS_REPAIRED (outputs valid).  Through the pipelined kernel (the default here) and the
+    window kernels (test hook)."""
     y = overflow_input()
     run_case([OP.SNAPKV, OP.H2O], [128, 128], [[y], [y]], window=32, label="ref_overflow", status=4)
-    monkeypatch.setenv("RKV_FORCE_TWO_PASS", "1")
+    monkeypatch.setenv("RKV_FORCE_WINDOW", "1")
     run_case([OP.SNAPKV, OP.H2O], [128, 128], [[y], [y]], window=32, label="ref_overflow_window", status=4)
-    monkeypatch.setenv("RKV_FORCE_TWO_PASS", "2")
-    run_case([OP.SNAPKV], [128], [[y]], window=32, label="ref_overflow_single_pass")
+
+
+def test_reference_overflow_is_repaired_at_eight_row_tiles():
+    """w = 64 with four query heads per KV head: 256 window rows per job (eight row tiles), which
+    the window kernels score and the exact rescoring must cover in full."""
+    y = overflow_input(L=1536, w=64)
+    run_case([OP.SNAPKV, OP.H2O], [200, 200], [[y], [y]], window=64, label="ref_overflow_w64", status=4)
 
 
 def test_status_word_spans_every_launch_group():
