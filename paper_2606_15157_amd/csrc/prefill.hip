@@ -215,8 +215,11 @@ __device__ __forceinline__ void lds_barrier() {
 // cross-workgroup dependency is store -> load, with no counter and no designated folder.
 //
 // Schedule of iteration t (item t enters phase A, item t - 2 phase B, each in its own register
-// set; no wait is for an operation issued in the same iteration):
-//   B1
+// set; no wait is for an operation issued in the same iteration).  There is no barrier between
+// one iteration's score stores and the next phase A: every buffer phase A and MID touch was
+// handed on by B1.5 or B2 of the previous iteration, and the score stores read the sColP buffer
+// of their own iteration's parity, so a wave whose SIMD partner is still issuing DMA starts the
+// next item's MFMAs at once:
 //   A     logits (k-step fragments read one step ahead), exponentials, per-row partial sums per
 //         key tile into sStat
 //   MID   every wave: all its earlier memory operations have completed; the row sums of item
@@ -224,7 +227,8 @@ __device__ __forceinline__ void lds_barrier() {
 //         -> reciprocal normalisers in sAlpha; then the loads of item t - 1's row sums
 //   B1.5
 //   wave 0: store item t's row sums
-//   B     item t - 2: probabilities, sums over the window rows per query head (or group) into sColP
+//   B     item t - 2: probabilities, sums over the window rows per query head (or group) into
+//         sColP[t % 2]
 //   B2
 //   waves 0-3: scores of item t - 2; waves 4-7: LDS DMA of item t + 2 into the buffer item t has
 //         just left
@@ -325,7 +329,8 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   __shared__ __attribute__((aligned(16))) float sNcl[2][R];
   __shared__ __attribute__((aligned(16))) float sAlpha[R];
   __shared__ float sStat[4][R];
-  __shared__ float sColP[2][2][kSlice];
+  __shared__ float sColPb[2][2][2][kSlice];   // two buffers, by iteration parity
+  float (*sColP)[2][kSlice] = sColPb[0];
 
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), lg = lane >> 4, l16 = lane & 15;
   const int kt = wv & 3, rh = wv >> 2;
@@ -664,10 +669,16 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
 
   auto iteration = [&](int t, f32x4v (&ea)[4][2], f32x4v (&eb)[4][2]) {
     const bool doA = t < T, doB = t >= 2 && t - 2 < T;
-    // B1 (the DMA of item t was complete at MID of iteration t - 1; the first iteration waits
-    // for the two DMAs issued before the loop)
-    if (t == 0) wait_vmcnt<0>();
-    lds_barrier();
+    // No barrier here: the buffers this iteration reads were filled and handed on before B1.5 of
+    // iteration t - 1 (DMA of item t), B2 of t - 1 (sStat, sAlpha free again), and the score
+    // stores of iteration t - 1 read the other sColP buffer.  A wave may so start phase A while
+    // another wave of its SIMD is still issuing DMA.  The first iteration waits for the two
+    // DMAs issued before the loop.
+    if (t == 0) {
+      wait_vmcnt<0>();
+      lds_barrier();
+    }
+    sColP = sColPb[t & 1];
     // both phases run in every iteration (on stale data at the ends of the pipeline, with their
     // results unused), so each register set is redefined unconditionally
     phase_a(ja, t & 1, ea);
