@@ -11,7 +11,10 @@ Recipe, per (workload id, sequence, layer):
 2. Draw the window queries Q [Hq, w, d], keys K [Hkv, L, d] and values
    V [Hkv, L, d] as float32 N(0, 1), in that order.
 3. For each KV head h, take the mean query direction of its query group,
-   qbar = mean over the group's heads and window rows, and the unit-logit step
+   qbar = mean over the group's heads and the last min(w, 64) query rows (the
+   whole window of the window-scored workloads, w <= 64; the last 64 positions
+   of a full-span workload, whose queries cover all L positions, where a mean
+   over every position would be near zero and u enormous), and the unit-logit step
    u = sqrt(d) * qbar / |qbar|^2.  Adding a*u to a key raises the mean query's
    scaled logit (q.k / sqrt(d)) by exactly a, i.e. by a standard deviations of
    an N(0,1) logit.
@@ -36,6 +39,7 @@ SINK_SHIFT = 3.0
 HEAVY_SHIFT = 2.0
 RECENT_SHIFT = 1.0
 RECENT_SPAN = 64
+PLANT_ROWS = 64   # query rows (the last ones) whose mean sets the planted direction
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
@@ -82,7 +86,7 @@ def prefill_layer(workload: int, seq: int, layer: int, *, seq_len: int, n_q_head
     hh = np.zeros((Hkv, n), dtype=np.int64)
     if plant and L > 0:
         for h in range(Hkv):
-            qbar = q[h * G:(h + 1) * G].astype(np.float64).mean(axis=(0, 1))
+            qbar = q[h * G:(h + 1) * G, max(0, w - PLANT_ROWS):].astype(np.float64).mean(axis=(0, 1))
             u = (np.sqrt(d) * qbar / np.dot(qbar, qbar)).astype(np.float32)
             k[h, 0] += np.float32(SINK_SHIFT) * u
             if n > 0:
@@ -129,7 +133,7 @@ def prefill_layer_torch(workload: int, layer: int, *, batch: int, seq_len: int, 
     k = torch.randn((batch, Hkv, L, d), generator=gen, device=device, dtype=torch.float32)
     v = torch.randn((batch, Hkv, L, d), generator=gen, device=device, dtype=torch.float32)
     rec, hi, n = planted_positions(L, n_hh)
-    qbar = q.view(batch, Hkv, G, w, d).double().mean(dim=(2, 3))            # [B,Hkv,d]
+    qbar = q.view(batch, Hkv, G, w, d)[:, :, :, max(0, w - PLANT_ROWS):].double().mean(dim=(2, 3))   # [B,Hkv,d]
     u = (d ** 0.5 * qbar / (qbar * qbar).sum(-1, keepdim=True)).float()     # [B,Hkv,d]
     k[:, :, 0] += SINK_SHIFT * u
     hh = torch.zeros((batch, Hkv, n), dtype=torch.int64, device=device)

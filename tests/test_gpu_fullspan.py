@@ -81,3 +81,28 @@ def test_full_span_totals_at_8k():
     assert rkv.prefill_check(out["workspace"]) == 0
     tot = out["scores"][0].double().sum(-1).cpu().numpy()
     np.testing.assert_allclose(tot, L, rtol=1e-4)
+
+
+def test_full_span_sampled_head_at_8k():
+    """L = 8192, one H2O_FULL layer with budget 1024 (512 heavy hitters from [0, 7680), 512
+    recent): KV head 5's full-span scores (every one of the 8192 queries of its four query
+    heads), its retained set, gathered rows and acc seed against the oracle element by element.
+    The oracle takes that head's slice alone: KV heads are independent problems."""
+    import paper_2606_15157_amd as rkv
+    import torch
+    L, h, G, b = 8192, 5, 4, 1024
+    x = gen(34, 0, 0, L, L)
+    plan = rkv.Plan([OP.H2O_FULL], [b], window=32)
+    q, k, v = (bits_to_torch(x[n][None]) for n in ("q", "k", "v"))
+    out = rkv.evict_prefill(plan, [q], [k], [v], score_out=True, acc_out=True)
+    torch.cuda.synchronize()
+    assert rkv.prefill_check(out["workspace"]) == 0
+    ora = OP.evict_layer(OP.H2O_FULL, b, x["q"][G * h:G * h + G], x["k"][h:h + 1], x["v"][h:h + 1], window=32)
+    what = f"H2O_FULL L={L} head {h}"
+    sc = out["scores"][0][0, h].cpu().numpy()
+    check_scores(sc[:ora["scores"].shape[1]], ora["scores"][0], what)
+    idx = out["idx"][0][0, h].cpu().numpy()
+    check_retained(idx, ora, 0, L, what)
+    check_gather(torch_to_bits(out["k_out"][0])[0, h], torch_to_bits(out["v_out"][0])[0, h], x["k"][h], x["v"][h],
+                 idx, what)
+    check_scores(out["acc"][0][0, h].cpu().numpy(), ora["acc"][0], what + " acc")
