@@ -1,7 +1,8 @@
 """HBM traffic of the scoring kernel from two rocprofv3 counter runs.
 
     rocprofv3 --pmc FETCH_SIZE --output-format csv -d <dir_fetch> -o run -- python3 bench.py \
-        --steps 5 --warmup 2 --no-cpu-baseline --copy-calibration
+        --steps 5 --warmup 2 --no-cpu-baseline --no-configs --no-decode --no-entropy --no-fullspan \
+        --copy-calibration
     rocprofv3 --pmc WRITE_SIZE --output-format csv -d <dir_write> -o run -- (same command)
     python -m paper_2606_15157_amd.pmc_summary <dir_fetch> <dir_write> <out.json> <out.md>
 
@@ -30,6 +31,9 @@ KERNEL_SRC = os.path.join(ROOT, "paper_2606_15157_amd", "csrc", "prefill.hip")
 SCORE_NAME = "score_pipe_kernel<1>"
 COPY_NAME = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
+# the profiled program: the headline route only, plus the 1 GiB calibration copy
+BENCH_CMD = ("python3 bench.py --steps 5 --warmup 2 --no-cpu-baseline --no-configs --no-decode --no-entropy "
+             "--no-fullspan --copy-calibration")
 
 
 def per_dispatch(run_dir: str, counter: str):
@@ -87,10 +91,8 @@ def main(argv):
     with open(out_md, "w") as f:
         f.write(f"# HBM traffic of {name} (32-layer mixed route, L=8192)\n\n")
         f.write("Commands (each in its own run, from /tmp with TMPDIR=/tmp):\n\n")
-        f.write("    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <fetch> -o run -- python3 bench.py "
-                "--steps 5 --warmup 2 --no-cpu-baseline --copy-calibration\n")
-        f.write("    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write> -o run -- python3 bench.py "
-                "--steps 5 --warmup 2 --no-cpu-baseline --copy-calibration\n")
+        f.write(f"    rocprofv3 --pmc FETCH_SIZE --output-format csv -d <fetch> -o run -- {BENCH_CMD}\n")
+        f.write(f"    rocprofv3 --pmc WRITE_SIZE --output-format csv -d <write> -o run -- {BENCH_CMD}\n")
         f.write("    python -m paper_2606_15157_amd.pmc_summary <fetch> <write> <json> <md>\n\n")
         f.write("| quantity | value |\n|---|---|\n")
         for k in ("fetch_kib_median", "write_kib_median", "copy_fetch_kib", "copy_write_kib", "fetch_scale",
@@ -123,8 +125,7 @@ def sq_main(out_md, dirs, iterations=64):
         for d in dirs:
             path = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
             cs = sorted({row["Counter_Name"] for row in csv.DictReader(open(path[0]))})
-            f.write(f"    rocprofv3 --pmc {' '.join(cs)} --output-format csv -d <dir> -o run -- python3 bench.py "
-                    "--steps 3 --warmup 1 --no-cpu-baseline --no-decode --no-entropy --no-fullspan\n")
+            f.write(f"    rocprofv3 --pmc {' '.join(cs)} --output-format csv -d <dir> -o run -- {BENCH_CMD}\n")
         f.write(f"    python -m paper_2606_15157_amd.pmc_summary --sq <out.md> <dir> ...\n\n")
         f.write(f"{waves:.0f} waves; each runs {iterations} pipeline iterations.\n\n")
         f.write("| counter | value | share of SQ_WAVE_CYCLES |\n|---|---|---|\n")

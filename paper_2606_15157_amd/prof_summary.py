@@ -51,16 +51,22 @@ def first_dispatches(run_dir: str, kernel: str, n: int):
     return [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows[:n]]
 
 
+MAX_ROWS = 25   # the table lists the kernels with the largest total time
+
+
 def main(argv):
     run_dir, out_md, title, command = argv[1:5]
     rows = kernel_stats(run_dir)
     with open(out_md, "w") as f:
         f.write(f"# {title}\n\nCommand (from /tmp with TMPDIR=/tmp):\n\n    {command}\n\n")
         f.write("| kernel | calls | average (us) | min (us) | max (us) | share |\n|---|---|---|---|---|---|\n")
-        for r in rows:
+        for r in rows[:MAX_ROWS]:
             f.write(f"| {short_name(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.1f} | "
                     f"{float(r['MinNs']) / 1e3:.1f} | {float(r['MaxNs']) / 1e3:.1f} | "
                     f"{float(r['Percentage']):.1f}% |\n")
+        if len(rows) > MAX_ROWS:
+            rest = sum(float(r["Percentage"]) for r in rows[MAX_ROWS:])
+            f.write(f"| ({len(rows) - MAX_ROWS} more kernels) | | | | | {rest:.1f}% |\n")
         if len(argv) > 6:
             kernel, n = argv[5], int(argv[6])
             d = first_dispatches(run_dir, kernel, n)
