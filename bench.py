@@ -423,6 +423,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle", type=int, default=100,
+                    help="untimed passes of the headline route before the warm-up steps (power-state settling)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-step measurement")
@@ -468,6 +470,11 @@ def main():
     call = rkv.PreparedPrefill(plan, q, k, v, out, ws)
     stream = torch.cuda.current_stream(dev)
 
+    # settle, then the W warm-up steps: after the first few passes under load the GPU's power
+    # management slows this kernel by up to ~15 % for a few tens of passes before it settles
+    # (kernel-trace durations 181 -> 207 -> 177 us), so that transient is run off untimed first
+    for _ in range(args.settle):
+        call(stream)
     for _ in range(args.warmup):
         call(stream)
     torch.cuda.synchronize()
@@ -538,6 +545,7 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_passes": args.settle,
         "ms_per_step": ms_step,
         "higher_is_better": True,
         "scaling": "weak",
@@ -574,6 +582,9 @@ def main():
             "frac": score_gbps / HBM_PEAK_GBPS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": score_bytes,
+            "timing": "the kernel's dispatch start and stop timestamps (HIP events) in a loop of K passes "
+                      "with only this stage profiled; profiled, the persistent kernel runs 10-20 % slower "
+                      "than in the unprofiled timed passes (kernel trace in profiles/), so this is a bound",
         },
     }
     del out, ws, call, q, k, v

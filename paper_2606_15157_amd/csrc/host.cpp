@@ -158,7 +158,22 @@ namespace {
 std::mutex g_prof_mu;
 int g_prof_stage = -1;
 std::vector<hipEvent_t> g_prof_events;  // begin/end pairs
+std::vector<hipEvent_t> g_prof_pool;    // created events not in use (taken by the marks, returned by the read)
 constexpr size_t kMaxProfiled = 4096;
+// Profiling events skip the system-scope memory fence of an ordinary event record (the kernels
+// they bracket need no fence to be timed).
+constexpr unsigned kProfEventFlags = hipEventDisableSystemFence;
+constexpr size_t kProfPoolFill = 1024;   // events created when profiling is enabled
+
+// An event from the pool (created on demand when the pool is empty); g_prof_mu held.
+bool take_event(hipEvent_t* e) {
+  if (!g_prof_pool.empty()) {
+    *e = g_prof_pool.back();
+    g_prof_pool.pop_back();
+    return true;
+  }
+  return hipEventCreateWithFlags(e, kProfEventFlags) == hipSuccess;
+}
 }  // namespace
 
 void profile_mark(int stage, bool end, void* stream) {
@@ -167,12 +182,29 @@ void profile_mark(int stage, bool end, void* stream) {
   if (!end && g_prof_events.size() >= 2 * kMaxProfiled) return;
   if (end && g_prof_events.size() % 2 == 0) return;  // begin was dropped
   hipEvent_t e;
-  if (hipEventCreate(&e) != hipSuccess) return;
+  if (!take_event(&e)) return;
   if (hipEventRecord(e, reinterpret_cast<hipStream_t>(stream)) != hipSuccess) {
-    (void)hipEventDestroy(e);
+    g_prof_pool.push_back(e);
     return;
   }
   g_prof_events.push_back(e);
+}
+
+bool profile_kernel_events(int stage, void** start, void** stop) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  *start = *stop = nullptr;
+  if (stage != g_prof_stage || g_prof_events.size() % 2 != 0 || g_prof_events.size() >= 2 * kMaxProfiled) return false;
+  hipEvent_t a, b;
+  if (!take_event(&a)) return false;
+  if (!take_event(&b)) {
+    g_prof_pool.push_back(a);
+    return false;
+  }
+  g_prof_events.push_back(a);
+  g_prof_events.push_back(b);
+  *start = a;
+  *stop = b;
+  return true;
 }
 
 int fail(int status, const std::string& msg) {
@@ -223,6 +255,13 @@ int rkv_profile_enable(int32_t stage) {
   if (stage < -1 || stage > rkv::kStageDecode) return rkv::fail(RKV_ERR_INVALID_ARG, "unknown stage");
   std::lock_guard<std::mutex> lk(rkv::g_prof_mu);
   rkv::g_prof_stage = stage;
+  // create the events up front: creating them during the profiled launches would slow the host
+  // enough to leave the GPU idle between launches
+  while (stage >= 0 && rkv::g_prof_pool.size() + rkv::g_prof_events.size() < rkv::kProfPoolFill) {
+    hipEvent_t e;
+    if (hipEventCreateWithFlags(&e, rkv::kProfEventFlags) != hipSuccess) break;
+    rkv::g_prof_pool.push_back(e);
+  }
   return RKV_OK;
 }
 
@@ -245,7 +284,7 @@ int rkv_profile_read(int32_t* n_launches, double* total_ms) {
     tot += ms;
     ++n;
   }
-  for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  for (hipEvent_t e : ev) rkv::g_prof_pool.push_back(e);   // reused by later profiled launches
   ev.clear();
   *n_launches = n;
   *total_ms = tot;

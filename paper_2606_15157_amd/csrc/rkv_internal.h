@@ -147,6 +147,10 @@ int launch_copies(const CopyLaunch& C, void* stream);
 // Stage timing with HIP events (enabled through rkv_profile_enable).
 enum Stage { kStageZero = 0, kStageScore = 1, kStageSelect = 2, kStageGather = 3, kStageDecode = 4 };
 void profile_mark(int stage, bool end, void* stream);
+// For a stage that is one kernel launch: when the stage is being profiled, two new events the
+// launch records its start and stop in (hipExtLaunchKernelGGL: the dispatch's own timestamps,
+// without the gaps that events recorded around it add); false otherwise.
+bool profile_kernel_events(int stage, void** start, void** stop);
 
 }  // namespace rkv
 

@@ -3,11 +3,11 @@
     rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o run -- python3 bench.py \
         --steps 50 --warmup 5 --no-cpu-baseline
     python -m paper_2606_15157_amd.prof_summary <dir> <out.md> "<title>" "<command>" \
-        [<kernel> <n>]
+        [<kernel> <skip> <n>]
 
-With <kernel> and <n>, the first n dispatches of that kernel (by start time; in the default
-benchmark run these are the warm-up and timed passes of the headline route, before any other
-measurement launches it) are also averaged on their own from the kernel trace.
+With <kernel>, <skip> and <n>, dispatches skip .. skip + n - 1 of that kernel (by start time;
+in the default benchmark run, after the 100 settle and 5 warm-up passes, these are the 50 timed
+passes of the headline route) are also averaged on their own from the kernel trace.
 """
 from __future__ import annotations
 
@@ -41,14 +41,14 @@ def short_name(name: str) -> str:
     return name[:cut]
 
 
-def first_dispatches(run_dir: str, kernel: str, n: int):
+def dispatches(run_dir: str, kernel: str, skip: int, n: int):
     """Durations (ns) of the first n dispatches of the kernel whose short name is `kernel`."""
     path = glob.glob(os.path.join(run_dir, "**", "*kernel_trace.csv"), recursive=True)
     if not path:
         raise FileNotFoundError(f"no kernel_trace.csv under {run_dir}")
     rows = [r for r in csv.DictReader(open(path[0])) if short_name(r["Kernel_Name"]) == kernel]
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
-    return [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows[:n]]
+    return [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in rows[skip:skip + n]]
 
 
 MAX_ROWS = 25   # the table lists the kernels with the largest total time
@@ -67,11 +67,11 @@ def main(argv):
         if len(rows) > MAX_ROWS:
             rest = sum(float(r["Percentage"]) for r in rows[MAX_ROWS:])
             f.write(f"| ({len(rows) - MAX_ROWS} more kernels) | | | | | {rest:.1f}% |\n")
-        if len(argv) > 6:
-            kernel, n = argv[5], int(argv[6])
-            d = first_dispatches(run_dir, kernel, n)
-            f.write(f"\nFirst {len(d)} dispatches of {kernel} (the headline route's warm-up and timed "
-                    f"passes): average {sum(d) / len(d) / 1e3:.1f} us, min {min(d) / 1e3:.1f} us, "
+        if len(argv) > 7:
+            kernel, skip, n = argv[5], int(argv[6]), int(argv[7])
+            d = dispatches(run_dir, kernel, skip, n)
+            f.write(f"\nDispatches {skip}-{skip + len(d) - 1} of {kernel} (the headline route's timed passes): "
+                    f"average {sum(d) / len(d) / 1e3:.1f} us, min {min(d) / 1e3:.1f} us, "
                     f"max {max(d) / 1e3:.1f} us.\n")
     print(open(out_md).read())
 
