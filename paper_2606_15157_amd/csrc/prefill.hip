@@ -1057,16 +1057,18 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
   }
 }
 
-// Selection with every candidate score held in registers (kSelRegs per thread, 1024 threads):
+// Selection with every candidate score held in registers (kSelRegs = 16 or 32 per thread, 1024
+// threads: prompts of up to 16K or 32K keys):
 // wave wv owns the contiguous key range [w0, w1); its lane l holds keys w0 + 64 i + l.  Dynamic
 // LDS holds the job's slice-edge column sums and the repaired scores next to slice borders
 // (with their per-head pool maxima).
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 static_assert(kSelWaves <= 16, "wave prefixes are summed over one 16-lane DPP row");
-constexpr int kSelRegs = 16;
-constexpr int kSelRegsMaxKeys = kSelRegs * kSelThreads;
+constexpr int kSelRegsMax = 32;                              // scores per thread, at most
+constexpr int kSelRegsMaxKeys = kSelRegsMax * kSelThreads;   // 32K keys
 
+template <int kSelRegs>
 __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillLaunch P) {
   // dynamic LDS: [n_edge] edges, [n_fix] repaired scores, [n_fix G] per-head pool maxima
   extern __shared__ __attribute__((aligned(16))) float sDyn[];
@@ -1425,7 +1427,10 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
       if (e == hipSuccess)
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_regs_kernel),
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_regs_kernel<16>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
+      if (e == hipSuccess)
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_regs_kernel<32>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
       if (e != hipSuccess) return (int)e;
       lds_set = true;
@@ -1434,9 +1439,13 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
     const size_t dyn = sizeof(float) * ((size_t)P.n_slices * P.group * 4 * P.pool_half +
                                         (size_t)(P.n_slices > 0 ? P.n_slices - 1 : 0) * 2 * P.pool_half *
                                             (1 + P.group));
-    if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - 2 * kHistBins * 4 - 256)
-      launch_staged(kStageSelect, select_regs_kernel, dim3(n_sel), dim3(kSelThreads), std::max(dyn, (size_t)kRepairLds),
-                    st, P);
+    if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - 2 * kHistBins * 4 - 256) {
+      const size_t lds = std::max(dyn, (size_t)kRepairLds);
+      if (P.seq_len <= 16 * kSelThreads)
+        launch_staged(kStageSelect, select_regs_kernel<16>, dim3(n_sel), dim3(kSelThreads), lds, st, P);
+      else
+        launch_staged(kStageSelect, select_regs_kernel<32>, dim3(n_sel), dim3(kSelThreads), lds, st, P);
+    }
     else
       launch_staged(kStageSelect, select_kernel, dim3(n_sel), dim3(kThreads), kSelectLds, st, P);
   }
