@@ -86,6 +86,19 @@ def test_degenerate_budgets(budget):
     run_case(rules, [budget] * 4, [[gen(8, 0, l, L)] for l in range(4)], window=32, label=f"b{budget}")
 
 
+@pytest.mark.parametrize("L,w", [(32, 32), (100, 1), (129, 64)], ids=["window_is_prompt", "w1", "w64_L129"])
+def test_window_edge_shapes(L, w, monkeypatch):
+    """A window covering the whole prompt (SnapKV has no candidates: the window is kept), a
+    one-row window (padded row tiles) and a 64-row window over one slice and a one-key tail
+    (eight row tiles), through the default path and the window kernels."""
+    b = min(L, 20)
+    rules = [OP.SNAPKV, OP.H2O, OP.STREAMING]
+    layers = [[gen(9, 0, l, L, w=w)] for l in range(3)]
+    run_case(rules, [b] * 3, layers, window=w, label=f"edge_L{L}_w{w}")
+    monkeypatch.setenv("RKV_FORCE_WINDOW", "1")
+    run_case(rules, [b] * 3, layers, window=w, label=f"edge_L{L}_w{w}_window")
+
+
 def test_window_totals_sum_to_w():
     """H2O keeping every position reports the unpooled group-mean score on all of [0, L):
     every window row's softmax sums to 1, so each KV head's scores sum to w."""
