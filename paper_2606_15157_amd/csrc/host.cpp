@@ -220,9 +220,14 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
   size_t off = 0;
   w.counters = off;
   off = round_up(off + sizeof(uint32_t) * kCounterStride * (1 + (size_t)n_jobs), 256);
-  w.stats = off;   // only the pipelined kernel (four row tiles, at most kPipeMaxSlices slices) uses it
+  // per-slice row sums of the pipelined kernel (four row tiles, at most kPipeMaxSlices slices), or
+  // the window rows kernel's partial row sums; the first is never smaller where both could run
+  w.stats = off;
   const bool pipe_layout = rows == kPipeRows && n_slices <= kPipeMaxSlices;
-  off = round_up(off + sizeof(float) * (pipe_layout ? (size_t)n_jobs * n_slices * kPipeRows : 0), 256);
+  const int parts = window_parts(n_jobs - n_full_jobs - n_tova_jobs, n_slices, rows);
+  const size_t stat_floats = pipe_layout ? (size_t)n_jobs * n_slices * kPipeRows
+                                         : (parts > 1 ? (size_t)n_jobs * parts * rows : 0);
+  off = round_up(off + sizeof(float) * stat_floats, 256);
   w.lam = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
   w.ncl = off;
@@ -643,6 +648,7 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     const int n_tova_jobs = shape->batch * n_class[2] * shape->n_kv_heads;
     rkv::PrefillWorkspace W = rkv::prefill_workspace_layout(n_jobs, P.n_slices, ktiles * 32, L, G, P.pool_half,
                                                             n_full_jobs, n_tova_jobs);
+    P.window_parts = rkv::window_parts(n_jobs - n_full_jobs - n_tova_jobs, P.n_slices, ktiles * 32);
     char* base = (char*)ws;
     P.counters = (uint32_t*)(base + W.counters);
     P.stats = (float*)(base + W.stats);

@@ -60,11 +60,14 @@ struct PrefillLaunch {
   int32_t want_unpooled;  // write the unpooled group-mean score (acc seeding of SnapKV layers)
   float scale_log2;       // log2(e) / sqrt(d)
   int32_t force_window;   // test hook: the window kernels even where the pipelined one applies
+  int32_t window_parts;   // window rows kernel: workgroups (key ranges) per job
   // workspace regions
   uint32_t* counters;     // [0] status; job j's slice-arrival counter at [kCounterStride * (1 + j)]
-  float* stats;           // [J][n_slices][128]  pipelined kernel: per-slice row sums (NaN until stored)
+  float* stats;           // [J][n_slices][128]  pipelined kernel: per-slice row sums (NaN until stored);
+                          // [J][window_parts][R]  window kernels with several parts: partial row sums
   float* lam;             // [J][R]  window kernels: per-row log2 softmax normaliser (+inf for padding rows)
-  float* ncl;             // [J][128]  pipelined kernel: minus the per-row reference logit (0 for padding rows)
+  float* ncl;             // [J][128]  pipelined kernel: minus the per-row reference logit (0 for padding rows);
+                          // [J][R]  window kernels with several parts: the reference in log2 units (+inf: padding)
   float* lamf;            // [J_full][G][L]  full-span H2O: log2 normaliser of every query row
   float* tz;              // [J_tova][G][L]  TOVA: log2-scaled logits of the last query per head
   float* tstat;           // [J_tova][n_slices][G][2]  TOVA: per-slice (max, sum of exp2(x - max))
@@ -86,6 +89,19 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
                                           int n_full_jobs, int n_tova_jobs);
 constexpr int kPipeRows = 128;      // window rows of a job in the pipelined scoring kernel
 constexpr int kPipeMaxSlices = 64;  // slices per job it takes (a lane reads four of 16 slices' row sums)
+
+// Key ranges per job of the window rows kernel: with few jobs, enough workgroups to fill the
+// chip (two resident per CU at four row tiles, one at eight); at most 8 parts of at least 8
+// slices each.  The host's workspace layout and launch both take it from here.
+inline int window_parts(int n_window_jobs, int n_slices, int rows) {
+  if (n_window_jobs <= 0) return 1;
+  const int want = rows <= 4 * 32 ? 512 : 256;
+  int p = (want + n_window_jobs - 1) / n_window_jobs;
+  p = p < 8 ? p : 8;
+  const int by_len = n_slices / 8 > 1 ? n_slices / 8 : 1;
+  p = p < by_len ? p : by_len;
+  return p > 1 ? p : 1;
+}
 
 // Error reporting (thread-local last error).
 int fail(int status, const std::string& msg);

@@ -4,8 +4,9 @@
 //   A[g][j] = sum_i softmax_j(Q[g,i] . K[j] / sqrt(d)), S = mean_g maxpool(A[g]) or mean_g A[g],
 // computed in two passes over the keys instead of one pass with a cross-workgroup exchange:
 //
-// window_rows_kernel<NRT>: one workgroup per job, one wave per 32 window rows (R = 32 NRT rows,
-//   the query rows of every head of the group, padded).  The wave's query fragments stay in
+// window_rows_kernel<NRT>: one workgroup per job (per part of its keys when there are few jobs:
+//   the columns kernel then adds the parts' row sums), one wave per 32 window rows (R = 32 NRT
+//   rows, the query rows of every head of the group, padded).  The wave's query fragments stay in
 //   registers; 128-key tiles stream through two LDS buffers (prefetched into registers one tile
 //   ahead) and bf16 MFMA logits are taken against a fixed per-row reference c_r = max(logit with
 //   the row's own key, logit with key 0), both true logits of the row; each lane sums e =
@@ -73,13 +74,17 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int L = P.seq_len, w = P.window, G = P.group, Hq = P.n_q_heads, Hkv = P.n_kv_heads, B = P.batch;
   const int tpr = P.row_tiles_per_group * 32;
-  const int job = blockIdx.x;
+  const int parts = P.window_parts, job = blockIdx.x / parts, part = blockIdx.x - job * parts;
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
   const PrefillLayer& ly = P.layer[slot];
   const uint16_t* khead = ly.k + (size_t)(s * Hkv + h) * L * kHeadDim;
   const uint16_t* qjob = ly.q + (size_t)(s * Hq + h * G) * w * kHeadDim;   // [G][w][d]
+  // this workgroup's key tiles [t0, t1) (part `part` of the job's tiles)
+  const int n_tiles = (L + kSlice - 1) / kSlice;
+  const int per_part = (n_tiles + parts - 1) / parts;
+  const int t0 = min(n_tiles, part * per_part), t1 = min(n_tiles, t0 + per_part);
 
-  // ---- per-row reference: thread r < R takes row r (its own key and key 0, 128-d dot products)
+  // ---- per-row reference (every part computes the same): thread r < R takes row r (its own key and key 0, 128-d dot products)
   if (tid < R) {
     const WinRow x = win_row(tid, tpr, G, w);
     float zd = 0.f, zs = 0.f;
@@ -114,7 +119,6 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
       qa[rs][st] = as_bf16x8w(v);
     }
   }
-  const int n_tiles = (L + kSlice - 1) / kSlice;
   u32x4 pre[PER];
   auto fetch = [&](int kt) {
 #pragma unroll
@@ -131,7 +135,7 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
       *reinterpret_cast<u32x4*>(&sK[buf][swzw(key, ch)]) = pre[u];
     }
   };
-  fetch(0);
+  if (t0 < t1) fetch(t0);
   __syncthreads();   // sC complete
   const float sl2 = P.scale_log2;
   float ncs[2][4], Z[2][4];
@@ -193,27 +197,30 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
   };
   f32x4 accA[2][4], accB[2][4];
   // bulk tiles: every key visible to every window row (keys below L - w + 1, the first row's
-  // position, all inside the prompt)
-  const int n_bulk = min(n_tiles, (L - w + 1) / kSlice);
-  put(0);
-  if (n_tiles > 1) fetch(1);
+  // position, all inside the prompt); buffer parity counts from t0
+  const int b_end = min(t1, (L - w + 1) / kSlice);
+  if (t0 < t1) {
+    put(0);
+    if (t0 + 1 < t1) fetch(t0 + 1);
+  }
   __syncthreads();
-  if (n_bulk > 0) mfma_half(0, 0, accA);
-  for (int kt = 0; kt < n_bulk; ++kt) {
-    interleaved(kt & 1, 4, accB, accA);
-    if (kt + 1 < n_tiles) {
-      put((kt + 1) & 1);
-      if (kt + 2 < n_tiles) fetch(kt + 2);
+  if (t0 < b_end) mfma_half(0, 0, accA);
+  for (int kt = t0; kt < b_end; ++kt) {
+    const int b = (kt - t0) & 1;
+    interleaved(b, 4, accB, accA);
+    if (kt + 1 < t1) {
+      put(b ^ 1);
+      if (kt + 2 < t1) fetch(kt + 2);
     }
     __syncthreads();
-    if (kt + 1 < n_bulk) interleaved((kt + 1) & 1, 0, accA, accB);
+    if (kt + 1 < b_end) interleaved(b ^ 1, 0, accA, accB);
     else valu_half(accB);
   }
   // edge tiles: keys past a row's position, and past the prompt, take no part
-  for (int kt = n_bulk; kt < n_tiles; ++kt) {
-    const int k0 = kt * kSlice;
-    mfma_half(kt & 1, 0, accA);
-    mfma_half(kt & 1, 4, accB);
+  for (int kt = max(t0, b_end); kt < t1; ++kt) {
+    const int k0 = kt * kSlice, b = (kt - t0) & 1;
+    mfma_half(b, 0, accA);
+    mfma_half(b, 4, accB);
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
@@ -227,13 +234,14 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
             if (key > last[rs][i]) x = kMaskedW;
             Z[rs][i] += __builtin_amdgcn_exp2f(x);
           }
-    if (kt + 1 < n_tiles) {
-      put((kt + 1) & 1);
-      if (kt + 2 < n_tiles) fetch(kt + 2);
+    if (kt + 1 < t1) {
+      put(b ^ 1);
+      if (kt + 2 < t1) fetch(kt + 2);
     }
     __syncthreads();
   }
-  // ---- sums over the 16 lanes of each row group; the row's log2 normaliser
+  // ---- sums over the 16 lanes of each row group; the row's log2 normaliser (one part), or the
+  // part's row sum and, from part 0, the reference (several parts: the columns kernel adds them)
 #pragma unroll
   for (int rs = 0; rs < 2; ++rs)
 #pragma unroll
@@ -245,17 +253,20 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
       z = dpp_addw<0x121>(z);
       const int r = 32 * wv + 16 * rs + 4 * lg + i;
       if (l16 == 0) {
-        float lm = __builtin_inff();   // padding rows: every probability 0
-        if (last[rs][i] >= 0) {
-          if (z < __builtin_inff()) {
-            lm = sC[r] * sl2 + __builtin_log2f(z);
-          } else {
-            // a key far above the row's reference: the job is rescored exactly before selection
-            atomicOr(P.counters, RKV_STATUS_REPAIRED);
-            atomicOr(P.counters + (size_t)kCounterStride * (1 + job) + 1, 1u);
-          }
+        const bool valid = last[rs][i] >= 0;
+        if (valid && !(z < __builtin_inff())) {
+          // a key far above the row's reference: the job is rescored exactly before selection
+          atomicOr(P.counters, RKV_STATUS_REPAIRED);
+          atomicOr(P.counters + (size_t)kCounterStride * (1 + job) + 1, 1u);
         }
-        P.lam[(size_t)job * R + r] = lm;
+        if (parts == 1) {
+          // padding and overflowing rows: +inf, every probability 0
+          P.lam[(size_t)job * R + r] = valid && z < __builtin_inff() ? sC[r] * sl2 + __builtin_log2f(z)
+                                                                      : __builtin_inff();
+        } else {
+          P.stats[((size_t)job * parts + part) * R + r] = z;
+          if (part == 0) P.ncl[(size_t)job * R + r] = valid ? sC[r] * sl2 : __builtin_inff();
+        }
       }
     }
 }
@@ -291,7 +302,18 @@ __global__ __launch_bounds__(256, 2) void window_cols_kernel(const PrefillLaunch
     if (x.valid) v = *reinterpret_cast<const u32x4*>(qjob + (size_t)(x.g * w + x.ii) * kHeadDim + 8 * ch);
     *reinterpret_cast<u32x4*>(&sQ[swzw(row, ch)]) = v;
   }
-  for (int r = tid; r < R; r += NT) sLam[r] = P.lam[(size_t)job * R + r];
+  if (P.window_parts == 1) {
+    for (int r = tid; r < R; r += NT) sLam[r] = P.lam[(size_t)job * R + r];
+  } else {
+    // the parts' row sums, added in part order; +inf for padding and overflowing rows
+    const int parts = P.window_parts;
+    for (int r = tid; r < R; r += NT) {
+      const float c = P.ncl[(size_t)job * R + r];
+      float z = 0.f;
+      for (int q = 0; q < parts; ++q) z += P.stats[((size_t)job * parts + q) * R + r];
+      sLam[r] = c < __builtin_inff() && z < __builtin_inff() ? c + __builtin_log2f(z) : __builtin_inff();
+    }
+  }
   // ---- this wave's 32 keys of block b as B-operand fragments (key 32 wv + 16 ks + l16)
   auto load_k = [&](int b, bf16x8 (&kf)[2][4]) {
 #pragma unroll
@@ -495,7 +517,7 @@ __global__ __launch_bounds__(256, 2) void window_cols_kernel(const PrefillLaunch
 
 template <int NRT>
 int launch_window_nrt(const PrefillLaunch& P, int n_jobs, hipStream_t st) {
-  window_rows_kernel<NRT><<<n_jobs, NRT * 64, 0, st>>>(P);
+  window_rows_kernel<NRT><<<n_jobs * P.window_parts, NRT * 64, 0, st>>>(P);
   const int nbg = (P.n_slices + kColBlocks - 1) / kColBlocks;
   window_cols_kernel<NRT><<<(unsigned)((int64_t)n_jobs * nbg), 256, 0, st>>>(P);
   return (int)hipGetLastError();

@@ -204,6 +204,16 @@ def test_window_kernels_match_oracle_on_short_prompts(monkeypatch):
              label="win_777")
 
 
+@pytest.mark.parametrize("L", [4096, 3000])
+def test_window_kernels_split_keys(monkeypatch, L):
+    """Few jobs (two layers x 8 KV heads): the rows kernel splits each job's keys over several
+    workgroups (4 parts at L = 4096; 3 at L = 3000, the last with the ragged tail) and the columns
+    kernel adds their row sums."""
+    monkeypatch.setenv("RKV_FORCE_WINDOW", "1")
+    run_case([OP.SNAPKV, OP.H2O], [300, 300], [[gen(15, 0, 0, L)], [gen(15, 0, 1, L)]], window=32,
+             label=f"win_split_{L}")
+
+
 def overflow_input(L=1024, w=32):
     """One window row (query head 5, row 7) set to 4 in every dimension and one prefix key
     (position 300) to 4 in every dimension: that row's logit there is 4 * 4 * 128 / sqrt(128) =
