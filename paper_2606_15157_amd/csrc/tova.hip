@@ -12,9 +12,10 @@
 //   units, go to the workspace through LDS (coalesced rows), and the slice leaves its per-head
 //   (max, sum of exp2(x - max)).  This is a matrix-vector product of G rows: HBM-bound on the
 //   key stream, so it stays on the vector ALUs.
-// tova_scores_kernel<G>: one workgroup per job.  Each head's slice pairs fold into (M_g, Z_g)
-//   by an online combination (exact: no fixed reference, nothing can overflow); then
-//   S[j] = (1/G) sum_g exp2(x_gj - M_g) / Z_g.
+// tova_scores_kernel<G>: one workgroup per job and kTovaScoreKeys keys.  Each head's slice
+//   pairs fold into (M_g, Z_g) by an online combination (exact: no fixed reference, nothing can
+//   overflow; every workgroup of a job folds them in the same order); then
+//   S[j] = (1/G) sum_g exp2(x_gj - M_g) / Z_g over the workgroup's keys.
 // Sums run in a fixed order, so results are reproducible.
 #include <hip/hip_runtime.h>
 
@@ -30,6 +31,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kTovaThreads = 256;
 constexpr int kKeysPerPass = kTovaThreads / 16;      // 16 key rows per pass of the workgroup
 constexpr int kPasses = kSlice / kKeysPerPass;       // 8 passes cover a 128-key slice
+constexpr int kTovaScoreKeys = 2048;                 // keys per score workgroup (8 per thread)
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_rot(float x) {
@@ -145,7 +147,8 @@ __global__ __launch_bounds__(kTovaThreads) void tova_scores_kernel(const Prefill
   __shared__ float sM[G], sRz[G];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int L = P.seq_len, nsl = P.n_slices;
-  const int jt = blockIdx.x;
+  const int n_parts = (L + kTovaScoreKeys - 1) / kTovaScoreKeys;
+  const int jt = blockIdx.x / n_parts, part = blockIdx.x - jt * n_parts;
   const int job = tova_job0(P) + jt;
   // fold each head's slice pairs: lanes stride over slices, then a butterfly over the wave
   for (int g = wv; g < G; g += kTovaThreads / 64) {
@@ -179,7 +182,8 @@ __global__ __launch_bounds__(kTovaThreads) void tova_scores_kernel(const Prefill
   const float* tz = P.tz + (size_t)jt * G * L;
   float* S = P.S + (size_t)job * L;
   const float inv_g = 1.f / (float)G;
-  for (int j = tid; j < L; j += kTovaThreads) {
+  const int j1 = min(L, (part + 1) * kTovaScoreKeys);
+  for (int j = part * kTovaScoreKeys + tid; j < j1; j += kTovaThreads) {
     float a = 0.f;
 #pragma unroll
     for (int g = 0; g < G; ++g) a += __builtin_amdgcn_exp2f(tz[(size_t)g * L + j] - sM[g]) * sRz[g];
@@ -190,7 +194,8 @@ __global__ __launch_bounds__(kTovaThreads) void tova_scores_kernel(const Prefill
 template <int G>
 void launch_g(const PrefillLaunch& P, int n_jobs, hipStream_t st) {
   tova_logits_kernel<G><<<n_jobs * P.n_slices, kTovaThreads, 0, st>>>(P);
-  tova_scores_kernel<G><<<n_jobs, kTovaThreads, 0, st>>>(P);
+  const int n_parts = (P.seq_len + kTovaScoreKeys - 1) / kTovaScoreKeys;
+  tova_scores_kernel<G><<<n_jobs * n_parts, kTovaThreads, 0, st>>>(P);
 }
 
 }  // namespace
