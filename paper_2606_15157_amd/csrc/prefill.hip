@@ -223,9 +223,10 @@ __device__ __forceinline__ void lds_barrier() {
 // next item's MFMAs at once:
 //   A     logits (k-step fragments read one step ahead), exponentials, per-row partial sums per
 //         key tile into sStat
-//   MID   every wave: all its earlier memory operations have completed; the row sums of item
-//         t - 2's job (loaded at MID of iteration t - 1; re-read while any is still NaN)
-//         -> reciprocal normalisers in sAlpha; then the loads of item t - 1's row sums
+//   MID   every wave: all its earlier memory operations have completed; waves 0-3: the row
+//         sums of item t - 2's job (loaded at MID of iteration t - 1; re-read while any is still
+//         NaN) -> reciprocal normalisers in sAlpha, then the loads of item t - 1's row sums
+//         (waves 4-7 issue the DMA, the longer task at the end of the iteration)
 //   B1.5
 //   wave 0: store item t's row sums
 //   B     item t - 2: probabilities, sums over the window rows per query head (or group) into
@@ -601,38 +602,43 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
   };
 
   // ---- normalisers of item j: every workgroup that scores a slice of the job sums the job's
-  // per-slice row sums itself.  Wave wv takes rows 16 wv + [0, 16); lane l reads rows
-  // 16 wv + 4 (l / 16) + [0, 4) of slices (l % 16) + 16 u, u = 0..3 (a job has at most 64 slices
-  // here), as 16-byte loads that bypass the non-coherent cache; the buffer's record count makes
-  // reads past the job's last slice return 0.  The loads are issued one iteration ahead
+  // per-slice row sums itself, in waves 0-3.  Wave wv takes rows 32 wv + [0, 32); lane l reads
+  // rows 32 wv + 16 hh + 4 (l / 16) + [0, 4) (hh = 0, 1) of slices (l % 16) + 16 u, u = 0..3 (a
+  // job has at most 64 slices here), as 16-byte loads that bypass the non-coherent cache; the
+  // buffer's record count makes reads past the job's last slice return 0.  The loads are issued one iteration ahead
   // (load_stats) and checked at the middle of the next (take_stats): a batch with sums not stored
   // yet (NaN) is read again as a whole.  The order of the additions is fixed, so results are
   // reproducible.
-  f32x4v sx[4];
+  f32x4v sx[8];
   auto load_stats = [&](int job) {
     // lane offset from an opaque copy of the thread index: no address is kept across the loop
     int tv = threadIdx.x;
     asm volatile("" : "+v"(tv));
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(P.stats + (size_t)job * nsl * R), (short)0, nsl * R * 4, 0x00020000);
-    const int off = ((tv & 15) * R + 16 * (tv >> 6) + 4 * ((tv & 63) >> 4)) * 4;
+    const int off = ((tv & 15) * R + 32 * (tv >> 6) + 4 * ((tv & 63) >> 4)) * 4;
 #pragma unroll
     for (int u = 0; u < 4; ++u)   // cache policy 16: sc1 (coherent at device scope)
-      sx[u] = __builtin_bit_cast(f32x4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 16 * R * 4, 0, 16));
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh)
+        sx[2 * u + hh] = __builtin_bit_cast(f32x4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 16 * R * 4 + hh * 64, 0, 16));
   };
   auto take_stats = [&](const PipeRef& j) {
     // lane sums over its four slices, then a reduce-scatter over the 16 lanes of the row group:
-    // lane l ends with the row 4 (l / 16) + bit3(l) + 2 bit2(l) sum.  A slice not stored yet
-    // (NaN) makes its row's sum NaN; the batch is then read again as a whole.
+    // lanes l and l ^ 1 end with the sum of row 4 (l / 16) + bit3(l) + 2 bit2(l) + 16 bit1(l) of
+    // the wave's 32.  A slice not stored yet (NaN) makes its row's sum NaN; the batch is then read
+    // again as a whole.
     uint32_t it = 0;
-    float v[4];
+    float v[8];
     while (true) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = (sx[0][i] + sx[1][i]) + (sx[2][i] + sx[3][i]);
-      dpp_halve<0x128, 4, 4>(v, (lane >> 3) & 1);   // row_ror:8       -> lane l ^ 8
-      dpp_halve<0x141, 2, 4>(v, (lane >> 2) & 1);   // row_half_mirror -> 7 - l within 8
-      dpp_halve<0x4E, 1, 4>(v, 0);                  // quad_perm [2,3,0,1]
-      dpp_halve<0xB1, 1, 4>(v, 0);                  // quad_perm [1,0,3,2]
+      for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[4 * hh + i] = (sx[hh][i] + sx[2 + hh][i]) + (sx[4 + hh][i] + sx[6 + hh][i]);
+      dpp_halve<0x128, 8, 8>(v, (lane >> 3) & 1);   // row_ror:8           -> lane l ^ 8
+      dpp_halve<0x141, 4, 8>(v, (lane >> 2) & 1);   // row_half_mirror     -> 7 - l within 8
+      dpp_halve<0x4E, 2, 8>(v, (lane >> 1) & 1);    // quad_perm [2,3,0,1] -> l ^ 2
+      dpp_halve<0xB1, 1, 8>(v, 0);                  // quad_perm [1,0,3,2] -> l ^ 1
       if (__builtin_amdgcn_ballot_w64(v[0] != v[0]) == 0 || gave_up) break;
       if (++it > kSpinLimit) {
         if (lane == 0) atomicOr(status, 1u);
@@ -644,15 +650,15 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       wait_vmcnt<0>();
     }
     const float z = v[0];
-    if (z == __builtin_inff() && (l16 & 3) == 0) {
+    if (z == __builtin_inff() && (l16 & 1) == 0) {
       // a key far above the row's reference: the job is rescored exactly before selection
       atomicOr(status, RKV_STATUS_REPAIRED);
       atomicOr(P.counters + (size_t)kCounterStride * (1 + j.job) + 1, 1u);
     }
     // z >= 1 for every valid row (the reference key contributes 1); padding rows have z = 0, and
     // a row left NaN after a time-out gets 0
-    if ((l16 & 3) == 0)
-      sAlpha[16 * wv + 4 * lg + ((l16 >> 3) & 1) + 2 * ((l16 >> 2) & 1)] =
+    if ((l16 & 1) == 0)
+      sAlpha[32 * wv + 4 * lg + 2 * ((l16 >> 2) & 1) + ((l16 >> 3) & 1) + 16 * ((l16 >> 1) & 1)] =
           z > 0.f && z < __builtin_inff() ? __builtin_amdgcn_rcpf(z) : 0.f;
   };
 
@@ -684,13 +690,15 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     // results unused), so each register set is redefined unconditionally
     phase_a(ja, t & 1, ea);
     // MID: everything this wave issued in earlier iterations has completed (the row sums of item
-    // t - 2's job and the DMA of item t + 1); the row sums become item t - 2's normalisers.  The
-    // row sums of item t - 1's job (stored by its workgroups after their phase A, consumed at
-    // the next MID) are loaded at once, in every iteration so that the registers have one
-    // definition (the job is clamped where the item lies outside the pipeline)
+    // t - 2's job and the DMA of item t + 1); in waves 0-3 the row sums become item t - 2's
+    // normalisers, and the row sums of item t - 1's job (stored by its workgroups after their
+    // phase A, consumed at the next MID) are loaded at once, in every iteration so that the
+    // registers have one definition (the job is clamped where the item lies outside the pipeline)
     wait_vmcnt<0>();
-    if (doB) take_stats(j2);
-    load_stats(min(j1.job, n_jobs - 1));
+    if (wv < 4) {
+      if (doB) take_stats(j2);
+      load_stats(min(j1.job, n_jobs - 1));
+    }
     lds_barrier();   // B1.5: every wave's phase A is done (sStat complete, buffer t % 2 free)
     // wave 0: item t's row sums (the consumers check for sums not stored yet)
     if (wv == 0 && doA) {
