@@ -228,6 +228,9 @@ PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, in
   const size_t stat_floats = pipe_layout ? (size_t)n_jobs * n_slices * kPipeRows
                                          : (parts > 1 ? (size_t)n_jobs * parts * rows : 0);
   off = round_up(off + sizeof(float) * stat_floats, 256);
+  // the pipelined kernel's per-group sums of the row sums
+  w.part = off;
+  off = round_up(off + sizeof(float) * (pipe_layout ? (size_t)n_jobs * kPipeGroups * kPipeRows : 0), 256);
   w.lam = off;
   off = round_up(off + sizeof(float) * (size_t)n_jobs * rows, 256);
   w.ncl = off;
@@ -652,6 +655,7 @@ int rkv_prefill_evict(const rkv_plan* plan, const rkv_shape* shape, const rkv_pr
     char* base = (char*)ws;
     P.counters = (uint32_t*)(base + W.counters);
     P.stats = (float*)(base + W.stats);
+    P.part = (float*)(base + W.part);
     P.lam = (float*)(base + W.lam);
     P.ncl = (float*)(base + W.ncl);
     P.lamf = (float*)(base + W.lamf);

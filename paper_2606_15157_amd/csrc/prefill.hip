@@ -193,7 +193,7 @@ __device__ __forceinline__ void lds_barrier() {
 
 // ---------------------------------------------------------------------------------------------
 // Pipelined scoring against a per-row reference (four row tiles, one eight-wave workgroup per
-// CU, three items in flight).
+// CU, four items in flight).
 //
 // Reference.  The softmax of a window row is shift-invariant, so the exponentials may be taken
 // against any per-row constant c_i that keeps them in range.  c_i is the larger of the row's
@@ -211,33 +211,40 @@ __device__ __forceinline__ void lds_barrier() {
 // permlane swaps; sums over keys (row statistics) take four DPP steps inside each row of 16
 // lanes.
 //
-// Normalisers.  Each slice stores its 128 row sums; every workgroup that scores a slice of the
-// job loads all of the job's row sums (at most 64 slices) and sums them itself, so the only
-// cross-workgroup dependency is store -> load, with no counter and no designated folder.
+// Normalisers, in two levels.  Each slice stores its 128 row sums (level 0).  A job's slices form
+// up to kPipeGroups groups of gs consecutive slices; the workgroup that scores a group's first
+// slice sums the group's row sums into a partial (level 1), and every workgroup that scores a
+// slice of the job sums the job's partials (level 2).  Every hop is store -> load with "not
+// stored" marked NaN, no counters; the additions run in a fixed order, so results are
+// reproducible.  Per item a workgroup reads 4 KiB of partials (and a group's first workgroup
+// 4 KiB of row sums) instead of the job's 32 KiB of row sums.
 //
-// Schedule of iteration t (item t enters phase A, item t - 2 phase B, each in its own register
+// Schedule of iteration t (item t enters phase A, item t - 3 phase B, each in its own register
 // set; no wait is for an operation issued in the same iteration).  There is no barrier between
 // one iteration's score stores and the next phase A: every buffer phase A and MID touch was
 // handed on by B1.5 or B2 of the previous iteration, and the score stores read the sColP buffer
 // of their own iteration's parity, so a wave whose SIMD partner is still issuing DMA starts the
 // next item's MFMAs at once:
-//   A     logits (k-step fragments read one step ahead), exponentials, per-row partial sums per
+//   A     logits (fragments read two MFMA pairs ahead), exponentials, per-row partial sums per
 //         key tile into sStat
-//   MID   every wave: all its earlier memory operations have completed; waves 0-3: the row
-//         sums of item t - 2's job (loaded at MID of iteration t - 1; re-read while any is still
-//         NaN) -> reciprocal normalisers in sAlpha, then the loads of item t - 1's row sums
-//         (waves 4-7 issue the DMA, the longer task at the end of the iteration)
+//   MID   every wave: all its earlier memory operations have completed; waves 0-3: the partials
+//         of item t - 3's job (loaded at the end of iteration t - 1; re-read while any is still
+//         NaN) -> reciprocal normalisers in sAlpha; the loads of item t - 1's group's row sums
+//         where this workgroup sums that group
 //   B1.5
 //   wave 0: store item t's row sums
-//   B     item t - 2: probabilities, sums over the window rows per query head (or group) into
+//   B     item t - 3: probabilities, sums over the window rows per query head (or group) into
 //         sColP[t % 2]
 //   B2
-//   waves 0-3: scores of item t - 2; waves 4-7: LDS DMA of item t + 2 into the buffer item t has
-//         just left
-// Progress: the loads of iteration t - 1 are for sums that other workgroups store in iterations
-// <= t - 1, before their own waits of iteration t (a job's slices sit in at most two consecutive
-// iterations because a job has no more slices than there are workgroups), so with every
-// workgroup resident no wait is on a later one.
+//   waves 0-3: the partial of item t - 1's group (where this workgroup sums it: its row sums
+//         re-read while any is NaN), the scores of item t - 3, the loads of item t - 2's
+//         partials; waves 4-7: LDS DMA of item t + 2 into the buffer item t has just left
+// The margins: row sums stored at B1.5 of iteration u are loaded at MID of u + 1; partials
+// stored at the end of u + 1 are loaded at the end of u + 2, about an iteration later each.
+// Progress: every wait is for a store that its workgroup makes earlier in its own sequence than
+// the waiting point (a job's slices sit in at most two consecutive iterations because a job has
+// no more slices than there are workgroups), so with every workgroup resident no wait is on a
+// later one.
 // ---------------------------------------------------------------------------------------------
 constexpr int kPipeWaves = 8;
 constexpr int kPipeThreads = kPipeWaves * 64;
@@ -246,7 +253,7 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 
 // Minus the reference logit of every row of every scored job, and the per-pass resets: the
-// status word and the job's slices' row sums ("not stored": NaN).
+// status word, the job's slices' row sums and its partials ("not stored": NaN).
 // Four workgroups per job, each with a quarter of the rows and of the resets.
 template <int NTH>
 __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
@@ -264,6 +271,9 @@ __global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
     u32x4* st = reinterpret_cast<u32x4*>(P.stats + (size_t)job * P.n_slices * R);
     const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
     for (int i = tid + 256 * q; i < P.n_slices * R / 4; i += 256 * kParts) st[i] = nan4;
+    // and the job's level-1 partials
+    u32x4* pt = reinterpret_cast<u32x4*>(P.part + (size_t)job * kPipeGroups * R);
+    for (int i = tid + 256 * q; i < kPipeGroups * R / 4; i += 256 * kParts) pt[i] = nan4;
   }
   // 16 lanes per row, lane c taking 16-byte chunk c of the query, the row's own key and key 0
   // (each load instruction reads whole 256-byte rows); 16 rows per pass, 2 passes
@@ -410,29 +420,40 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       e[rs][0] = c4;
       e[rs][1] = c4;
     }
-    // software pipeline over the four k-steps: the six fragments of k-step st + 1 are read
-    // from LDS while the eight MFMAs of k-step st run (two fragment sets live)
-    bf16x8 kf[2][2], qf[2][4];
-    auto load_step = [&](int st, int b2) {
-      kf[b2][0] = frag16(k, kt * 32 + l16, 4 * st + lg);
-      kf[b2][1] = frag16(k, kt * 32 + 16 + l16, 4 * st + lg);
+    // software pipeline over the 16 (k-step, row tile) MFMA pairs: the query fragment of pair p
+    // is read two pairs ahead, the two key fragments of k-step st + 1 at the first pair of st.
+    // The fragment addresses come from an opaque copy of the thread index, so that they are
+    // recomputed per item instead of being held in registers across the loop.
+    int tv = threadIdx.x;
+    asm volatile("" : "+v"(tv));
+    const int l16v = tv & 15, lgv = (tv >> 4) & 3;
+    const char* qrow = reinterpret_cast<const char*>(q) + (rh * 64 + l16v) * 256;
+    const char* krow = reinterpret_cast<const char*>(k) + (kt * 32 + l16v) * 256;
+    // 16-byte chunk 4 st + lg of a row sits at chunk position (4 st + lg) ^ (row % 16)
+    auto xo = [&](int st) { return ((4 * st + lgv) ^ l16v) << 4; };
+    auto qfrag = [&](int pp) { return *reinterpret_cast<const bf16x8*>(qrow + (pp & 3) * 4096 + xo(pp >> 2)); };
+    auto kfrag = [&](int st, int ks) { return *reinterpret_cast<const bf16x8*>(krow + ks * 4096 + xo(st)); };
+    bf16x8 kf[2][2], qf[3];
+    kf[0][0] = kfrag(0, 0);
+    kf[0][1] = kfrag(0, 1);
+    qf[0] = qfrag(0);
+    qf[1] = qfrag(1);
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);   // DS reads: the references, k-step 0
 #pragma unroll
-      for (int rs = 0; rs < 4; ++rs) qf[b2][rs] = frag16(q, rh * 64 + rs * 16 + l16, 4 * st + lg);
-    };
-    load_step(0, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 10, 0);   // DS reads: the references and k-step 0
-#pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      if (st < 3) {
-        load_step(st + 1, (st + 1) & 1);
-        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+    for (int pp = 0; pp < 16; ++pp) {
+      const int st = pp >> 2, rs = pp & 3;
+      const bool rq = pp + 2 < 16, rk = rs == 0 && st < 3;
+      if (rq) qf[(pp + 2) % 3] = qfrag(pp + 2);
+      if (rk) {
+        kf[(st + 1) & 1][0] = kfrag(st + 1, 0);
+        kf[(st + 1) & 1][1] = kfrag(st + 1, 1);
       }
-#pragma unroll
-      for (int rs = 0; rs < 4; ++rs) {
-        e[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st & 1][rs], kf[st & 1][0], e[rs][0], 0, 0, 0);
-        e[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[st & 1][rs], kf[st & 1][1], e[rs][1], 0, 0, 0);
-      }
-      __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);   // MFMA
+      if (rq && rk) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+      else if (rk) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      else if (rq) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      e[rs][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[pp % 3], kf[st & 1][0], e[rs][0], 0, 0, 0);
+      e[rs][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[pp % 3], kf[st & 1][1], e[rs][1], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);   // MFMA
     }
     __builtin_amdgcn_sched_barrier(0);
     const int key_w0 = j.slice * kSlice + kt * 32;
@@ -601,55 +622,78 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     }
   };
 
-  // ---- normalisers of item j: every workgroup that scores a slice of the job sums the job's
-  // per-slice row sums itself, in waves 0-3.  Wave wv takes rows 32 wv + [0, 32); lane l reads
-  // rows 32 wv + 16 hh + 4 (l / 16) + [0, 4) (hh = 0, 1) of slices (l % 16) + 16 u, u = 0..3 (a
-  // job has at most 64 slices here), as 16-byte loads that bypass the non-coherent cache; the
-  // buffer's record count makes reads past the job's last slice return 0.  The loads are issued one iteration ahead
-  // (load_stats) and checked at the middle of the next (take_stats): a batch with sums not stored
-  // yet (NaN) is read again as a whole.  The order of the additions is fixed, so results are
-  // reproducible.
-  f32x4v sx[8];
-  auto load_stats = [&](int job) {
+  // ---- normalisers, two levels (waves 0-3).  Level 1: the workgroup scoring slice g gs of a job
+  // sums the row sums of slices [g gs, g gs + gs) into partial g; level 2: every workgroup sums
+  // the job's ng partials.  Both read one value per (row, slice or group) with the same mapping:
+  // wave wv takes rows 32 wv + [0, 32), lane l reads rows 32 wv + 16 hh + 4 (l / 16) + [0, 4)
+  // (hh = 0, 1) of slice or group l % 16, as 16-byte loads that bypass the non-coherent cache;
+  // the buffer's record count makes reads past the last slice or group return 0.  A batch with a
+  // value not stored yet (NaN) is read again as a whole.
+  const int gs = (nsl + kPipeGroups - 1) / kPipeGroups, ng = (nsl + gs - 1) / gs;
+  f32x4v l1x[2], l2x[2];
+  auto sum_off = [&]() {
     // lane offset from an opaque copy of the thread index: no address is kept across the loop
     int tv = threadIdx.x;
     asm volatile("" : "+v"(tv));
-    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        (void*)(P.stats + (size_t)job * nsl * R), (short)0, nsl * R * 4, 0x00020000);
-    const int off = ((tv & 15) * R + 32 * (tv >> 6) + 4 * ((tv & 63) >> 4)) * 4;
-#pragma unroll
-    for (int u = 0; u < 4; ++u)   // cache policy 16: sc1 (coherent at device scope)
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-        sx[2 * u + hh] = __builtin_bit_cast(f32x4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + u * 16 * R * 4 + hh * 64, 0, 16));
+    return ((tv & 15) * R + 32 * (tv >> 6) + 4 * ((tv & 63) >> 4)) * 4;
   };
-  auto take_stats = [&](const PipeRef& j) {
-    // lane sums over its four slices, then a reduce-scatter over the 16 lanes of the row group:
-    // lanes l and l ^ 1 end with the sum of row 4 (l / 16) + bit3(l) + 2 bit2(l) + 16 bit1(l) of
-    // the wave's 32.  A slice not stored yet (NaN) makes its row's sum NaN; the batch is then read
-    // again as a whole.
-    uint32_t it = 0;
+  auto load_l1 = [&](const PipeRef& j) {
+    const int s0 = (j.slice / gs) * gs, ns = min(gs, nsl - s0);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(P.stats + ((size_t)j.job * nsl + s0) * R), (short)0, ns * R * 4, 0x00020000);
+    const int off = sum_off();
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)   // cache policy 16: sc1 (coherent at device scope)
+      l1x[hh] = __builtin_bit_cast(f32x4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + hh * 64, 0, 16));
+  };
+  auto load_l2 = [&](int job) {
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(P.part + (size_t)job * kPipeGroups * R), (short)0, ng * R * 4, 0x00020000);
+    const int off = sum_off();
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+      l2x[hh] = __builtin_bit_cast(f32x4v, __builtin_amdgcn_raw_buffer_load_b128(rs, off + hh * 64, 0, 16));
+  };
+  // reduce-scatter of a lane's 8 values over the 16 lanes of its row group: lanes l and l ^ 1 end
+  // with the sum of row 32 wv + 4 (l / 16) + bit3(l) + 2 bit2(l) + 16 bit1(l)
+  auto reduce8 = [&](const f32x4v (&x)[2]) -> float {
     float v[8];
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[4 * hh + i] = x[hh][i];
+    dpp_halve<0x128, 8, 8>(v, (lane >> 3) & 1);   // row_ror:8           -> lane l ^ 8
+    dpp_halve<0x141, 4, 8>(v, (lane >> 2) & 1);   // row_half_mirror     -> 7 - l within 8
+    dpp_halve<0x4E, 2, 8>(v, (lane >> 1) & 1);    // quad_perm [2,3,0,1] -> l ^ 2
+    dpp_halve<0xB1, 1, 8>(v, 0);                  // quad_perm [1,0,3,2] -> l ^ 1
+    return v[0];
+  };
+  const int my_row = 32 * wv + 4 * lg + 2 * ((l16 >> 2) & 1) + ((l16 >> 3) & 1) + 16 * ((l16 >> 1) & 1);
+  // a sum over a batch, re-read (after a short sleep) while a value in it is not stored yet; a
+  // wait that times out sets status bit 0 and stops this wave's waits
+  auto settled = [&](f32x4v (&x)[2], auto&& reload) -> float {
+    uint32_t it = 0;
     while (true) {
-#pragma unroll
-      for (int hh = 0; hh < 2; ++hh)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[4 * hh + i] = (sx[hh][i] + sx[2 + hh][i]) + (sx[4 + hh][i] + sx[6 + hh][i]);
-      dpp_halve<0x128, 8, 8>(v, (lane >> 3) & 1);   // row_ror:8           -> lane l ^ 8
-      dpp_halve<0x141, 4, 8>(v, (lane >> 2) & 1);   // row_half_mirror     -> 7 - l within 8
-      dpp_halve<0x4E, 2, 8>(v, (lane >> 1) & 1);    // quad_perm [2,3,0,1] -> l ^ 2
-      dpp_halve<0xB1, 1, 8>(v, 0);                  // quad_perm [1,0,3,2] -> l ^ 1
-      if (__builtin_amdgcn_ballot_w64(v[0] != v[0]) == 0 || gave_up) break;
+      const float z = reduce8(x);
+      if (__builtin_amdgcn_ballot_w64(z != z) == 0 || gave_up) return z;
       if (++it > kSpinLimit) {
         if (lane == 0) atomicOr(status, 1u);
         gave_up = true;   // report once, then stop waiting in this workgroup
-        break;
+        return z;
       }
       __builtin_amdgcn_s_sleep(1);
-      load_stats(j.job);
+      reload();
       wait_vmcnt<0>();
     }
-    const float z = v[0];
+  };
+  auto take_l1 = [&](const PipeRef& j) {
+    const float z = settled(l1x, [&] { load_l1(j); });
+    if ((l16 & 1) == 0)
+      __hip_atomic_store(P.part + ((size_t)j.job * kPipeGroups + j.slice / gs) * R + my_row, z, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  };
+  auto take_l2 = [&](const PipeRef& j) {
+    const float z = settled(l2x, [&] { load_l2(j.job); });
     if (z == __builtin_inff() && (l16 & 1) == 0) {
       // a key far above the row's reference: the job is rescored exactly before selection
       atomicOr(status, RKV_STATUS_REPAIRED);
@@ -657,14 +701,12 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     }
     // z >= 1 for every valid row (the reference key contributes 1); padding rows have z = 0, and
     // a row left NaN after a time-out gets 0
-    if ((l16 & 1) == 0)
-      sAlpha[32 * wv + 4 * lg + 2 * ((l16 >> 2) & 1) + ((l16 >> 3) & 1) + 16 * ((l16 >> 1) & 1)] =
-          z > 0.f && z < __builtin_inff() ? __builtin_amdgcn_rcpf(z) : 0.f;
+    if ((l16 & 1) == 0) sAlpha[my_row] = z > 0.f && z < __builtin_inff() ? __builtin_amdgcn_rcpf(z) : 0.f;
   };
 
   f32x4v e0[4][2], e1[4][2], e2[4][2], e3[4][2];
   PipeRef ja = pipe_item(first, nsl, B, Hkv);   // item t
-  PipeRef j1 = ja, j2 = ja;                       // items t - 1, t - 2
+  PipeRef j1 = ja, j2 = ja, j3 = ja;              // items t - 1, t - 2, t - 3
   if (wv >= 4) {
     issue_dma(ja, 0);
     if (T > 1) {
@@ -672,10 +714,16 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       pipe_advance(jn, dj, ds, nsl, B, Hkv);
       issue_dma(jn, 1);
     }
+  } else {
+    // every register the loop reads is defined (values unused)
+    load_l1(ja);
+    load_l2(min(ja.job, n_jobs - 1));
   }
 
   auto iteration = [&](int t, f32x4v (&ea)[4][2], f32x4v (&eb)[4][2]) {
-    const bool doA = t < T, doB = t >= 2 && t - 2 < T;
+    const bool doA = t < T, doB = t >= 3 && t - 3 < T;
+    // this workgroup sums the group of item t - 1 (it scores the group's first slice)
+    const bool sums = t >= 1 && t - 1 < T && j1.slice % gs == 0;
     // No barrier here: the buffers this iteration reads were filled and handed on before B1.5 of
     // iteration t - 1 (DMA of item t), B2 of t - 1 (sStat, sAlpha free again), and the score
     // stores of iteration t - 1 read the other sColP buffer.  A wave may so start phase A while
@@ -689,49 +737,57 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     // both phases run in every iteration (on stale data at the ends of the pipeline, with their
     // results unused), so each register set is redefined unconditionally
     phase_a(ja, t & 1, ea);
-    // MID: everything this wave issued in earlier iterations has completed (the row sums of item
-    // t - 2's job and the DMA of item t + 1); in waves 0-3 the row sums become item t - 2's
-    // normalisers, and the row sums of item t - 1's job (stored by its workgroups after their
-    // phase A, consumed at the next MID) are loaded at once, in every iteration so that the
-    // registers have one definition (the job is clamped where the item lies outside the pipeline)
+    // MID: everything this wave issued in earlier iterations has completed (the partials of item
+    // t - 3's job, the DMA of item t + 1)
     wait_vmcnt<0>();
     if (wv < 4) {
-      if (doB) take_stats(j2);
-      load_stats(min(j1.job, n_jobs - 1));
+      if (doB) take_l2(j3);
+      if (sums) load_l1(j1);   // item t - 1's row sums, stored at B1.5 of iteration t - 1
     }
     lds_barrier();   // B1.5: every wave's phase A is done (sStat complete, buffer t % 2 free)
-    // wave 0: item t's row sums (the consumers check for sums not stored yet)
+    // wave 0: item t's row sums (the summing workgroup checks for sums not stored yet)
     if (wv == 0 && doA) {
       float2 o;
       o.x = sStat[0][2 * lane] + sStat[1][2 * lane] + sStat[2][2 * lane] + sStat[3][2 * lane];
       o.y = sStat[0][2 * lane + 1] + sStat[1][2 * lane + 1] + sStat[2][2 * lane + 1] + sStat[3][2 * lane + 1];
       store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + 2 * lane, o.x, o.y);
     }
-    phase_b(j2, eb);
+    phase_b(j3, eb);
     lds_barrier();   // B2: sColP complete
     if (wv < 4) {
-      if (doB) store(j2);
+      if (sums) {
+        // the group's row sums loaded at MID (wave 0's row-sum store may still be in flight)
+        if (wv == 0 && doA) wait_vmcnt<1>();
+        else wait_vmcnt<0>();
+        take_l1(j1);
+      }
+      if (doB) store(j3);
+      // the partials of item t - 2's job (stored at the end of iteration t - 1), consumed at the
+      // next MID; loaded in every iteration so that the registers have one definition (the job
+      // is clamped where the item lies outside the pipeline)
+      load_l2(min(j2.job, n_jobs - 1));
     } else if (t + 2 < T) {
       PipeRef jn = ja;
       pipe_advance(jn, dj, ds, nsl, B, Hkv);
       pipe_advance(jn, dj, ds, nsl, B, Hkv);
       issue_dma(jn, t & 1);
     }
+    j3 = j2;
     j2 = j1;
     j1 = ja;
     pipe_advance(ja, dj, ds, nsl, B, Hkv);
   };
 
-  // T + 2 iterations drain the pipeline; the count is padded to a multiple of four (the padding
+  // T + 3 iterations drain the pipeline; the count is padded to a multiple of four (the padding
   // iterations store nothing) so that the unrolled body has a single exit at its end.  Item t's
-  // exponentials live in set t % 4 from iteration t to t + 2, so three sets are live at a time.
-  const int n_iter = (T + 2 + 3) & ~3;
+  // exponentials live in set t % 4 from iteration t to t + 3.
+  const int n_iter = (T + 3 + 3) & ~3;
 #pragma unroll 1
   for (int t = 0; t < n_iter; t += 4) {
-    iteration(t, e0, e2);
-    iteration(t + 1, e1, e3);
-    iteration(t + 2, e2, e0);
-    iteration(t + 3, e3, e1);
+    iteration(t, e0, e1);
+    iteration(t + 1, e1, e2);
+    iteration(t + 2, e2, e3);
+    iteration(t + 3, e3, e0);
   }
 }
 

@@ -65,6 +65,7 @@ struct PrefillLaunch {
   uint32_t* counters;     // [0] status; job j's slice-arrival counter at [kCounterStride * (1 + j)]
   float* stats;           // [J][n_slices][128]  pipelined kernel: per-slice row sums (NaN until stored);
                           // [J][window_parts][R]  window kernels with several parts: partial row sums
+  float* part;            // [J][kPipeGroups][128]  pipelined kernel: per-group sums of those (NaN until stored)
   float* lam;             // [J][R]  window kernels: per-row log2 softmax normaliser (+inf for padding rows)
   float* ncl;             // [J][128]  pipelined kernel: minus the per-row reference logit (0 for padding rows);
                           // [J][R]  window kernels with several parts: the reference in log2 units (+inf: padding)
@@ -83,12 +84,13 @@ static_assert(sizeof(PrefillLaunch) <= 4000, "kernel argument block too large");
 
 // Workspace layout for one launch group.
 struct PrefillWorkspace {
-  size_t counters, stats, lam, ncl, lamf, tz, tstat, S, Su, edge, end, total;
+  size_t counters, stats, part, lam, ncl, lamf, tz, tstat, S, Su, edge, end, total;
 };
 PrefillWorkspace prefill_workspace_layout(int n_jobs, int n_slices, int rows, int seq_len, int group, int pool_half,
                                           int n_full_jobs, int n_tova_jobs);
 constexpr int kPipeRows = 128;      // window rows of a job in the pipelined scoring kernel
-constexpr int kPipeMaxSlices = 64;  // slices per job it takes (a lane reads four of 16 slices' row sums)
+constexpr int kPipeMaxSlices = 64;  // slices per job it takes
+constexpr int kPipeGroups = 8;      // slice groups per job of its two-level row-sum exchange
 
 // Key ranges per job of the window rows kernel: with few jobs, enough workgroups to fill the
 // chip (two resident per CU at four row tiles, one at eight); at most 8 parts of at least 8
