@@ -1121,8 +1121,8 @@ __global__ __launch_bounds__(kThreads) void select_kernel(const PrefillLaunch P)
   }
 }
 
-// Selection with every candidate score held in registers (kSelRegs = 16 or 32 per thread, 1024
-// threads: prompts of up to 16K or 32K keys):
+// Selection with every candidate score held in registers (kSelRegs = 8, 16 or 32 per thread, 1024
+// threads: prompts of up to 8K, 16K or 32K keys):
 // wave wv owns the contiguous key range [w0, w1); its lane l holds keys w0 + 64 i + l.  Dynamic
 // LDS holds the job's slice-edge column sums and the repaired scores next to slice borders
 // (with their per-head pool maxima).
@@ -1139,6 +1139,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   __shared__ int sHist[2][kHistBins];   // pass p uses buffer p % 2
   __shared__ int sScan[2 * kSelWaves];
   __shared__ int sSel[2][2];            // likewise
+  __shared__ uint32_t sRange[2][kSelWaves];   // per-wave smallest and largest ranking key
   const int tid = threadIdx.x, lane = tid & 63, wv = wave_id(), l16 = lane & 15;
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, NC = P.n_slices;
   const int job = blockIdx.x;
@@ -1235,25 +1236,58 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   } else {
     const int k = ly.k_sel;
     if (k > 0) {
-      // k-th largest candidate score: three radix passes over the 31 value bits (scores are
-      // >= 0, so the unsigned order of their bit patterns is the numeric order)
+      // k-th largest candidate score: radix passes over the ranking keys (scores are >= 0, so the
+      // unsigned order of their bit patterns is the numeric order) taken relative to the
+      // smallest candidate key, d = u - umin: the first pass bins the top 11 bits of the span
+      // [0, umax - umin], which spreads the candidates over its 2048 bins (the scores of a job
+      // span far fewer binades than a float holds, and same-bin atomics serialise), the next
+      // passes 10 bits each until every bit is resolved (at most three passes)
+      uint32_t umin = 0xffffffffu, umax = 0u;
+#pragma unroll
+      for (int i = 0; i < kSelRegs; ++i) {
+        const int j = w0 + 64 * i + lane;
+        const uint32_t u = rank_bits(x[i]);
+        if (j < w1) {
+          umin = min(umin, u);
+          umax = max(umax, u);
+        }
+      }
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        umin = min(umin, (uint32_t)__shfl_xor((int)umin, o));
+        umax = max(umax, (uint32_t)__shfl_xor((int)umax, o));
+      }
+      if (lane == 0) {
+        sRange[0][wv] = umin;
+        sRange[1][wv] = umax;
+      }
       uint32_t prefix = 0u, pmask = 0u;
       int kk = k;
       // both histogram buffers start cleared; buffer 0 is cleared again during pass 1 (pass 0's
       // last read of it precedes pass 0's last barrier), so a pass needs three barriers
       for (int b = tid; b < 2 * kHistBins; b += kSelThreads) (&sHist[0][0])[b] = 0;
       lds_barrier();
+#pragma unroll
+      for (int q = 0; q < kSelWaves; ++q) {
+        umin = min(umin, sRange[0][q]);
+        umax = max(umax, sRange[1][q]);
+      }
+      const int span_bits = 32 - __builtin_clz((umax - umin) | 1u);
+      int shift = max(0, span_bits - 11);
 #pragma unroll 1
       for (int pass = 0; pass < 3; ++pass) {
-        const int shift = pass == 0 ? 20 : (pass == 1 ? 10 : 0);
+        if (pass > 0) {
+          if (shift == 0) break;   // every bit resolved
+          shift = max(0, shift - 10);
+        }
         const int nb = pass == 0 ? 2048 : 1024;
         int* hist = sHist[pass & 1];
         int* sel = sSel[pass & 1];
 #pragma unroll
         for (int i = 0; i < kSelRegs; ++i) {
           const int j = w0 + 64 * i + lane;
-          const uint32_t u = rank_bits(x[i]);
-          if (j < w1 && (u & pmask) == prefix) atomicAdd(&hist[(u >> shift) & (nb - 1)], 1);
+          const uint32_t d = rank_bits(x[i]) - umin;
+          if (j < w1 && (d & pmask) == prefix) atomicAdd(&hist[(d >> shift) & (nb - 1)], 1);
         }
         if (pass == 1)
           for (int b = tid; b < 1024; b += kSelThreads) sHist[0][b] = 0;   // for pass 2
@@ -1285,11 +1319,13 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
           }
         }
         lds_barrier();
+        // a later pass's bin field may overlap bits an earlier pass fixed: those bits of sel
+        // equal the prefix's (every counted key matched it), so OR-ing them changes nothing
         prefix |= (uint32_t)sel[0] << shift;
         pmask |= (uint32_t)(nb - 1) << shift;
         kk = sel[1];
       }
-      const uint32_t tau = prefix;
+      const uint32_t tau = umin + prefix;
       const int need = kk;  // ties at tau taken in position order
       // ordered compaction over the waves' contiguous ranges: ballots rank each taken key
       // among the greater / equal keys before it
@@ -1491,6 +1527,9 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_kernel),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
       if (e == hipSuccess)
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_regs_kernel<8>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
+      if (e == hipSuccess)
         e = hipFuncSetAttribute(reinterpret_cast<const void*>(select_regs_kernel<16>),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, kSelectLds);
       if (e == hipSuccess)
@@ -1505,7 +1544,9 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
                                             (1 + P.group));
     if (P.seq_len <= kSelRegsMaxKeys && dyn <= (size_t)kSelectLds - 2 * kHistBins * 4 - 256) {
       const size_t lds = std::max(dyn, (size_t)kRepairLds);
-      if (P.seq_len <= 16 * kSelThreads)
+      if (P.seq_len <= 8 * kSelThreads)
+        launch_staged(kStageSelect, select_regs_kernel<8>, dim3(n_sel), dim3(kSelThreads), lds, st, P);
+      else if (P.seq_len <= 16 * kSelThreads)
         launch_staged(kStageSelect, select_regs_kernel<16>, dim3(n_sel), dim3(kSelThreads), lds, st, P);
       else
         launch_staged(kStageSelect, select_regs_kernel<32>, dim3(n_sel), dim3(kSelThreads), lds, st, P);
