@@ -1134,7 +1134,7 @@ constexpr int kSelRegsMaxKeys = kSelRegsMax * kSelThreads;   // 32K keys
 
 template <int kSelRegs>
 __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillLaunch P) {
-  // dynamic LDS: [n_edge] edges, [n_fix] repaired scores, [n_fix G] per-head pool maxima
+  // dynamic LDS: [n_edge] edges, [n_fix] repaired scores (or the exact rescoring's staging)
   extern __shared__ __attribute__((aligned(16))) float sDyn[];
   __shared__ int sHist[2][kHistBins];   // pass p uses buffer p % 2
   __shared__ int sScan[2 * kSelWaves];
@@ -1152,18 +1152,15 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   const float* Srow = P.S + (size_t)job * L;
   const int n = ly.all ? (snap ? L - w : L) : ly.cand_end;   // candidate (and reported) positions
   const int ph = P.pool_half, E = 4 * ph, twoP = 2 * ph;
-  // a window-scored job flagged by the pipelined kernel is rescored exactly first; its scores
-  // are then complete (no slice-border pool repair)
-  const bool repaired =
-      slot < P.n_window &&
-      __hip_atomic_load(P.counters + (size_t)kCounterStride * (1 + job) + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
-  if (repaired)
-    rescore_exact(ly.q + (size_t)(s * P.n_q_heads + h * G) * w * kHeadDim, ly.k + (size_t)bh * L * kHeadDim,
-                  P.S + (size_t)job * L, P.Su + (size_t)job * L, L, w, G, ph, snap ? 1 : 0, P.scale_log2, sDyn);
-  const bool fix = snap && ph > 0 && n > 0 && NC > 1 && !repaired;
-  const int n_edge = fix ? NC * G * E : 0, n_fix = fix ? (NC - 1) * twoP : 0;
-  float* sEdge = sDyn;
-  float* sFix = sDyn + n_edge;
+  // the repair flag, the candidate scores and the slice-edge sums are requested together (one
+  // round trip); a window-scored job flagged by the pipelined kernel (rare) is then rescored
+  // exactly and its scores read again, complete (no slice-border pool repair)
+  const uint32_t flag =
+      slot < P.n_window
+          ? __hip_atomic_load(P.counters + (size_t)kCounterStride * (1 + job) + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+          : 0u;
+  const bool fix0 = snap && ph > 0 && n > 0 && NC > 1;
+  const int n_edge0 = fix0 ? NC * G * E : 0;
 
   // ---- candidate scores into registers, slice-edge sums into LDS
   const int per_w = ((n + kSelWaves - 1) / kSelWaves + 63) & ~63;
@@ -1174,44 +1171,54 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
     const int j = w0 + 64 * i + lane;
     x[i] = j < w1 ? Srow[j] : 0.f;
   }
-  if (fix) {
+  if (fix0) {
     const float* Erow = P.edge + (size_t)job * NC * G * E;
-    for (int e0 = tid; e0 < n_edge; e0 += kSelThreads * 4) {
+    for (int e0 = tid; e0 < n_edge0; e0 += kSelThreads * 4) {
       float v[4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = e0 + u * kSelThreads < n_edge ? Erow[e0 + u * kSelThreads] : 0.f;
+      for (int u = 0; u < 4; ++u) v[u] = e0 + u * kSelThreads < n_edge0 ? Erow[e0 + u * kSelThreads] : 0.f;
 #pragma unroll
       for (int u = 0; u < 4; ++u)
-        if (e0 + u * kSelThreads < n_edge) sEdge[e0 + u * kSelThreads] = v[u];
+        if (e0 + u * kSelThreads < n_edge0) sDyn[e0 + u * kSelThreads] = v[u];
     }
   }
   loads_done();
+  const bool repaired = flag != 0u;
+  if (repaired) {
+    __syncthreads();   // the edge sums written above are done before the rescoring reuses that LDS
+    rescore_exact(ly.q + (size_t)(s * P.n_q_heads + h * G) * w * kHeadDim, ly.k + (size_t)bh * L * kHeadDim,
+                  P.S + (size_t)job * L, P.Su + (size_t)job * L, L, w, G, ph, snap ? 1 : 0, P.scale_log2, sDyn);
+    // the rescored values, past any copy the loads above left in the non-coherent cache
+#pragma unroll
+    for (int i = 0; i < kSelRegs; ++i) {
+      const int j = w0 + 64 * i + lane;
+      x[i] = j < w1 ? __hip_atomic_load(Srow + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0.f;
+    }
+    loads_done();
+  }
+  const bool fix = fix0 && !repaired;
+  const int n_edge = fix ? n_edge0 : 0, n_fix = fix ? (NC - 1) * twoP : 0;
+  float* sEdge = sDyn;
+  float* sFix = sDyn + n_edge;
   if (fix) {
     lds_barrier();
     // SnapKV: redo the pooled score of positions within pool_half of an interior slice border;
     // slice cb-1 holds keys [bnd-2P, bnd) at edge offsets [2P, 4P), slice cb keys [bnd, bnd+2P) at [0, 2P)
-    // first the pool maximum of every (position, head) over all threads, then the head sum of
-    // every position in head order
+    // one thread per position: the pool maximum of every head, summed in head order
     const int npre = L - w;
-    float* sPart = sFix + n_fix;
-    for (int task = tid; task < n_fix * G; task += kSelThreads) {
-      const int e = task / G, g = task - e * G;
+    for (int e = tid; e < n_fix; e += kSelThreads) {
       const int cb = 1 + e / twoP, o = e - (cb - 1) * twoP;
       const int bnd = cb * kSlice, j = bnd - ph + o;
-      float m = NEG_INF;
-      if (j >= 0 && j < npre && j < n) {
-        const int left = (cb - 1) * G * E + g * E + twoP - (bnd - twoP), right = cb * G * E + g * E - bnd;
-        const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
-        for (int t = lo; t <= hi; ++t) m = fmaxf(m, sEdge[t < bnd ? left + t : right + t]);
-      }
-      sPart[task] = m;
-    }
-    lds_barrier();
-    for (int e = tid; e < n_fix; e += kSelThreads) {
-      const int cb = 1 + e / twoP, j = cb * kSlice - ph + (e - (cb - 1) * twoP);
       float sc = 0.f;
-      if (j >= 0 && j < npre && j < n)
-        for (int g = 0; g < G; ++g) sc += sPart[e * G + g];
+      if (j >= 0 && j < npre && j < n) {
+        const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
+        for (int g = 0; g < G; ++g) {
+          const int left = (cb - 1) * G * E + g * E + twoP - (bnd - twoP), right = cb * G * E + g * E - bnd;
+          float m = NEG_INF;
+          for (int t = lo; t <= hi; ++t) m = fmaxf(m, sEdge[t < bnd ? left + t : right + t]);
+          sc += m;
+        }
+      }
       sFix[e] = sc * inv_g;
     }
     lds_barrier();
