@@ -263,18 +263,26 @@ def run_route(dev, rules, budgets, B, L, w, workload, steps, warmup, n_hh):
     per = time_steps(call, stream, steps, warmup)
     if rkv.prefill_check(ws) != 0:
         raise RuntimeError("eviction pass reported a failure")
-    rkv.profile_enable(rkv.STAGE_SCORE)
-    for _ in range(max(3, steps // 2)):
-        call(stream)
-    torch.cuda.synchronize()
-    n, tot = rkv.profile_read()
-    rkv.profile_enable(-1)
-    score_ms = tot / max(n, 1)
+    stage = {}
+    for name, sid in (("score", rkv.STAGE_SCORE), ("select", rkv.STAGE_SELECT), ("gather", rkv.STAGE_GATHER),
+                      ("zero", rkv.STAGE_ZERO)):
+        rkv.profile_enable(sid)
+        for _ in range(max(3, steps // 2)):
+            call(stream)
+        torch.cuda.synchronize()
+        n, tot = rkv.profile_read()
+        rkv.profile_enable(-1)
+        stage[name] = tot / max(n, 1)
     sb, pb = route_bytes(rules, budgets, B, L, w=w)
     flop = route_flop(rules, B, L, w=w)
     st = percentiles(per)
     ms = st["median_us"] * 1e-3
-    res = {"steps": percentiles(per), "score_us": score_ms * 1e3, "algorithmic_bytes": pb,
+    # scoring in the unprofiled passes: the pass less the other stages (as for the headline line)
+    score_ms = ms - (stage["select"] + stage["gather"] + stage["zero"])
+    if not 0.0 < score_ms <= stage["score"]:
+        score_ms = stage["score"]
+    res = {"steps": percentiles(per), "score_us": score_ms * 1e3, "score_profiled_us": stage["score"] * 1e3,
+           "algorithmic_bytes": pb,
            "score_algorithmic_bytes": sb, "hbm_frac": pb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
            "score_hbm_frac": sb / (score_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
            "score_mfma_frac": flop / (score_ms * 1e-3) / 1e12 / 2500.0,
@@ -532,7 +540,15 @@ def main():
     log("stage us/launch: " + ", ".join(f"{kk} {vv * 1e3:.1f}" for kk, vv in stage_ms.items()))
 
     score_bytes, pass_bytes = algorithmic_bytes(rules, budgets)
-    score_gbps = score_bytes / (stage_ms["score"] * 1e-3) / 1e9
+    # the scoring kernel's duration in the unprofiled timed passes: the pass time less the other
+    # three stages' own dispatch durations (those kernels time the same profiled or not; any gap
+    # between launches is counted as scoring, so this bounds the duration from above).  Profiled
+    # directly, the persistent scoring kernel runs 10-20 % slower (kept as score_profiled_us).
+    score_ms = ms_step - (stage_ms["select"] + stage_ms["gather"] + stage_ms["zero"])
+    if not 0.0 < score_ms <= stage_ms["score"]:
+        score_ms = stage_ms["score"]
+    log(f"scoring kernel in the timed passes: {score_ms * 1e3:.1f} us (profiled: {stage_ms['score'] * 1e3:.1f} us)")
+    score_gbps = score_bytes / (score_ms * 1e-3) / 1e9
     score_flop = route_flop(rules, 1, L_CTX)
     pass_gbps = pass_bytes / (ms_step * 1e-3) / 1e9
     traffic = traffic_record()
@@ -565,13 +581,14 @@ def main():
             "hbm_frac": pass_gbps / HBM_PEAK_GBPS,
             "single_steps": {**step_stats, "note": "another K steps, each between its own pair of events"},
             "stage_us": {kk: vv * 1e3 for kk, vv in stage_ms.items()},
+            "score_us_in_timed_passes": score_ms * 1e3,
         },
         "score_mfma": {
             "kernel": SCORE_KERNEL,
             "flop_per_launch": score_flop,
-            "achieved_TFLOPs": score_flop / (stage_ms["score"] * 1e-3) / 1e12,
+            "achieved_TFLOPs": score_flop / (score_ms * 1e-3) / 1e12,
             "peak_TFLOPs": 2500.0,
-            "frac": score_flop / (stage_ms["score"] * 1e-3) / 1e12 / 2500.0,
+            "frac": score_flop / (score_ms * 1e-3) / 1e12 / 2500.0,
         },
         "roofline": {
             "kernel": SCORE_KERNEL,
@@ -582,9 +599,12 @@ def main():
             "frac": score_gbps / HBM_PEAK_GBPS,
             "traffic": traffic,
             "algorithmic_bytes_per_launch": score_bytes,
-            "timing": "the kernel's dispatch start and stop timestamps (HIP events) in a loop of K passes "
-                      "with only this stage profiled; profiled, the persistent kernel runs 10-20 % slower "
-                      "than in the unprofiled timed passes (kernel trace in profiles/), so this is a bound",
+            "timing": "the smaller of two upper bounds on the scoring kernel's duration in the timed "
+                      "passes: their per-pass time (one HIP event pair around K back-to-back passes) less "
+                      "the prepare, select and gather kernels' own durations (their dispatch timestamps, "
+                      "HIP events, K passes each), and its own dispatch timestamps (score_profiled_us; "
+                      "the persistent kernel runs 10-20 % slower while profiled); kernel trace in profiles/",
+            "score_profiled_us": stage_ms["score"] * 1e3,
         },
     }
     del out, ws, call, q, k, v
