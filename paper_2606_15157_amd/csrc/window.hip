@@ -7,9 +7,9 @@
 // window_rows_kernel<NRT>: one workgroup per job (per part of its keys when there are few jobs:
 //   the columns kernel then adds the parts' row sums), one wave per 32 window rows (R = 32 NRT
 //   rows, the query rows of every head of the group, padded).  The wave's query fragments stay in
-//   registers; 128-key tiles stream through two LDS buffers (prefetched into registers one tile
-//   ahead) and bf16 MFMA logits are taken against a fixed per-row reference c_r = max(logit with
-//   the row's own key, logit with key 0), both true logits of the row; each lane sums e =
+//   registers; 128-key tiles stream through two LDS buffers (LDS DMA, one tile ahead) and bf16
+//   MFMA logits are taken against a fixed per-row reference c_r = max(logit with the row's own
+//   key, logit with key 0), both true logits of the row; each lane sums e =
 //   exp2((z - c_r) log2(e) / sqrt(d)) over its keys.  The row's log2 normaliser Lambda_r = c_r
 //   log2(e)/sqrt(d) + log2(Z_r) goes to the workspace; a row whose sum overflows (a key more than
 //   ~88 natural-log units above its reference) flags the job for the exact rescoring of the
@@ -28,6 +28,7 @@
 
 #include <math.h>
 
+#include "lds_dma.h"
 #include "rkv_internal.h"
 
 namespace rkv {
@@ -67,7 +68,9 @@ __device__ __forceinline__ WinRow win_row(int r, int tpr, int G, int w) {
 template <int NRT>
 __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillLaunch P) {
   constexpr int R = NRT * 32, NT = NRT * 64;
-  constexpr int PER = kSlice * kHeadDim / 8 / NT;   // 16-byte K chunks per thread per tile
+  // LDS DMA of a 128-key tile: 32 instructions of 4 keys (1 KiB) each, NI per wave
+  constexpr int NI = kSlice / 4 / NRT;
+  static_assert(NI % 2 == 0 && NRT % 4 == 0, "instruction pairs 4 KiB apart, waves in groups of four");
   __shared__ __attribute__((aligned(16))) uint16_t sK[2][kSlice * kHeadDim];
   __shared__ float sC[R];
   const int tid = threadIdx.x, lane = tid & 63, lg = lane >> 4, l16 = lane & 15;
@@ -119,23 +122,34 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
       qa[rs][st] = as_bf16x8w(v);
     }
   }
-  u32x4 pre[PER];
-  auto fetch = [&](int kt) {
+  // Wave wv moves instructions I = (wv % 4) + 4 u + 16 (wv / 4), u = 0 .. NI - 1: keys 4 I + [0, 4)
+  // of the tile, lane l filling key 4 I + l / 16 at chunk position l % 16 (the XOR swizzle of
+  // swzw, so the lane's source chunk is (l % 16) ^ ((4 I + l / 16) % 16)).  I % 4 is the wave's,
+  // so the lane's byte offset is the same for every instruction; instructions u and u + 1 are
+  // 4 KiB apart and go as one pair.  The tile past the prompt's end repeats its last key.
+  const uint32_t dma_off = (uint32_t)(lane >> 4) * 256u + (uint32_t)((lane & 15) ^ (4 * (wv & 3) + (lane >> 4))) * 16u;
+  const int i0 = (wv & 3) + 16 * (wv >> 2);
+  auto issue = [&](int kt, int buf) {
+    const uint32_t lds0 = lds_addr(&sK[buf][0]);
+    if (kt * kSlice + kSlice <= L) {
+      const char* tile = reinterpret_cast<const char*>(khead + (size_t)kt * kSlice * kHeadDim);
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
-      const int kk = min(kt * kSlice + key, L - 1);
-      pre[u] = *reinterpret_cast<const u32x4*>(khead + (size_t)kk * kHeadDim + 8 * ch);
+      for (int u = 0; u < NI; u += 2) {
+        const int I = i0 + 4 * u;
+        dma16s_pair(tile + 1024u * I, dma_off, lds0 + 1024u * I);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < NI; ++u) {
+        const int I = i0 + 4 * u, r = 4 * I + (lane >> 4);
+        const int key = min(kt * kSlice + r, L - 1);
+        dma16(khead + (size_t)key * kHeadDim + 8 * ((lane & 15) ^ (r & 15)), lds0 + 1024u * I);
+      }
     }
   };
-  auto put = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int c = tid + NT * u, key = c >> 4, ch = c & 15;
-      *reinterpret_cast<u32x4*>(&sK[buf][swzw(key, ch)]) = pre[u];
-    }
-  };
-  if (t0 < t1) fetch(t0);
+  // the first two tiles (the second stays in flight)
+  if (t0 < t1) issue(t0, 0);
+  if (t0 + 1 < t1) issue(t0 + 1, 1);
   __syncthreads();   // sC complete
   const float sl2 = P.scale_log2;
   float ncs[2][4], Z[2][4];
@@ -199,20 +213,19 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
   // bulk tiles: every key visible to every window row (keys below L - w + 1, the first row's
   // position, all inside the prompt); buffer parity counts from t0
   const int b_end = min(t1, (L - w + 1) / kSlice);
-  if (t0 < t1) {
-    put(0);
-    if (t0 + 1 < t1) fetch(t0 + 1);
-  }
+  // tile t0 in (this wave's part; then every wave's)
+  if (t0 + 1 < t1) wait_vmcnt<NI>();
+  else wait_vmcnt<0>();
   __syncthreads();
   if (t0 < b_end) mfma_half(0, 0, accA);
   for (int kt = t0; kt < b_end; ++kt) {
     const int b = (kt - t0) & 1;
     interleaved(b, 4, accB, accA);
-    if (kt + 1 < t1) {
-      put(b ^ 1);
-      if (kt + 2 < t1) fetch(kt + 2);
-    }
+    // tile kt + 1 (issued an iteration ago) in; after the barrier every wave is done with
+    // buffer b, which takes tile kt + 2
+    wait_vmcnt<0>();
     __syncthreads();
+    if (kt + 2 < t1) issue(kt + 2, b);
     if (kt + 1 < b_end) interleaved(b ^ 1, 0, accA, accB);
     else valu_half(accB);
   }
@@ -234,11 +247,9 @@ __global__ __launch_bounds__(NRT * 64, 1) void window_rows_kernel(const PrefillL
             if (key > last[rs][i]) x = kMaskedW;
             Z[rs][i] += __builtin_amdgcn_exp2f(x);
           }
-    if (kt + 1 < t1) {
-      put(b ^ 1);
-      if (kt + 2 < t1) fetch(kt + 2);
-    }
+    wait_vmcnt<0>();
     __syncthreads();
+    if (kt + 2 < t1) issue(kt + 2, b);
   }
   // ---- sums over the 16 lanes of each row group; the row's log2 normaliser (one part), or the
   // part's row sum and, from part 0, the reference (several parts: the columns kernel adds them)
