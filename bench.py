@@ -18,7 +18,6 @@ and the CPU oracle.  Prints one JSON line.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -33,7 +32,6 @@ WORKLOAD_ID = 2
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_pipe_kernel_route8k_traffic.json")
 SCORE_KERNEL = "score_pipe_kernel<1>"
 COPY_CAL_BYTES = 1 << 30     # plain device copy used to scale the PMC byte counters
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_15157_amd", "csrc", "prefill.hip")
 
 
 def log(msg):
@@ -412,7 +410,8 @@ def cpu_model():
 
 
 def kernel_source_hash():
-    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()
+    from paper_2606_15157_amd.pmc_summary import kernel_source_hash as source_hash
+    return source_hash()
 
 
 def traffic_record():

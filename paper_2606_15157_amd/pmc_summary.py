@@ -27,7 +27,8 @@ import statistics
 import sys
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-KERNEL_SRC = os.path.join(ROOT, "paper_2606_15157_amd", "csrc", "prefill.hip")
+# the scoring kernel's sources: a traffic record is taken on exactly these texts
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_15157_amd", "csrc", n) for n in ("prefill.hip", "lds_dma.h", "rkv_internal.h")]
 SCORE_NAME = "score_pipe_kernel<1>"
 COPY_NAME = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
@@ -60,6 +61,15 @@ def pick(d, needle):
     raise KeyError(needle)
 
 
+def kernel_source_hash() -> str:
+    """SHA-256 over the scoring kernel's source files (names and contents, in order)."""
+    h = hashlib.sha256()
+    for path in KERNEL_SOURCES:
+        h.update(os.path.basename(path).encode())
+        h.update(open(path, "rb").read())
+    return h.hexdigest()
+
+
 def main(argv):
     fetch_dir, write_dir, out_json, out_md = argv[1:5]
     fetch = per_dispatch(fetch_dir, "FETCH_SIZE")
@@ -74,7 +84,7 @@ def main(argv):
     write_b = statistics.median(sw) * w_scale
     rec = {
         "kernel": name,
-        "kernel_source_sha256": hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest(),
+        "kernel_source_sha256": kernel_source_hash(),
         "fetch_kib_median": statistics.median(sf),
         "write_kib_median": statistics.median(sw),
         "copy_calibration_bytes": COPY_BYTES,
