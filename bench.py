@@ -510,6 +510,19 @@ def main():
         b.record(stream)
     torch.cuda.synchronize()
     step_stats = percentiles([a.elapsed_time(b) for a, b in step_ev])
+    # cold steps: before each, a 512 MiB buffer is read (outside the events), so that the 256 MB
+    # last-level cache holds none of the pass's inputs when it starts
+    cold_buf = torch.ones(256 << 20, dtype=torch.bfloat16, device=dev)
+    cold_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for a, b in cold_ev:
+        cold_buf.sum()
+        a.record(stream)
+        call(stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    cold_stats = percentiles([a.elapsed_time(b) for a, b in cold_ev])
+    del cold_buf
+    log(f"cold steps (512 MiB read before each): median {cold_stats['median_us']:.1f} us")
     if rkv.prefill_check(ws) != 0:
         raise RuntimeError("scoring work items timed out in the timed region")
 
@@ -579,6 +592,8 @@ def main():
             "achieved_GBps": pass_gbps,
             "hbm_frac": pass_gbps / HBM_PEAK_GBPS,
             "single_steps": {**step_stats, "note": "another K steps, each between its own pair of events"},
+            "cold_steps": {**cold_stats, "note": "another K steps, each between its own pair of events, after a "
+                                                "512 MiB read that leaves none of the inputs in the last-level cache"},
             "stage_us": {kk: vv * 1e3 for kk, vv in stage_ms.items()},
             "score_us_in_timed_passes": score_ms * 1e3,
         },
