@@ -212,68 +212,62 @@ typedef float f32x4v __attribute__((ext_vector_type(4)));
 
 // Minus the reference logit of every row of every scored job, and the per-pass resets: the
 // status word, the job's slices' row sums and its partials ("not stored": NaN).
-// Four workgroups per job, each with a quarter of the rows and of the resets.
+// Sixteen workgroups of 128 threads per job, each with eight of the rows and a sixteenth of the
+// resets (many small workgroups: the kernel is a few dependent memory round trips).
+constexpr int kPrepParts = 16, kPrepThreads = 128;
 template <int NTH>
-__global__ __launch_bounds__(256) void prepare_kernel(const PrefillLaunch P) {
+__global__ __launch_bounds__(kPrepThreads) void prepare_kernel(const PrefillLaunch P) {
   constexpr int R = 128;
-  // four workgroups per job: workgroup q takes rows 32 q + [0, 32) and a quarter of the fill
-  constexpr int kParts = 4;
+  // workgroup q of the job takes rows 8 q + [0, 8) and a sixteenth of the fill
+  constexpr int kParts = kPrepParts;
   const int tid = threadIdx.x, job = blockIdx.x / kParts, q = blockIdx.x % kParts;
   const int Hkv = P.n_kv_heads, B = P.batch, L = P.seq_len, w = P.window, G = P.group, Hq = P.n_q_heads;
   const int h = job % Hkv, s = (job / Hkv) % B, slot = job / (Hkv * B);
   const PrefillLayer& ly = P.layer[P.slot_layer[slot]];
   if (blockIdx.x == 0 && tid == 0 && P.first_group) P.counters[0] = 0u;   // once per call
   if (q == 0 && tid == 0) P.counters[(size_t)kCounterStride * (1 + job) + 1] = 0u;   // the job's repair flag
+  // 16 lanes per row, lane c taking 16-byte chunk c of the query, the row's own key and key 0
+  // (each load instruction reads whole 256-byte rows); the loads are issued before the fill's
+  // stores so that their latency overlaps them
+  const int c = tid & 15;
+  const u32x4* ks = reinterpret_cast<const u32x4*>(ly.k + (size_t)(s * Hkv + h) * L * kHeadDim) + c;
+  const int r = 8 * q + (tid >> 4);
+  const int g = r / (NTH * 32), ii = r - g * (NTH * 32);
+  const bool valid = g < G && ii < w;
+  u32x4 qa = {0u, 0u, 0u, 0u}, da = qa, sa = qa;
+  if (valid) {
+    qa = reinterpret_cast<const u32x4*>(ly.q + ((size_t)(s * Hq + h * G + g) * w + ii) * kHeadDim)[c];
+    da = ks[(size_t)(L - w + ii) * 16];
+    sa = ks[0];
+  }
   {
     // every slice's row sums "not stored yet" (NaN): the consumers check them
     u32x4* st = reinterpret_cast<u32x4*>(P.stats + (size_t)job * P.n_slices * R);
     const u32x4 nan4 = {0xffffffffu, 0xffffffffu, 0xffffffffu, 0xffffffffu};
-    for (int i = tid + 256 * q; i < P.n_slices * R / 4; i += 256 * kParts) st[i] = nan4;
+    for (int i = tid + kPrepThreads * q; i < P.n_slices * R / 4; i += kPrepThreads * kParts) st[i] = nan4;
     // and the job's level-1 partials
     u32x4* pt = reinterpret_cast<u32x4*>(P.part + (size_t)job * kPipeGroups * R);
-    for (int i = tid + 256 * q; i < kPipeGroups * R / 4; i += 256 * kParts) pt[i] = nan4;
+    for (int i = tid + kPrepThreads * q; i < kPipeGroups * R / 4; i += kPrepThreads * kParts) pt[i] = nan4;
   }
-  // 16 lanes per row, lane c taking 16-byte chunk c of the query, the row's own key and key 0
-  // (each load instruction reads whole 256-byte rows); 16 rows per pass, 2 passes
-  const int c = tid & 15;
-  const u32x4* ks = reinterpret_cast<const u32x4*>(ly.k + (size_t)(s * Hkv + h) * L * kHeadDim) + c;
-  u32x4 qa[2], da[2], sa[2];
-  bool valid[2];
+  float zd = 0.f, zs = 0.f;
 #pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const int r = 32 * q + 16 * p + (tid >> 4);
-    const int g = r / (NTH * 32), ii = r - g * (NTH * 32);
-    valid[p] = g < G && ii < w;
-    if (valid[p]) {
-      qa[p] = reinterpret_cast<const u32x4*>(ly.q + ((size_t)(s * Hq + h * G + g) * w + ii) * kHeadDim)[c];
-      da[p] = ks[(size_t)(L - w + ii) * 16];
-      sa[p] = ks[0];
-    }
+  for (int u = 0; u < 4; ++u) {
+    const float q0 = __uint_as_float(qa[u] << 16), q1 = __uint_as_float(qa[u] & 0xffff0000u);
+    zd = fmaf(q0, __uint_as_float(da[u] << 16), zd);
+    zd = fmaf(q1, __uint_as_float(da[u] & 0xffff0000u), zd);
+    zs = fmaf(q0, __uint_as_float(sa[u] << 16), zs);
+    zs = fmaf(q1, __uint_as_float(sa[u] & 0xffff0000u), zs);
   }
-#pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    float zd = 0.f, zs = 0.f;
-    if (valid[p]) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const float q0 = __uint_as_float(qa[p][u] << 16), q1 = __uint_as_float(qa[p][u] & 0xffff0000u);
-        zd = fmaf(q0, __uint_as_float(da[p][u] << 16), zd);
-        zd = fmaf(q1, __uint_as_float(da[p][u] & 0xffff0000u), zd);
-        zs = fmaf(q0, __uint_as_float(sa[p][u] << 16), zs);
-        zs = fmaf(q1, __uint_as_float(sa[p][u] & 0xffff0000u), zs);
-      }
-    }
-    // sums over the 16 lanes of the row: rotations by 8, 4, 2, 1 inside each 16-lane DPP row
-    zd += dppf<0x128>(zd);
-    zs += dppf<0x128>(zs);
-    zd += dppf<0x124>(zd);
-    zs += dppf<0x124>(zs);
-    zd += dppf<0x122>(zd);
-    zs += dppf<0x122>(zs);
-    zd += dppf<0x121>(zd);
-    zs += dppf<0x121>(zs);
-    if (c == 0) P.ncl[(size_t)job * R + 32 * q + 16 * p + (tid >> 4)] = valid[p] ? -fmaxf(zd, zs) : 0.f;
-  }
+  // sums over the 16 lanes of the row: rotations by 8, 4, 2, 1 inside each 16-lane DPP row
+  zd += dppf<0x128>(zd);
+  zs += dppf<0x128>(zs);
+  zd += dppf<0x124>(zd);
+  zs += dppf<0x124>(zs);
+  zd += dppf<0x122>(zd);
+  zs += dppf<0x122>(zs);
+  zd += dppf<0x121>(zd);
+  zs += dppf<0x121>(zs);
+  if (c == 0) P.ncl[(size_t)job * R + r] = valid ? -fmaxf(zd, zs) : 0.f;
 }
 
 // Reduce-scatter of 16 values over the 16 lanes of each row: afterwards lane l holds the sum of
@@ -1442,7 +1436,7 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
   static const int pipe_wg = resident_pipe_groups();
   const bool pipe = n_jobs > 0 && row_tiles == 4 && P.force_window == 0 && P.n_slices <= kPipeMaxSlices &&
                     P.n_slices <= pipe_wg;
-  const dim3 prep_grid(n_jobs * 4), prep_block(256);
+  const dim3 prep_grid(n_jobs * kPrepParts), prep_block(kPrepThreads);
   if (pipe) {
     if (ntg == 1) launch_staged(kStageZero, prepare_kernel<1>, prep_grid, prep_block, 0, st, P);
     else if (ntg == 2) launch_staged(kStageZero, prepare_kernel<2>, prep_grid, prep_block, 0, st, P);
