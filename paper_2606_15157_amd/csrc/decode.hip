@@ -168,9 +168,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
     // dot products of the block at base (rows in kv), summed over the 16 lanes of each entry
     // (one DPP row, every lane gets the sum); one lane writes each logit to LDS
     auto process = [&](int base, const u32x4 (&kv)[4]) {
-      float dot[4][G];
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 4; ++j) {
+        const int e = base + rsub + 16 * j;
 #pragma unroll
         for (int g = 0; g < G; ++g) {
           float d = 0.f;
@@ -180,16 +180,9 @@ __global__ __launch_bounds__(kDecThreads) void decode_kernel(const DecodeLaunch 
           d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x124, 0xf, 0xf, false));
           d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x122, 0xf, 0xf, false));
           d += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, d), 0x121, 0xf, 0xf, false));
-          dot[j][g] = d;
-        }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int e = base + rsub + 16 * j;
-        if (e <= C) {
-#pragma unroll
-          for (int g = 0; g < G; ++g) {
-            mx[g] = fmaxf(mx[g], dot[j][g]);
-            if (c16 == ((j * G + g) & 15)) sZ[g * (C + 1) + e] = dot[j][g];
+          if (e <= C) {
+            mx[g] = fmaxf(mx[g], d);
+            if (c16 == ((j * G + g) & 15)) sZ[g * (C + 1) + e] = d;
           }
         }
       }
