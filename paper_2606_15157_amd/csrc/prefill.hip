@@ -1114,14 +1114,16 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
   const bool fix0 = snap && ph > 0 && n > 0 && NC > 1;
   const int n_edge0 = fix0 ? NC * G * E : 0;
 
-  // ---- candidate scores into registers, slice-edge sums into LDS
-  const int per_w = ((n + kSelWaves - 1) / kSelWaves + 63) & ~63;
-  const int w0 = min(n, wv * per_w), w1 = min(n, w0 + per_w);
+  // ---- candidate scores into registers, slice-edge sums into LDS.  The waves' ranges are cut
+  // from the prompt length, a kernel argument, so that the score loads do not wait for the
+  // layer-table lookups that give the candidate count n; positions from n on are not candidates
+  const int per_w = ((L + kSelWaves - 1) / kSelWaves + 63) & ~63;
+  const int w0 = wv * per_w, wL = min(L, w0 + per_w), w1 = min(n, w0 + per_w);
   float x[kSelRegs];
 #pragma unroll
   for (int i = 0; i < kSelRegs; ++i) {
     const int j = w0 + 64 * i + lane;
-    x[i] = j < w1 ? Srow[j] : 0.f;
+    x[i] = j < wL ? Srow[j] : 0.f;
   }
   if (fix0) {
     const float* Erow = P.edge + (size_t)job * NC * G * E;
@@ -1158,20 +1160,44 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
     // slice cb-1 holds keys [bnd-2P, bnd) at edge offsets [2P, 4P), slice cb keys [bnd, bnd+2P) at [0, 2P)
     // one thread per position: the pool maximum of every head, summed in head order
     const int npre = L - w;
-    for (int e = tid; e < n_fix; e += kSelThreads) {
-      const int cb = 1 + e / twoP, o = e - (cb - 1) * twoP;
-      const int bnd = cb * kSlice, j = bnd - ph + o;
-      float sc = 0.f;
-      if (j >= 0 && j < npre && j < n) {
-        const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
-        for (int g = 0; g < G; ++g) {
-          const int left = (cb - 1) * G * E + g * E + twoP - (bnd - twoP), right = cb * G * E + g * E - bnd;
+    if (G == 4 && ph == 3) {
+      // the common layout: four heads, 7-wide pool, every read issued at once (neighbours clamped
+      // into the pool window repeat a member, which leaves the maximum unchanged)
+      for (int e = tid; e < n_fix; e += kSelThreads) {
+        const int cb = 1 + e / 6, o = e - (cb - 1) * 6;
+        const int bnd = cb * kSlice, j = bnd - 3 + o;
+        const bool ok = j >= 0 && j < npre && j < n;
+        const int lo = ok ? max(j - 3, 0) : bnd, hi = ok ? min(j + 3, npre - 1) : bnd;
+        float sc = 0.f;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int left = (cb - 1) * 4 * 12 + g * 12 + 6 - (bnd - 6), right = cb * 4 * 12 + g * 12 - bnd;
           float m = NEG_INF;
-          for (int t = lo; t <= hi; ++t) m = fmaxf(m, sEdge[t < bnd ? left + t : right + t]);
+#pragma unroll
+          for (int u = 0; u < 7; ++u) {
+            const int t = min(max(j - 3 + u, lo), hi);
+            m = fmaxf(m, sEdge[t < bnd ? left + t : right + t]);
+          }
           sc += m;
         }
+        sFix[e] = ok ? sc * inv_g : 0.f;
       }
-      sFix[e] = sc * inv_g;
+    } else {
+      for (int e = tid; e < n_fix; e += kSelThreads) {
+        const int cb = 1 + e / twoP, o = e - (cb - 1) * twoP;
+        const int bnd = cb * kSlice, j = bnd - ph + o;
+        float sc = 0.f;
+        if (j >= 0 && j < npre && j < n) {
+          const int lo = max(j - ph, 0), hi = min(j + ph, npre - 1);
+          for (int g = 0; g < G; ++g) {
+            const int left = (cb - 1) * G * E + g * E + twoP - (bnd - twoP), right = cb * G * E + g * E - bnd;
+            float m = NEG_INF;
+            for (int t = lo; t <= hi; ++t) m = fmaxf(m, sEdge[t < bnd ? left + t : right + t]);
+            sc += m;
+          }
+        }
+        sFix[e] = sc * inv_g;
+      }
     }
     lds_barrier();
 #pragma unroll
