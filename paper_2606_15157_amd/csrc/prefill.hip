@@ -78,6 +78,33 @@ __device__ __forceinline__ int row16_sum(int x) {
   x += __builtin_amdgcn_update_dpp(0, x, 0x121, 0xf, 0xf, false);   // row_ror:1
   return x;
 }
+// Minimum / maximum of an unsigned value over the 16 lanes of each DPP row (every lane gets it).
+__device__ __forceinline__ uint32_t row16_umin(uint32_t x) {
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x128, 0xf, 0xf, false));   // row_ror:8
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x124, 0xf, 0xf, false));   // row_ror:4
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x122, 0xf, 0xf, false));   // row_ror:2
+  x = min(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x121, 0xf, 0xf, false));   // row_ror:1
+  return x;
+}
+__device__ __forceinline__ uint32_t row16_umax(uint32_t x) {
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x128, 0xf, 0xf, false));
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x124, 0xf, 0xf, false));
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x122, 0xf, 0xf, false));
+  x = max(x, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x121, 0xf, 0xf, false));
+  return x;
+}
+// Inclusive prefix sum over the 64 lanes of a wave: shifts by 1, 2, 4, 8 inside each 16-lane row
+// (lanes shifted in from outside the row read 0), then each row's total carried into the rows
+// after it (row_bcast:15 into rows 1 and 3, row_bcast:31 into rows 2 and 3).
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xf, 0xf, true);    // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xf, 0xf, true);    // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xf, 0xf, true);    // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xf, 0xf, true);    // row_shr:8
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xa, 0xf, false);   // row_bcast:15
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xc, 0xf, false);   // row_bcast:31
+  return x;
+}
 template <int CTRL>
 __device__ __forceinline__ float dppf(float x) {
   return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
@@ -1237,11 +1264,13 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
           umax = max(umax, u);
         }
       }
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        umin = min(umin, (uint32_t)__shfl_xor((int)umin, o));
-        umax = max(umax, (uint32_t)__shfl_xor((int)umax, o));
-      }
+      // wave minimum and maximum: DPP inside the rows, then the four rows' results
+      umin = row16_umin(umin);
+      umax = row16_umax(umax);
+      umin = min(min((uint32_t)__builtin_amdgcn_readlane((int)umin, 0), (uint32_t)__builtin_amdgcn_readlane((int)umin, 16)),
+                 min((uint32_t)__builtin_amdgcn_readlane((int)umin, 32), (uint32_t)__builtin_amdgcn_readlane((int)umin, 48)));
+      umax = max(max((uint32_t)__builtin_amdgcn_readlane((int)umax, 0), (uint32_t)__builtin_amdgcn_readlane((int)umax, 16)),
+                 max((uint32_t)__builtin_amdgcn_readlane((int)umax, 32), (uint32_t)__builtin_amdgcn_readlane((int)umax, 48)));
       if (lane == 0) {
         sRange[0][wv] = umin;
         sRange[1][wv] = umax;
@@ -1252,11 +1281,9 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
       // last read of it precedes pass 0's last barrier), so a pass needs three barriers
       for (int b = tid; b < 2 * kHistBins; b += kSelThreads) (&sHist[0][0])[b] = 0;
       lds_barrier();
-#pragma unroll
-      for (int q = 0; q < kSelWaves; ++q) {
-        umin = min(umin, sRange[0][q]);
-        umax = max(umax, sRange[1][q]);
-      }
+      // the workgroup's: one read per lane (wave l16's values), a 16-lane DPP reduction
+      umin = row16_umin(l16 < kSelWaves ? sRange[0][l16] : 0xffffffffu);
+      umax = row16_umax(l16 < kSelWaves ? sRange[1][l16] : 0u);
       const int span_bits = 32 - __builtin_clz((umax - umin) | 1u);
       int shift = max(0, span_bits - 11);
 #pragma unroll 1
@@ -1281,12 +1308,7 @@ __global__ __launch_bounds__(kSelThreads) void select_regs_kernel(const PrefillL
         const int per = nb / kSelThreads;
         int cnt = 0;
         for (int q = 0; q < per; ++q) cnt += hist[nb - 1 - (tid * per + q)];
-        int inc = cnt;  // inclusive scan of cnt over the workgroup
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-          const int y = __shfl_up(inc, o);
-          if (lane >= o) inc += y;
-        }
+        const int inc = wave_inclusive_scan(cnt);   // inclusive scan of cnt over the wave
         if (lane == 63) sScan[wv] = inc;
         lds_barrier();
         // plus the counts of the waves before this one: one read per lane, a 16-lane sum
