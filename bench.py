@@ -30,7 +30,7 @@ HBM_PEAK_GBPS = 8000.0
 L_CTX, N_LAYERS, HQ, HKV, D, W, POOL, AVG_BUDGET, B_MIN = 8192, 32, 32, 8, 128, 32, 7, 512, 48
 WORKLOAD_ID = 2
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "score_pipe_kernel_route8k_traffic.json")
-SCORE_KERNEL = "score_pipe_kernel<1>"
+SCORE_KERNEL = "score_pipe_kernel<1, false>"
 COPY_CAL_BYTES = 1 << 30     # plain device copy used to scale the PMC byte counters
 
 

@@ -233,6 +233,7 @@ __device__ __forceinline__ void lds_barrier() {
 // ---------------------------------------------------------------------------------------------
 constexpr int kPipeWaves = 8;
 constexpr int kPipeThreads = kPipeWaves * 64;
+constexpr int kPipeShortItems = 4;   // items per workgroup up to which the short form runs
 
 typedef float f32x4v __attribute__((ext_vector_type(4)));
 
@@ -312,7 +313,10 @@ __device__ __forceinline__ bf16x8 frag16(const uint16_t* base, int row, int chun
   return *reinterpret_cast<const bf16x8*>(base + (row * 16 + (chunk ^ (row & 15))) * 8);
 }
 
-template <int NTH>
+// SHORT: every workgroup has at most a few items (short prompts, few layers); then the phases of
+// the pipeline's fill and drain iterations, which only run on stale data, are skipped (in long
+// runs they stay unconditional: the loop's code is then the tighter one).
+template <int NTH, bool SHORT>
 __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const PrefillLaunch P, int n_wg) {
   constexpr int R = 128;
   __shared__ __attribute__((aligned(16))) uint16_t sQ[2][R * kHeadDim];
@@ -715,7 +719,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
     sColP = sColPb[t & 1];
     // both phases run in every iteration (on stale data at the ends of the pipeline, with their
     // results unused), so each register set is redefined unconditionally
-    phase_a(ja, t & 1, ea);
+    if (!SHORT || doA) phase_a(ja, t & 1, ea);
     // MID: everything this wave issued in earlier iterations has completed (the partials of item
     // t - 3's job, the DMA of item t + 1)
     wait_vmcnt<0>();
@@ -731,7 +735,7 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
       o.y = sStat[0][2 * lane + 1] + sStat[1][2 * lane + 1] + sStat[2][2 * lane + 1] + sStat[3][2 * lane + 1];
       store_coherent2(P.stats + ((size_t)ja.job * nsl + ja.slice) * R + 2 * lane, o.x, o.y);
     }
-    phase_b(j3, eb);
+    if (!SHORT || doB) phase_b(j3, eb);
     lds_barrier();   // B2: sColP complete
     if (wv < 4) {
       if (sums) {
@@ -1451,7 +1455,7 @@ int device_cus() {
 // Resident workgroups of the pipelined kernel (one per CU; the same for every NTH).
 int resident_pipe_groups() {
   int per_cu = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_pipe_kernel<1>, kPipeThreads, 0) != hipSuccess ||
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, score_pipe_kernel<1, false>, kPipeThreads, 0) != hipSuccess ||
       per_cu < 1)
     per_cu = 1;
   return per_cu * device_cus();
@@ -1503,9 +1507,17 @@ int launch_prefill(const PrefillLaunch& P, int row_tiles, void* stream) {
       // its completion: dispatch timestamps or a marker after it), so its profiled time is an
       // upper bound; kernel traces of unprofiled passes give the undisturbed time
       const dim3 grid(n_wg), block(kPipeThreads);
-      if (ntg == 1) launch_staged(kStageScore, score_pipe_kernel<1>, grid, block, 0, st, P, n_wg);
-      else if (ntg == 2) launch_staged(kStageScore, score_pipe_kernel<2>, grid, block, 0, st, P, n_wg);
-      else launch_staged(kStageScore, score_pipe_kernel<4>, grid, block, 0, st, P, n_wg);
+      // at most kPipeShortItems items per workgroup: the form that skips the stale phases
+      const bool short_run = (n_items + n_wg - 1) / n_wg <= kPipeShortItems;
+      if (short_run) {
+        if (ntg == 1) launch_staged(kStageScore, score_pipe_kernel<1, true>, grid, block, 0, st, P, n_wg);
+        else if (ntg == 2) launch_staged(kStageScore, score_pipe_kernel<2, true>, grid, block, 0, st, P, n_wg);
+        else launch_staged(kStageScore, score_pipe_kernel<4, true>, grid, block, 0, st, P, n_wg);
+      } else {
+        if (ntg == 1) launch_staged(kStageScore, score_pipe_kernel<1, false>, grid, block, 0, st, P, n_wg);
+        else if (ntg == 2) launch_staged(kStageScore, score_pipe_kernel<2, false>, grid, block, 0, st, P, n_wg);
+        else launch_staged(kStageScore, score_pipe_kernel<4, false>, grid, block, 0, st, P, n_wg);
+      }
     } else {
       // longer prompts and eight row tiles: row normalisers, then column sums
       profile_mark(kStageScore, false, stream);

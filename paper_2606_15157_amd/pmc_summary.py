@@ -29,7 +29,7 @@ import sys
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 # the scoring kernel's sources: a traffic record is taken on exactly these texts
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2606_15157_amd", "csrc", n) for n in ("prefill.hip", "lds_dma.h", "rkv_internal.h")]
-SCORE_NAME = "score_pipe_kernel<1>"
+SCORE_NAME = "score_pipe_kernel<1, false>"
 COPY_NAME = "__amd_rocclr_copyBuffer"
 COPY_BYTES = 1 << 30
 # the profiled program: the headline route only, plus the 1 GiB calibration copy
