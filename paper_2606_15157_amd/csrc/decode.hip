@@ -24,39 +24,61 @@ constexpr int kDecWaves = kDecThreads / 64;
 
 __device__ __forceinline__ bf16x2 as_bf16x2(uint32_t v) { return __builtin_bit_cast(bf16x2, v); }
 
-__device__ __forceinline__ float block_reduce_max(float v, float* sh) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  if (lane == 0) sh[wv] = v;
-  __syncthreads();
-  float r = sh[0];
-#pragma unroll
-  for (int i = 1; i < kDecWaves; ++i) r = fmaxf(r, sh[i]);
-  __syncthreads();
-  return r;
+// Wave reductions by DPP: rotations inside each 16-lane row (every lane of a row ends with the
+// row's value), then the four rows' values read from lanes 0, 16, 32 and 48 and combined in that
+// order (a fixed order: the sums are reproducible).
+template <int CTRL>
+__device__ __forceinline__ float dppf(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xf, 0xf, false));
 }
-
-__device__ __forceinline__ float block_reduce_sum(float v, float* sh) {
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+template <int CTRL>
+__device__ __forceinline__ uint32_t dppu(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xf, 0xf, false);
+}
+__device__ __forceinline__ float rows4(float v, int i) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16 * i));
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dppf<0x128>(v));   // row_ror:8
+  v = fmaxf(v, dppf<0x124>(v));   // row_ror:4
+  v = fmaxf(v, dppf<0x122>(v));   // row_ror:2
+  v = fmaxf(v, dppf<0x121>(v));   // row_ror:1
+  return fmaxf(fmaxf(rows4(v, 0), rows4(v, 1)), fmaxf(rows4(v, 2), rows4(v, 3)));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dppf<0x128>(v);
+  v += dppf<0x124>(v);
+  v += dppf<0x122>(v);
+  v += dppf<0x121>(v);
+  return (rows4(v, 0) + rows4(v, 1)) + (rows4(v, 2) + rows4(v, 3));
+}
+// minimum of a 64-bit key (compared as (high word, low word))
+template <int CTRL>
+__device__ __forceinline__ void min_step(uint32_t& hi, uint32_t& lo) {
+  const uint32_t oh = dppu<CTRL>(hi), ol = dppu<CTRL>(lo);
+  const bool take = oh < hi || (oh == hi && ol < lo);
+  hi = take ? oh : hi;
+  lo = take ? ol : lo;
+}
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
+  uint32_t hi = (uint32_t)(v >> 32), lo = (uint32_t)v;
+  min_step<0x128>(hi, lo);
+  min_step<0x124>(hi, lo);
+  min_step<0x122>(hi, lo);
+  min_step<0x121>(hi, lo);
+  uint64_t r = ~0ull;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  if (lane == 0) sh[wv] = v;
-  __syncthreads();
-  float r = 0.f;
-#pragma unroll
-  for (int i = 0; i < kDecWaves; ++i) r += sh[i];
-  __syncthreads();
+  for (int i = 0; i < 4; ++i) {
+    const uint64_t x = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)hi, 16 * i) << 32) |
+                       (uint32_t)__builtin_amdgcn_readlane((int)lo, 16 * i);
+    r = x < r ? x : r;
+  }
   return r;
 }
 
 __device__ __forceinline__ uint64_t block_reduce_min_u64(uint64_t v, uint64_t* sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint64_t y = __shfl_xor(v, o);
-    v = y < v ? y : v;
-  }
+  v = wave_min_u64(v);
   if (lane == 0) sh[wv] = v;
   __syncthreads();
   uint64_t r = sh[0];
@@ -66,14 +88,13 @@ __device__ __forceinline__ uint64_t block_reduce_min_u64(uint64_t v, uint64_t* s
   return r;
 }
 
-// Block-wide max / sum of G values at once (per-value order as in the scalar versions).
+// Block-wide max / sum of G values at once (each value: its waves' results in wave order).
 template <int G>
 __device__ __forceinline__ void block_reduce_max_v(float (&v)[G], float* sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v[g] = fmaxf(v[g], __shfl_xor(v[g], o));
+    v[g] = wave_max(v[g]);
     if (lane == 0) sh[wv * G + g] = v[g];
   }
   __syncthreads();
@@ -91,8 +112,7 @@ __device__ __forceinline__ void block_reduce_sum_v(float (&v)[G], float* sh) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v[g] += __shfl_xor(v[g], o);
+    v[g] = wave_sum(v[g]);
     if (lane == 0) sh[wv * G + g] = v[g];
   }
   __syncthreads();
