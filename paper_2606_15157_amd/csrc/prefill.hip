@@ -559,8 +559,8 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
         m1 = fmaxf(m1, b[u]);
       }
       float su = c0[kl] + c1[kl], sc = m0 + m1;
-      su += __shfl_xor(su, 1);
-      sc += __shfl_xor(sc, 1);
+      su += dppf<0xB1>(su);   // quad_perm [1,0,3,2]: the other head half's sum (lane ^ 1)
+      sc += dppf<0xB1>(sc);
       if (h == 0 && kk < L) {
         su *= inv_g;
         Srow[kk] = kk < npre ? sc * inv_g : su;
@@ -584,8 +584,8 @@ __global__ __launch_bounds__(kPipeThreads, 1) void score_pipe_kernel(const Prefi
           sc += m;
         }
       }
-      su += __shfl_xor(su, 1);
-      sc += __shfl_xor(sc, 1);
+      su += dppf<0xB1>(su);   // quad_perm [1,0,3,2]: the other head half's sum (lane ^ 1)
+      sc += dppf<0xB1>(sc);
       if ((tid & 1) == 0 && kk < L) {
         su *= inv_g;
         Srow[kk] = kk < npre ? sc * inv_g : su;
