@@ -153,6 +153,17 @@ def test_odd_window_and_group_shapes():
     run_case(rules, [150, 150], layers, window=20, pool_kernel=5, label="w20g2")
 
 
+@pytest.mark.parametrize("L,Hq,Hkv", [(33000, 32, 8), (28000, 32, 4)], ids=["L33000_g4", "L28000_g8"])
+def test_long_prompts_general_selection(L, Hq, Hkv):
+    """The selection kernel for what the register-resident one cannot hold: more than 32K keys
+    (L = 33000, ragged, its scores past the LDS cache), and eight query heads per KV head at 28K
+    keys, whose slice-edge sums do not fit beside the registers (scores in the LDS cache); both
+    score through the window kernels (more than 64 slices)."""
+    rules = [OP.SNAPKV, OP.H2O]
+    layers = [[gen(11, 0, l, L, Hq=Hq, Hkv=Hkv)] for l in range(2)]
+    run_case(rules, [1024, 1024], layers, window=32, label=f"L{L}_Hq{Hq}_Hkv{Hkv}")
+
+
 @pytest.mark.parametrize("Hq,Hkv", [(8, 8), (32, 4)], ids=["g1", "g8"])
 def test_group_sizes_one_and_eight(Hq, Hkv):
     """G = 1 (one row tile of 32, padded to four in the pipelined kernel) and G = 8 (eight row
