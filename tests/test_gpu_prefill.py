@@ -153,6 +153,15 @@ def test_odd_window_and_group_shapes():
     run_case(rules, [150, 150], layers, window=20, pool_kernel=5, label="w20g2")
 
 
+def test_prompt_between_8k_and_16k():
+    """L = 12345 (ragged, 97 slices): the window kernels with the rows kernel's keys split over
+    workgroups, and the selection with 16 scores per thread; SnapKV, H2O and TOVA layers."""
+    L = 12345
+    rules = [OP.SNAPKV, OP.H2O, OP.TOVA]
+    layers = [[gen(12, 0, l, L)] for l in range(3)]
+    run_case(rules, [1024, 1024, 1024], layers, window=32, label="L12345")
+
+
 @pytest.mark.parametrize("L,Hq,Hkv", [(33000, 32, 8), (28000, 32, 4)], ids=["L33000_g4", "L28000_g8"])
 def test_long_prompts_general_selection(L, Hq, Hkv):
     """The selection kernel for what the register-resident one cannot hold: more than 32K keys
