@@ -153,6 +153,18 @@ def test_odd_window_and_group_shapes():
     run_case(rules, [150, 150], layers, window=20, pool_kernel=5, label="w20g2")
 
 
+@pytest.mark.parametrize("w,Hq,Hkv", [(64, 16, 8), (100, 8, 8)], ids=["w64_g2", "w100_g1"])
+def test_wide_windows_few_heads(w, Hq, Hkv):
+    """Windows of two and four 32-row tiles per head with two and one query heads per KV head
+    (four row tiles in all: the pipelined kernel's two- and four-tile forms, the second with
+    padding rows), L = 5000 and four layers: more than four items per workgroup, so the
+    long-run form of the kernel."""
+    L = 5000
+    rules = [OP.SNAPKV, OP.H2O, OP.SNAPKV, OP.H2O]
+    layers = [[gen(13, 0, l, L, w=w, Hq=Hq, Hkv=Hkv)] for l in range(4)]
+    run_case(rules, [400] * 4, layers, window=w, label=f"w{w}_Hq{Hq}")
+
+
 def test_prompt_between_8k_and_16k():
     """L = 12345 (ragged, 97 slices): the window kernels with the rows kernel's keys split over
     workgroups, and the selection with 16 scores per thread; SnapKV, H2O and TOVA layers."""
