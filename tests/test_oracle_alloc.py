@@ -26,10 +26,10 @@ def test_single_clamp_round():
     assert list(alloc.allocate([10, 1, 1], 30, 8)) == [14, 8, 8]
 
 
-def test_clamp_needs_several_rounds():
-    # round 1: 24*[10,3,1]/14 = [17.1, 5.14, 1.71] -> fix layer 2 at 5
-    # round 2: 19*[10,3]/13 = [14.6, 4.38] -> fix layer 1 at 5
-    # round 3: layer 0 takes the remaining 14
+def test_clamp_needs_several_passes():
+    # pass 1: 24*[10,3,1]/14 = [17.1, 5.14, 1.71] -> fix layer 2 at 5
+    # pass 2: 19*[10,3]/13 = [14.6, 4.38] -> fix layer 1 at 5
+    # pass 3: layer 0 takes the remaining 14
     assert list(alloc.allocate([10, 3, 1], 24, 5)) == [14, 5, 5]
 
 
