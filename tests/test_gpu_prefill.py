@@ -319,3 +319,32 @@ def test_bench_call_matches_debug_call_at_full_size():
         idx = out["idx"][l].cpu().numpy()
         for h in range(8):
             check_retained(idx[0, h], ora, h, 8192, f"bench call layer {l} head {h}")
+
+
+@pytest.mark.parametrize("case", range(40))
+def test_random_shapes_against_oracle(case):
+    """Seeded random shapes: batch 1-2, 1-8 KV heads, 1-8 query heads per KV head (3 included),
+    windows of 1 up to the row-tile limit, prompts of a few keys up to 6000 (ragged slices), odd
+    pools up to 15, sink counts and recent fractions of H2O varied, and 1-4 layers mixing SnapKV,
+    H2O, StreamingLLM, Full and TOVA with budgets from 0 past the prompt length."""
+    rng = np.random.default_rng(9000 + case)
+    batch = int(rng.integers(1, 3))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 3, 4, 8]))
+    w = int(rng.integers(1, 32 * (8 // G) + 1))
+    L = int(np.exp(rng.uniform(np.log(max(w, 2)), np.log(6000))))
+    pool = int(rng.choice([1, 3, 5, 7, 9, 15]))
+    n_sink = int(rng.integers(0, 9))
+    num, den = [(1, 2), (1, 3), (2, 3), (0, 1)][int(rng.integers(0, 4))]
+    choices = [OP.SNAPKV, OP.H2O, OP.STREAMING, OP.FULL] + ([OP.TOVA] if G != 3 else [])
+    n_layers = int(rng.integers(1, 5))
+    rules = [int(rng.choice(choices)) for _ in range(n_layers)]
+    budgets = []
+    for _ in range(n_layers):
+        kind = int(rng.integers(0, 8))
+        budgets.append([0, 1, L, L + 5][kind] if kind < 4 else int(rng.integers(1, L + 1)))
+    layers = [[gen(60 + case, s, l, L, w=w, Hq=G * Hkv, Hkv=Hkv) for s in range(batch)] for l in range(n_layers)]
+    label = (f"case {case}: B{batch} Hkv{Hkv} G{G} w{w} L{L} pool{pool} sink{n_sink} recent {num}/{den} "
+             f"rules {rules} budgets {budgets}")
+    print(label, flush=True)
+    run_case(rules, budgets, layers, window=w, pool_kernel=pool, n_sink=n_sink, num=num, den=den, label=label)
