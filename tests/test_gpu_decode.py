@@ -223,3 +223,26 @@ def test_decode_capacity_past_1024():
     state["acc"] = [state["acc"][0], None]
     n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers)
     print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_decode_shapes(case):
+    """Seeded random decode shapes: batch 1-3, 1-8 KV heads, 1, 2, 4 or 8 query heads per KV
+    head, capacities from 2 to 1300 (past the 1024 entries requested with the key stream),
+    prompts longer than the capacity by a ragged amount, 1-3 layers each H2O or TOVA, 2-5
+    teacher-forced steps."""
+    rng = np.random.default_rng(7000 + case)
+    B = int(rng.integers(1, 4))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 4, 8]))
+    C = int(np.exp(rng.uniform(np.log(2), np.log(1300))))
+    L = C + int(rng.integers(32, 400))
+    n_layers = int(rng.integers(1, 4))
+    steps = int(rng.integers(2, 6))
+    rules_dec = [int(rng.choice([OP.H2O, OP.TOVA])) for _ in range(n_layers)]
+    print(f"case {case}: B{B} Hkv{Hkv} G{G} C{C} L{L} steps {steps} rules {rules_dec}", flush=True)
+    plan, state = prefill_state(rules_dec, C, L, B, n_layers, Hq=G * Hkv, Hkv=Hkv)
+    state["acc"] = [a if r == OP.H2O else None for a, r in zip(state["acc"], rules_dec)]
+    n_close = _decode_and_check(plan, state, rules_dec, C, L, B, steps, n_layers, Hq=G * Hkv, Hkv=Hkv,
+                                seed_workload=20 + case)
+    print(f"victims chosen differently inside the 1e-3 tie band: {n_close}")
