@@ -106,3 +106,27 @@ def test_full_span_sampled_head_at_8k():
     check_gather(torch_to_bits(out["k_out"][0])[0, h], torch_to_bits(out["v_out"][0])[0, h], x["k"][h], x["v"][h],
                  idx, what)
     check_scores(out["acc"][0][0, h].cpu().numpy(), ora["acc"][0], what + " acc")
+
+
+@pytest.mark.parametrize("case", range(16))
+def test_random_full_span_and_tova_shapes(case):
+    """Seeded random routes mixing full-span H2O, TOVA, window H2O and SnapKV layers: batch 1-2,
+    1-8 KV heads, 1, 2, 4 or 8 query heads per KV head, ragged prompts of 2-1500 keys, windows
+    up to the row-tile limit, budgets from 0 past the prompt length."""
+    rng = np.random.default_rng(8000 + case)
+    B = int(rng.integers(1, 3))
+    Hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 4, 8]))
+    L = int(np.exp(rng.uniform(np.log(2), np.log(1500))))
+    w = int(rng.integers(1, min(L, 32 * (8 // G)) + 1))
+    n_layers = int(rng.integers(1, 4))
+    rules = [int(rng.choice([OP.H2O_FULL, OP.TOVA, OP.H2O, OP.SNAPKV], p=[0.35, 0.35, 0.15, 0.15]))
+             for _ in range(n_layers)]
+    budgets = []
+    for _ in range(n_layers):
+        kind = int(rng.integers(0, 7))
+        budgets.append([0, L, L + 3][kind] if kind < 3 else int(rng.integers(1, L + 1)))
+    print(f"case {case}: B{B} Hkv{Hkv} G{G} L{L} w{w} rules {rules} budgets {budgets}", flush=True)
+    layers = [[gen(40 + case, s, l, L, L if rules[l] == OP.H2O_FULL else w, G * Hkv, Hkv) for s in range(B)]
+              for l in range(n_layers)]
+    run_route(rules, budgets, layers, window=w, L=L)
